@@ -1,0 +1,204 @@
+/*
+ * hwkv.h -- C ABI of the HeadWiseKV grouped-cache runtime for MI355X (gfx950).
+ *
+ * HeadWiseKV gives every physical KV head (l, h) of a residual full-attention
+ * layer -- a "unit" -- a static history: full, or a recent window of w_lh
+ * tokens, chosen from a small codebook of window levels (paper: Method,
+ * "Structured Residency Model", the policy matrix a_lh over
+ * W = {w_1..w_K, full}).  The runtime stores that history as physical
+ * residency, not as a mask over a full cache (Method, "From Policy to
+ * Physical Residency"): storage is allocated per (window level, unit) before
+ * prefill, each unit reads and writes only its own slice, and the query heads
+ * of a GQA group read their shared KV-head slice; per-head outputs are
+ * concatenated before gating and the output projection.
+ *
+ * Residency of a finite unit with window w and S sink tokens, for a sequence
+ * of length n (positions 0..n-1):  R(n) = {p < S} U {p >= n - w}, of size
+ * min(n, S + w).  The window follows the paper's J_t(w) (Method, sequential
+ * calibration: positions t-w+1..t, the query's own token included); sinks
+ * are an additive prefix as in the paper's sink+recent control (Appendix,
+ * baseline controls: 4 sinks + 90,364 recent = a 90,368-token cache).
+ * S = 0 is exactly the paper's suffix window.  A window with S + w >= max_ctx
+ * is full ("any w >= C is equivalent to full").
+ *
+ * Physical slot of position p in its unit: p for full units and sinks,
+ * S + ((p - S) mod w) otherwise (a ring).  After any sequence of calls the
+ * occupied slots of a (unit, sequence) are exactly [0, min(n, cap)).
+ *
+ * Conventions for every entry point:
+ *   - returns HWKV_OK (0) or one of the positive error codes below; on error no
+ *     state changes and hwkv_last_error() describes the failure;
+ *   - all validation happens on the host before any device work;
+ *   - handles are opaque; hwkv_policy_set copies its arrays and
+ *     hwkv_cache_alloc copies the policy (the policy may be freed after);
+ *   - device pointers (k, v, q, out, workspace, dev_buf) are caller-owned
+ *     device memory, 16-byte aligned, contiguous; the library never frees
+ *     them.  bf16 tensors are passed as raw 16-bit bf16 storage;
+ *   - `stream` is a borrowed hipStream_t passed as void* (NULL = the null
+ *     stream); device work is enqueued on it asynchronously and launch errors
+ *     are reported as HWKV_EDEVICE;
+ *   - a cache is not thread-safe: calls on one cache must be serialised, and
+ *     the host keeps the sequence lengths, so calls on one cache must be
+ *     issued in the order the device should execute them.
+ */
+#ifndef HWKV_H
+#define HWKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define HWKV_OK 0
+#define HWKV_EINVAL 1    /* invalid argument */
+#define HWKV_ENOMEM 2    /* host or device memory, or a too-small buffer */
+#define HWKV_ECAPACITY 3 /* a full unit would exceed max_ctx */
+#define HWKV_ESTATE 4    /* call does not match the cache state */
+#define HWKV_EDEVICE 5   /* HIP runtime or launch error */
+
+typedef struct hwkv_policy hwkv_policy;
+typedef struct hwkv_cache hwkv_cache;
+
+/* Text of the last error raised on the calling thread ("" if none).  The
+ * pointer stays valid until the next call on that thread. */
+const char *hwkv_last_error(void);
+
+/* ------------------------------------------------------------------------ */
+/* Policy: the static layer x KV-head matrix over a window codebook         */
+/* (Method, "Structured Residency Model"; Appendix, runtime realization:    */
+/* the matrix is loaded once and never recomputed from the prompt).         */
+/* ------------------------------------------------------------------------ */
+
+/* Create a policy.
+ *   n_layers, n_kv_heads  units are (layer, kv_head), layer-major;
+ *                         1 <= n_kv_heads <= 64
+ *   n_q_heads             multiple of n_kv_heads; query head q reads KV head
+ *                         q / (n_q_heads / n_kv_heads) (contiguous GQA
+ *                         groups); group size 1, 2, 4, 6 or 8
+ *   head_dim              64, 128 or 256 (K and V share it)
+ *   n_sinks               S >= 0, shared by all finite units
+ *   n_levels              codebook size K + 1 (>= 1)
+ *   level_window[k]       window of level k: > 0 finite, 0 = full history
+ *   level_of_unit[u]      level index of unit u = layer * n_kv_heads + h
+ * Units with the same level form one storage group (same capacity, disjoint
+ * contents).  EINVAL on any out-of-range value. */
+int hwkv_policy_set(hwkv_policy **out, int32_t n_layers, int32_t n_kv_heads,
+                    int32_t n_q_heads, int32_t head_dim, int32_t n_sinks,
+                    int32_t n_levels, const int64_t *level_window,
+                    const int32_t *level_of_unit);
+
+int hwkv_policy_free(hwkv_policy *policy);
+
+/* Nominal K/V bytes of the policy at context ctx (Eq. nominal-storage with
+ * bf16 K and V: r_C(w) * head_dim * (2 + 2) per unit and sequence, where
+ * r_C(w) = min(S + w, ctx) for a finite window and ctx for full). */
+int hwkv_policy_bytes(const hwkv_policy *policy, int64_t ctx, double *bytes);
+
+/* Normalized rate R_C (Eq. normalized-rate): nominal bytes divided by the
+ * all-full policy's nominal bytes at the same ctx.  Host only. */
+int hwkv_policy_rate(const hwkv_policy *policy, int64_t ctx, double *rate);
+
+/* ------------------------------------------------------------------------ */
+/* Cache: grouped physical storage allocated before prefill                  */
+/* (Method, "From Policy to Physical Residency"; Appendix, physical cache    */
+/* realization: per-(window, KV head) groups, disjoint per-layer contents).  */
+/* ------------------------------------------------------------------------ */
+
+/* Exact device bytes hwkv_cache_alloc needs for `batch` sequences of at most
+ * max_ctx tokens: per unit and sequence, cap rounded up to a multiple of 64
+ * token rows (the K tile), times head_dim * (2 + 2) bytes, where cap = max_ctx
+ * for full units (or S + w >= max_ctx) and S + w otherwise.  Equals
+ * batch x Eq. nominal-storage at ctx = max_ctx up to that rounding.
+ * 1 <= max_ctx <= 2^31 - 128.  EINVAL on overflow. */
+int hwkv_cache_bytes(const hwkv_policy *policy, int32_t batch, int64_t max_ctx,
+                     size_t *bytes);
+
+/* Allocate a cache.  dev_buf == NULL: the library allocates (hipMalloc on the
+ * current device), zero-fills, and owns the memory.  Otherwise the caller's
+ * device buffer of buf_bytes is adopted as is (ENOMEM if smaller than
+ * hwkv_cache_bytes); it must stay valid until hwkv_cache_free.  Every
+ * sequence length starts at 0. */
+int hwkv_cache_alloc(hwkv_cache **out, const hwkv_policy *policy,
+                     int32_t batch, int64_t max_ctx, void *dev_buf,
+                     size_t buf_bytes);
+
+/* Release the cache; frees device memory only if the library allocated it.
+ * The caller must make sure no enqueued work still uses the cache. */
+int hwkv_cache_free(hwkv_cache *cache);
+
+/* Host mirror of the length n of sequence `seq` in `layer`. */
+int hwkv_cache_seq_len(const hwkv_cache *cache, int32_t layer, int32_t seq,
+                       int64_t *n);
+
+/* Capacity (token rows holding data, before tile rounding) of unit
+ * (layer, kv_head) per sequence, and its window after canonicalisation
+ * (0 = full). */
+int hwkv_cache_unit_info(const hwkv_cache *cache, int32_t layer,
+                         int32_t kv_head, int64_t *capacity, int64_t *window);
+
+/* ------------------------------------------------------------------------ */
+/* Data path                                                                 */
+/* ------------------------------------------------------------------------ */
+
+/* Prefill materialisation of tokens [pos0, pos0 + n_tokens) of sequence
+ * `seq` in `layer`: only positions still retained once the sequence has
+ * length pos0 + n_tokens are written, each into its slot; no full-length
+ * cache is ever formed (Method, physical residency; Intro: storage shrinks
+ * before the cache is built).  Then n(layer, seq) = pos0 + n_tokens.
+ *   k, v   device bf16 [n_tokens][n_kv_heads][head_dim], post-RoPE keys.
+ * ESTATE if pos0 != n(layer, seq); ECAPACITY if a full unit would pass
+ * max_ctx; n_tokens == 0 is a no-op. */
+int hwkv_prefill_write(hwkv_cache *cache, int32_t layer, int32_t seq,
+                       int64_t pos0, int64_t n_tokens, const void *k,
+                       const void *v, void *stream);
+
+/* Append one token to every sequence of `layer`: token n_b of sequence b
+ * goes to slot(n_b) of each unit (once n_b >= S + w this overwrites token
+ * n_b - w, the one leaving the window), then n_b += 1.
+ *   k_new, v_new   device bf16 [batch][n_kv_heads][head_dim].
+ * ECAPACITY if a full unit of the layer already holds max_ctx tokens. */
+int hwkv_append(hwkv_cache *cache, int32_t layer, const void *k_new,
+                const void *v_new, void *stream);
+
+/* Workspace bytes hwkv_decode_attn / hwkv_append_decode_attn need for any
+ * layer at any length up to max_ctx (split partials). */
+int hwkv_decode_workspace_bytes(const hwkv_cache *cache, size_t *bytes);
+
+/* Decode attention of `layer` over the current residency (Eqs.
+ * conditional-attention-weight and conditional-attention with the exact
+ * scaled dot product z = scale * q.k): for sequence b and query head qh,
+ * out = sum_s softmax_s(z) v_s over the tokens resident in KV head
+ * qh / G, i.e. R(n_b) -- call after hwkv_append for the query's own token.
+ *   q     device bf16 [batch][n_q_heads][head_dim]
+ *   out   device fp32 [batch][n_q_heads][head_dim] (pre-gate, heads
+ *         concatenated)
+ *   ws    device workspace of ws_bytes >= hwkv_decode_workspace_bytes
+ * EINVAL if a sequence is empty or the workspace is short.  Does not change
+ * state.  Fp32 accumulation; the result does not depend on the slot order. */
+int hwkv_decode_attn(hwkv_cache *cache, int32_t layer, const void *q,
+                     float scale, void *out, void *ws, size_t ws_bytes,
+                     void *stream);
+
+/* hwkv_append followed by hwkv_decode_attn, in one pass over the cache: the
+ * new token is attended from k_new/v_new and written to its slot by the same
+ * kernel.  Same arguments, errors and result as the two calls in sequence. */
+int hwkv_append_decode_attn(hwkv_cache *cache, int32_t layer,
+                            const void *k_new, const void *v_new,
+                            const void *q, float scale, void *out, void *ws,
+                            size_t ws_bytes, void *stream);
+
+/* Test hook: synchronously copy unit (layer, kv_head) of sequence `seq` to
+ * the host after all device work completes.  host_k, host_v receive
+ * [capacity][head_dim] bf16 in slot order; *n_valid = min(n, capacity), the
+ * number of occupied slots.  Slots >= n_valid hold unspecified values. */
+int hwkv_cache_read_unit(const hwkv_cache *cache, int32_t layer,
+                         int32_t kv_head, int32_t seq, void *host_k,
+                         void *host_v, int64_t *n_valid);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HWKV_H */

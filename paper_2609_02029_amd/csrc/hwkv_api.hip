@@ -1,0 +1,604 @@
+// hwkv_api.hip -- host side of the C ABI declared in include/hwkv.h:
+// policy validation and accounting, grouped-cache layout and allocation, the
+// host mirror of sequence lengths, argument validation (always before any
+// device work, no state change on error), and the per-call work tables the
+// kernels consume.
+#include "hwkv.h"
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "hwkv_internal.h"
+
+struct hwkv_policy {
+  int32_t n_layers = 0, n_kv_heads = 0, n_q_heads = 0, head_dim = 0;
+  int32_t n_sinks = 0, n_levels = 0;
+  std::vector<int64_t> level_window;  // 0 = full
+  std::vector<int32_t> level_of_unit; // [n_layers * n_kv_heads]
+};
+
+struct hwkv_cache {
+  hwkv_policy pol;
+  int32_t batch = 0;
+  int64_t max_ctx = 0;
+  // per unit u = layer * n_kv_heads + h
+  std::vector<int64_t> window;   // canonical: 0 = full (incl. S + w >= max_ctx)
+  std::vector<int64_t> cap;      // rows holding data
+  std::vector<int64_t> cap_pad;  // rows allocated (multiple of 64)
+  std::vector<int64_t> k_off;    // element offset of (u, seq 0); seq stride
+  std::vector<int64_t> v_off;    //   is cap_pad * head_dim
+  std::vector<int64_t> n;        // [layer * batch + b] sequence lengths
+  uint16_t *base = nullptr;
+  size_t bytes = 0;
+  bool owned = false;
+  size_t ws_bytes = 0;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string &msg) {
+  g_err = msg;
+  return code;
+}
+
+int ok() {
+  g_err.clear();
+  return HWKV_OK;
+}
+
+bool valid_group(int g) {
+  return g == 1 || g == 2 || g == 4 || g == 6 || g == 8;
+}
+
+int64_t round_tile(int64_t x) {
+  return (x + hwkv::kTile - 1) / hwkv::kTile * hwkv::kTile;
+}
+
+// Canonical window and capacity of a finite or full unit at max_ctx.
+void unit_shape(const hwkv_policy &p, int32_t u, int64_t max_ctx,
+                int64_t *window, int64_t *cap) {
+  const int64_t w = p.level_window[p.level_of_unit[u]];
+  if (w == 0 || (int64_t)p.n_sinks + w >= max_ctx) {
+    *window = 0;
+    *cap = max_ctx;
+  } else {
+    *window = w;
+    *cap = p.n_sinks + w;
+  }
+}
+
+// Lays out the grouped pools; fills per-unit vectors when `c` is non-null.
+int layout(const hwkv_policy &p, int32_t batch, int64_t max_ctx, size_t *bytes,
+           hwkv_cache *c) {
+  if (batch < 1) return fail(HWKV_EINVAL, "batch must be >= 1");
+  if (max_ctx < 1 || max_ctx > (int64_t(1) << 31) - 128)
+    return fail(HWKV_EINVAL, "max_ctx must be in [1, 2^31 - 128]");
+  const int32_t U = p.n_layers * p.n_kv_heads;
+  const uint64_t D = (uint64_t)p.head_dim;
+  std::vector<int64_t> win(U), cap(U), capp(U), koff(U), voff(U);
+  for (int32_t u = 0; u < U; ++u) {
+    unit_shape(p, u, max_ctx, &win[u], &cap[u]);
+    capp[u] = round_tile(cap[u]);
+  }
+  // [level][unit in level][seq] K regions, then the V regions of the level
+  uint64_t off = 0;  // elements
+  auto mul_ok = [&](uint64_t a, uint64_t b, uint64_t *r) {
+    return !__builtin_mul_overflow(a, b, r);
+  };
+  for (int32_t lv = 0; lv < p.n_levels; ++lv) {
+    for (int pass = 0; pass < 2; ++pass) {
+      for (int32_t u = 0; u < U; ++u) {
+        if (p.level_of_unit[u] != lv) continue;
+        uint64_t region;
+        if (!mul_ok((uint64_t)capp[u] * D, (uint64_t)batch, &region) ||
+            __builtin_add_overflow(off, region, &off) ||
+            off > (uint64_t)INT64_MAX / 4)
+          return fail(HWKV_EINVAL, "cache size overflows");
+        (pass == 0 ? koff : voff)[u] = (int64_t)(off - region);
+      }
+    }
+  }
+  *bytes = (size_t)(off * 2);
+  if (c) {
+    c->window = win;
+    c->cap = cap;
+    c->cap_pad = capp;
+    c->k_off = koff;
+    c->v_off = voff;
+  }
+  return HWKV_OK;
+}
+
+int64_t group_size(const hwkv_policy &p) { return p.n_q_heads / p.n_kv_heads; }
+
+// Splits needed by one (unit, seq) item with n_valid rows.
+int64_t splits_for(int64_t n_valid) {
+  const int64_t t = hwkv::decode_split_tokens();
+  return (n_valid + t - 1) / t;
+}
+
+size_t partial_bytes(const hwkv_policy &p) {
+  return (size_t)group_size(p) * (size_t)(p.head_dim + 2) * sizeof(float);
+}
+
+int64_t &seq_len(hwkv_cache *c, int32_t layer, int32_t b) {
+  return c->n[(size_t)layer * c->batch + b];
+}
+
+int64_t slot_of(const hwkv_cache *c, int32_t u, int64_t pos) {
+  const int64_t w = c->window[u];
+  const int64_t S = c->pol.n_sinks;
+  if (w == 0 || pos < S) return pos;
+  return S + (pos - S) % w;
+}
+
+int check_device(hipError_t e, const char *what) {
+  if (e == hipSuccess) return HWKV_OK;
+  return fail(HWKV_EDEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+// Shared validation of a decode call; fills per-item lengths.
+int decode_impl(hwkv_cache *c, int32_t layer, const void *k_new,
+                const void *v_new, const void *q, float scale, void *out,
+                void *ws, size_t ws_bytes, void *stream, bool fused) {
+  if (!c) return fail(HWKV_EINVAL, "cache is null");
+  const hwkv_policy &p = c->pol;
+  if (layer < 0 || layer >= p.n_layers)
+    return fail(HWKV_EINVAL, "layer out of range");
+  if (!q || !out) return fail(HWKV_EINVAL, "q and out must be non-null");
+  if (fused && (!k_new || !v_new))
+    return fail(HWKV_EINVAL, "k_new and v_new must be non-null");
+  if (!std::isfinite(scale)) return fail(HWKV_EINVAL, "scale must be finite");
+  const int32_t H = p.n_kv_heads, B = c->batch;
+  const int G = (int)group_size(p);
+  // item lengths
+  const int n_items_total = B * H;
+  std::vector<int32_t> nv(n_items_total), ns(n_items_total), nslot(n_items_total);
+  int64_t total_splits = 0;
+  for (int32_t b = 0; b < B; ++b) {
+    const int64_t n = seq_len(c, layer, b);
+    for (int32_t h = 0; h < H; ++h) {
+      const int32_t u = layer * H + h;
+      int64_t len = n;
+      int32_t s_new = -1;
+      if (fused) {
+        if (c->window[u] == 0 && n >= c->cap[u])
+          return fail(HWKV_ECAPACITY, "append past max_ctx on a full unit");
+        s_new = (int32_t)slot_of(c, u, n);
+        len = n + 1;
+      } else if (n == 0) {
+        return fail(HWKV_EINVAL, "decode on an empty sequence");
+      }
+      const int i = b * H + h;
+      nv[i] = (int32_t)std::min(len, c->cap[u]);
+      ns[i] = (int32_t)splits_for(nv[i]);
+      nslot[i] = s_new;
+      total_splits += ns[i];
+    }
+  }
+  const size_t need = (size_t)total_splits * partial_bytes(p);
+  if (!ws || ws_bytes < need)
+    return fail(HWKV_EINVAL, "workspace missing or too small (need " +
+                                 std::to_string(need) + " bytes)");
+  // launches of at most kMaxItems items
+  const hipStream_t s = (hipStream_t)stream;
+  int ws_split = 0;
+  for (int i0 = 0; i0 < n_items_total; i0 += hwkv::kMaxItems) {
+    const int cnt = std::min(hwkv::kMaxItems, n_items_total - i0);
+    hwkv::DecodeArgs a;
+    std::memset(&a, 0, sizeof a);
+    int splits = 0;
+    for (int j = 0; j < cnt; ++j) {
+      const int i = i0 + j;
+      const int32_t b = i / H, h = i % H;
+      const int32_t u = layer * H + h;
+      const int64_t seq_off = (int64_t)b * c->cap_pad[u] * p.head_dim;
+      a.it.k_off[j] = c->k_off[u] + seq_off;
+      a.it.v_off[j] = c->v_off[u] + seq_off;
+      a.it.n_valid[j] = nv[i];
+      a.it.new_slot[j] = nslot[i];
+      a.it.q_row[j] = b * p.n_q_heads + h * G;
+      a.it.kv_row[j] = b * H + h;
+      a.it.split_begin[j] = splits;
+      splits += ns[i];
+    }
+    a.it.split_begin[cnt] = splits;
+    a.it.n_items = cnt;
+    a.it.ws_split0 = ws_split;
+    a.cache = c->base;
+    a.q = static_cast<const uint16_t *>(q);
+    a.k_new = static_cast<const uint16_t *>(k_new);
+    a.v_new = static_cast<const uint16_t *>(v_new);
+    a.out = static_cast<float *>(out);
+    a.ws = static_cast<float *>(ws);
+    a.scale_log2 = scale * 1.4426950408889634f;
+    const int n_combine = cnt * G * (p.head_dim / 64);
+    const int rc = check_device(
+        hwkv::launch_decode(p.head_dim, G, a, splits, n_combine, s),
+        "decode launch");
+    if (rc != HWKV_OK) return rc;  // earlier launches of this call may run
+    ws_split += splits;
+  }
+  if (fused)
+    for (int32_t b = 0; b < B; ++b) seq_len(c, layer, b) += 1;
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *hwkv_last_error(void) { return g_err.c_str(); }
+
+int hwkv_policy_set(hwkv_policy **out, int32_t n_layers, int32_t n_kv_heads,
+                    int32_t n_q_heads, int32_t head_dim, int32_t n_sinks,
+                    int32_t n_levels, const int64_t *level_window,
+                    const int32_t *level_of_unit) {
+  if (!out) return fail(HWKV_EINVAL, "out is null");
+  *out = nullptr;
+  if (n_layers < 1) return fail(HWKV_EINVAL, "n_layers must be >= 1");
+  if (n_kv_heads < 1 || n_kv_heads > hwkv::kMaxItems)
+    return fail(HWKV_EINVAL, "n_kv_heads must be in [1, 64]");
+  if (n_q_heads < 1 || n_q_heads % n_kv_heads != 0)
+    return fail(HWKV_EINVAL, "n_q_heads must be a multiple of n_kv_heads");
+  if (!valid_group(n_q_heads / n_kv_heads))
+    return fail(HWKV_EINVAL, "GQA group size must be 1, 2, 4, 6 or 8");
+  if (head_dim != 64 && head_dim != 128 && head_dim != 256)
+    return fail(HWKV_EINVAL, "head_dim must be 64, 128 or 256");
+  if (n_sinks < 0) return fail(HWKV_EINVAL, "n_sinks must be >= 0");
+  if (n_levels < 1) return fail(HWKV_EINVAL, "n_levels must be >= 1");
+  if (!level_window || !level_of_unit)
+    return fail(HWKV_EINVAL, "level arrays must be non-null");
+  if ((int64_t)n_layers * n_kv_heads > (int64_t(1) << 24))
+    return fail(HWKV_EINVAL, "too many units");
+  for (int32_t k = 0; k < n_levels; ++k)
+    if (level_window[k] < 0)
+      return fail(HWKV_EINVAL, "level windows must be > 0 (or 0 for full)");
+  const int32_t U = n_layers * n_kv_heads;
+  for (int32_t u = 0; u < U; ++u)
+    if (level_of_unit[u] < 0 || level_of_unit[u] >= n_levels)
+      return fail(HWKV_EINVAL, "level index out of range");
+  try {
+    hwkv_policy *p = new hwkv_policy;
+    p->n_layers = n_layers;
+    p->n_kv_heads = n_kv_heads;
+    p->n_q_heads = n_q_heads;
+    p->head_dim = head_dim;
+    p->n_sinks = n_sinks;
+    p->n_levels = n_levels;
+    p->level_window.assign(level_window, level_window + n_levels);
+    p->level_of_unit.assign(level_of_unit, level_of_unit + U);
+    *out = p;
+  } catch (const std::bad_alloc &) {
+    return fail(HWKV_ENOMEM, "host allocation failed");
+  }
+  return ok();
+}
+
+int hwkv_policy_free(hwkv_policy *policy) {
+  delete policy;
+  return ok();
+}
+
+int hwkv_policy_bytes(const hwkv_policy *p, int64_t ctx, double *bytes) {
+  if (!p || !bytes) return fail(HWKV_EINVAL, "null argument");
+  if (ctx < 1) return fail(HWKV_EINVAL, "ctx must be >= 1");
+  double tot = 0.0;
+  const double row = (double)p->head_dim * (2.0 + 2.0);
+  for (int32_t lv : p->level_of_unit) {
+    const int64_t w = p->level_window[lv];
+    const int64_t r = (w == 0) ? ctx : std::min<int64_t>(p->n_sinks + w, ctx);
+    tot += (double)r * row;
+  }
+  *bytes = tot;
+  return ok();
+}
+
+int hwkv_policy_rate(const hwkv_policy *p, int64_t ctx, double *rate) {
+  if (!p || !rate) return fail(HWKV_EINVAL, "null argument");
+  double b = 0.0;
+  const int rc = hwkv_policy_bytes(p, ctx, &b);
+  if (rc != HWKV_OK) return rc;
+  const double full = (double)p->level_of_unit.size() * (double)ctx *
+                      (double)p->head_dim * 4.0;
+  *rate = b / full;
+  return ok();
+}
+
+int hwkv_cache_bytes(const hwkv_policy *p, int32_t batch, int64_t max_ctx,
+                     size_t *bytes) {
+  if (!p || !bytes) return fail(HWKV_EINVAL, "null argument");
+  const int rc = layout(*p, batch, max_ctx, bytes, nullptr);
+  return rc == HWKV_OK ? ok() : rc;
+}
+
+int hwkv_cache_alloc(hwkv_cache **out, const hwkv_policy *p, int32_t batch,
+                     int64_t max_ctx, void *dev_buf, size_t buf_bytes) {
+  if (!out || !p) return fail(HWKV_EINVAL, "null argument");
+  *out = nullptr;
+  hwkv_cache *c = nullptr;
+  try {
+    c = new hwkv_cache;
+    c->pol = *p;
+    c->batch = batch;
+    c->max_ctx = max_ctx;
+    size_t bytes = 0;
+    int rc = layout(*p, batch, max_ctx, &bytes, c);
+    if (rc != HWKV_OK) {
+      delete c;
+      return rc;
+    }
+    c->bytes = bytes;
+    c->n.assign((size_t)p->n_layers * batch, 0);
+    // workspace: worst layer at full capacity
+    size_t ws = 0;
+    for (int32_t l = 0; l < p->n_layers; ++l) {
+      int64_t sp = 0;
+      for (int32_t h = 0; h < p->n_kv_heads; ++h)
+        sp += splits_for(c->cap[l * p->n_kv_heads + h]);
+      ws = std::max(ws, (size_t)(sp * batch) * partial_bytes(*p));
+    }
+    c->ws_bytes = ws;
+    if (dev_buf) {
+      if (buf_bytes < bytes) {
+        delete c;
+        return fail(HWKV_ENOMEM, "device buffer smaller than cache bytes (" +
+                                     std::to_string(bytes) + ")");
+      }
+      c->base = static_cast<uint16_t *>(dev_buf);
+      c->owned = false;
+    } else {
+      void *ptr = nullptr;
+      hipError_t e = hipMalloc(&ptr, bytes ? bytes : 256);
+      if (e != hipSuccess) {
+        delete c;
+        (void)hipGetLastError();
+        return fail(e == hipErrorOutOfMemory ? HWKV_ENOMEM : HWKV_EDEVICE,
+                    std::string("hipMalloc: ") + hipGetErrorString(e));
+      }
+      e = hipMemset(ptr, 0, bytes);
+      if (e != hipSuccess) {
+        (void)hipFree(ptr);
+        delete c;
+        return fail(HWKV_EDEVICE, std::string("hipMemset: ") + hipGetErrorString(e));
+      }
+      c->base = static_cast<uint16_t *>(ptr);
+      c->owned = true;
+    }
+  } catch (const std::bad_alloc &) {
+    delete c;
+    return fail(HWKV_ENOMEM, "host allocation failed");
+  }
+  *out = c;
+  return ok();
+}
+
+int hwkv_cache_free(hwkv_cache *c) {
+  if (!c) return ok();
+  int rc = HWKV_OK;
+  if (c->owned && c->base) {
+    hipError_t e = hipFree(c->base);
+    if (e != hipSuccess) rc = check_device(e, "hipFree");
+  }
+  delete c;
+  return rc == HWKV_OK ? ok() : rc;
+}
+
+int hwkv_cache_seq_len(const hwkv_cache *c, int32_t layer, int32_t seq,
+                       int64_t *n) {
+  if (!c || !n) return fail(HWKV_EINVAL, "null argument");
+  if (layer < 0 || layer >= c->pol.n_layers || seq < 0 || seq >= c->batch)
+    return fail(HWKV_EINVAL, "layer or seq out of range");
+  *n = c->n[(size_t)layer * c->batch + seq];
+  return ok();
+}
+
+int hwkv_cache_unit_info(const hwkv_cache *c, int32_t layer, int32_t kv_head,
+                         int64_t *capacity, int64_t *window) {
+  if (!c || !capacity || !window) return fail(HWKV_EINVAL, "null argument");
+  if (layer < 0 || layer >= c->pol.n_layers || kv_head < 0 ||
+      kv_head >= c->pol.n_kv_heads)
+    return fail(HWKV_EINVAL, "layer or kv_head out of range");
+  const int32_t u = layer * c->pol.n_kv_heads + kv_head;
+  *capacity = c->cap[u];
+  *window = c->window[u];
+  return ok();
+}
+
+int hwkv_prefill_write(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0,
+                       int64_t n_tokens, const void *k, const void *v,
+                       void *stream) {
+  if (!c) return fail(HWKV_EINVAL, "cache is null");
+  const hwkv_policy &p = c->pol;
+  if (layer < 0 || layer >= p.n_layers || seq < 0 || seq >= c->batch)
+    return fail(HWKV_EINVAL, "layer or seq out of range");
+  if (n_tokens < 0) return fail(HWKV_EINVAL, "n_tokens must be >= 0");
+  if (pos0 != seq_len(c, layer, seq))
+    return fail(HWKV_ESTATE, "pos0 " + std::to_string(pos0) +
+                                 " != sequence length " +
+                                 std::to_string(seq_len(c, layer, seq)));
+  if (n_tokens == 0) return ok();
+  if (!k || !v) return fail(HWKV_EINVAL, "k and v must be non-null");
+  const int64_t p0 = pos0, p1 = pos0 + n_tokens;
+  const int32_t H = p.n_kv_heads;
+  const int64_t S = p.n_sinks;
+  for (int32_t h = 0; h < H; ++h) {
+    const int32_t u = layer * H + h;
+    if (c->window[u] == 0 && p1 > c->cap[u])
+      return fail(HWKV_ECAPACITY, "prefill past max_ctx on a full unit");
+  }
+  hwkv::WriteArgs a;
+  std::memset(&a, 0, sizeof a);
+  int max_tiles = 0;
+  for (int32_t h = 0; h < H; ++h) {
+    const int32_t u = layer * H + h;
+    const int64_t w = c->window[u];
+    const int64_t seq_off = (int64_t)seq * c->cap_pad[u] * p.head_dim;
+    hwkv::WriteHead &wh = a.head[h];
+    wh.k_off = c->k_off[u] + seq_off;
+    wh.v_off = c->v_off[u] + seq_off;
+    wh.window = w;
+    // slot ranges [lo, hi) written by this chunk
+    std::vector<std::pair<int64_t, int64_t>> sr;
+    if (w == 0) {
+      sr.push_back({p0, p1});
+    } else {
+      if (p0 < S) sr.push_back({p0, std::min(p1, S)});
+      const int64_t start = std::max({p0, p1 - w, S});
+      if (start < p1) {
+        const int64_t cnt = p1 - start;
+        const int64_t f = S + (start - S) % w;
+        if (f + cnt <= S + w) {
+          sr.push_back({f, f + cnt});
+        } else {
+          sr.push_back({f, S + w});
+          sr.push_back({S, S + (f + cnt - (S + w))});
+        }
+      }
+    }
+    // to tile ranges, merged
+    std::vector<std::pair<int64_t, int64_t>> tr;
+    for (auto &r : sr)
+      tr.push_back({r.first / hwkv::kTile, (r.second - 1) / hwkv::kTile + 1});
+    std::sort(tr.begin(), tr.end());
+    std::vector<std::pair<int64_t, int64_t>> merged;
+    for (auto &r : tr) {
+      if (!merged.empty() && r.first <= merged.back().second)
+        merged.back().second = std::max(merged.back().second, r.second);
+      else
+        merged.push_back(r);
+    }
+    int tot = 0;
+    for (size_t r = 0; r < merged.size() && r < 3; ++r) {
+      wh.tile0[r] = (int32_t)merged[r].first;
+      wh.n_tiles[r] = (int32_t)(merged[r].second - merged[r].first);
+      tot += wh.n_tiles[r];
+    }
+    max_tiles = std::max(max_tiles, tot);
+  }
+  a.cache = c->base;
+  a.k = static_cast<const uint16_t *>(k);
+  a.v = static_cast<const uint16_t *>(v);
+  a.p0 = p0;
+  a.p1 = p1;
+  a.n_kv_heads = H;
+  a.n_sinks = p.n_sinks;
+  if (max_tiles > 0) {
+    const int rc = check_device(
+        hwkv::launch_prefill_write(p.head_dim, a, max_tiles, (hipStream_t)stream),
+        "prefill_write launch");
+    if (rc != HWKV_OK) return rc;
+  }
+  seq_len(c, layer, seq) = p1;
+  return ok();
+}
+
+int hwkv_append(hwkv_cache *c, int32_t layer, const void *k_new,
+                const void *v_new, void *stream) {
+  if (!c) return fail(HWKV_EINVAL, "cache is null");
+  const hwkv_policy &p = c->pol;
+  if (layer < 0 || layer >= p.n_layers)
+    return fail(HWKV_EINVAL, "layer out of range");
+  if (!k_new || !v_new) return fail(HWKV_EINVAL, "k_new and v_new must be non-null");
+  const int32_t H = p.n_kv_heads, B = c->batch;
+  for (int32_t b = 0; b < B; ++b)
+    for (int32_t h = 0; h < H; ++h) {
+      const int32_t u = layer * H + h;
+      if (c->window[u] == 0 && seq_len(c, layer, b) >= c->cap[u])
+        return fail(HWKV_ECAPACITY, "append past max_ctx on a full unit");
+    }
+  const int total = B * H;
+  for (int i0 = 0; i0 < total; i0 += hwkv::kMaxItems) {
+    const int cnt = std::min(hwkv::kMaxItems, total - i0);
+    hwkv::AppendArgs a;
+    std::memset(&a, 0, sizeof a);
+    for (int j = 0; j < cnt; ++j) {
+      const int i = i0 + j;
+      const int32_t b = i / H, h = i % H;
+      const int32_t u = layer * H + h;
+      const int64_t seq_off = (int64_t)b * c->cap_pad[u] * p.head_dim;
+      a.k_off[j] = c->k_off[u] + seq_off;
+      a.v_off[j] = c->v_off[u] + seq_off;
+      a.slot[j] = (int32_t)slot_of(c, u, seq_len(c, layer, b));
+      a.kv_row[j] = b * H + h;
+    }
+    a.n_items = cnt;
+    a.cache = c->base;
+    a.k_new = static_cast<const uint16_t *>(k_new);
+    a.v_new = static_cast<const uint16_t *>(v_new);
+    const int rc = check_device(
+        hwkv::launch_append(p.head_dim, a, (hipStream_t)stream), "append launch");
+    if (rc != HWKV_OK) return rc;
+  }
+  for (int32_t b = 0; b < B; ++b) seq_len(c, layer, b) += 1;
+  return ok();
+}
+
+int hwkv_decode_workspace_bytes(const hwkv_cache *c, size_t *bytes) {
+  if (!c || !bytes) return fail(HWKV_EINVAL, "null argument");
+  *bytes = c->ws_bytes;
+  return ok();
+}
+
+int hwkv_decode_attn(hwkv_cache *c, int32_t layer, const void *q, float scale,
+                     void *out, void *ws, size_t ws_bytes, void *stream) {
+  return decode_impl(c, layer, nullptr, nullptr, q, scale, out, ws, ws_bytes,
+                     stream, false);
+}
+
+int hwkv_append_decode_attn(hwkv_cache *c, int32_t layer, const void *k_new,
+                            const void *v_new, const void *q, float scale,
+                            void *out, void *ws, size_t ws_bytes,
+                            void *stream) {
+  return decode_impl(c, layer, k_new, v_new, q, scale, out, ws, ws_bytes,
+                     stream, true);
+}
+
+int hwkv_cache_read_unit(const hwkv_cache *c, int32_t layer, int32_t kv_head,
+                         int32_t seq, void *host_k, void *host_v,
+                         int64_t *n_valid) {
+  if (!c || !host_k || !host_v || !n_valid)
+    return fail(HWKV_EINVAL, "null argument");
+  const hwkv_policy &p = c->pol;
+  if (layer < 0 || layer >= p.n_layers || kv_head < 0 ||
+      kv_head >= p.n_kv_heads || seq < 0 || seq >= c->batch)
+    return fail(HWKV_EINVAL, "layer, kv_head or seq out of range");
+  const int32_t u = layer * p.n_kv_heads + kv_head;
+  const int64_t D = p.head_dim, cap = c->cap[u], capp = c->cap_pad[u];
+  const int64_t seq_off = (int64_t)seq * capp * D;
+  std::vector<uint16_t> tiles;
+  try {
+    tiles.resize((size_t)(capp * D));
+  } catch (const std::bad_alloc &) {
+    return fail(HWKV_ENOMEM, "host allocation failed");
+  }
+  int rc = check_device(hipDeviceSynchronize(), "synchronize");
+  if (rc != HWKV_OK) return rc;
+  rc = check_device(hipMemcpy(tiles.data(), c->base + c->k_off[u] + seq_off,
+                              (size_t)(capp * D) * 2, hipMemcpyDeviceToHost),
+                    "copy K");
+  if (rc != HWKV_OK) return rc;
+  rc = check_device(hipMemcpy(host_v, c->base + c->v_off[u] + seq_off,
+                              (size_t)(cap * D) * 2, hipMemcpyDeviceToHost),
+                    "copy V");
+  if (rc != HWKV_OK) return rc;
+  // untile K: [tile][D/8][64][8] -> [slot][D]
+  uint16_t *hk = static_cast<uint16_t *>(host_k);
+  const int64_t NC = D / 8;
+  for (int64_t j = 0; j < cap; ++j) {
+    const int64_t t = j / hwkv::kTile, sl = j % hwkv::kTile;
+    for (int64_t g = 0; g < NC; ++g)
+      std::memcpy(hk + j * D + g * 8,
+                  tiles.data() + ((t * NC + g) * hwkv::kTile + sl) * 8, 16);
+  }
+  *n_valid = std::min(c->n[(size_t)layer * c->batch + seq], cap);
+  return ok();
+}
+
+}  // extern "C"

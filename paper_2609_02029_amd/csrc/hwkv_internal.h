@@ -1,0 +1,95 @@
+// hwkv_internal.h -- types shared by the host API and the gfx950 kernels.
+//
+// Device layout of one (unit, sequence) region, element type bf16:
+//   K: cap_pad / 64 tiles; tile t holds slots 64t .. 64t+63 as
+//      [head_dim / 8][64 slots][8 channels]   (16-byte chunks, slot-minor)
+//      so that a wavefront with one lane per slot reads 1 KiB contiguous per
+//      channel chunk (lane-per-token q.k without LDS staging or reductions).
+//   V: [cap_pad][head_dim] row-major, so that lanes owning channel slices
+//      read whole rows contiguously for the p * v accumulation.
+// cap_pad = cap rounded up to a multiple of 64.  Regions are grouped by
+// window level: for each level, the K regions of its units ([unit][seq]),
+// then their V regions.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace hwkv {
+
+constexpr int kTile = 64;        // token slots per K tile (= wavefront width)
+constexpr int kMaxItems = 64;    // (sequence, kv-head) items per launch
+
+// Decode work of one launch: items are (sequence b, kv head h) pairs of one
+// layer; item i owns splits [split_begin[i], split_begin[i + 1]) of the
+// launch and rows [0, n_valid[i]) of its unit.
+struct DecodeItems {
+  int64_t k_off[kMaxItems];      // element offset of the item's K tiles
+  int64_t v_off[kMaxItems];      // element offset of the item's V rows
+  int32_t n_valid[kMaxItems];    // occupied slots attended (>= 1)
+  int32_t new_slot[kMaxItems];   // slot taking the appended token, or -1
+  int32_t q_row[kMaxItems];      // b * n_q_heads + h * G (first q head)
+  int32_t kv_row[kMaxItems];     // b * n_kv_heads + h (row of k_new/v_new)
+  int32_t split_begin[kMaxItems + 1];
+  int32_t n_items;
+  int32_t ws_split0;             // first partial slot of this launch in ws
+};
+
+struct DecodeArgs {
+  DecodeItems it;
+  uint16_t *cache;               // cache base (bf16)
+  const uint16_t *q;             // [B][Hq][D]
+  const uint16_t *k_new;         // [B][Hkv][D] or null
+  const uint16_t *v_new;
+  float *out;                    // [B][Hq][D]
+  float *ws;                     // partials [split][G][2 + D]
+  float scale_log2;              // scale * log2(e)
+};
+
+// Materialisation of one chunk: for kv head h, the tiles listed in up to
+// three disjoint ranges [tile0[r], tile0[r] + n_tiles[r]).
+struct WriteHead {
+  int64_t k_off;                 // element offset of the (unit, seq) K tiles
+  int64_t v_off;                 // element offset of its V rows
+  int64_t window;                // 0 = full
+  int32_t tile0[3];
+  int32_t n_tiles[3];
+};
+
+struct WriteArgs {
+  WriteHead head[kMaxItems];     // one per kv head of the layer
+  uint16_t *cache;
+  const uint16_t *k;             // [n_tokens][Hkv][D]
+  const uint16_t *v;
+  int64_t p0, p1;                // chunk [p0, p1)
+  int32_t n_kv_heads;
+  int32_t n_sinks;
+};
+
+struct AppendArgs {
+  int64_t k_off[kMaxItems];
+  int64_t v_off[kMaxItems];
+  int32_t slot[kMaxItems];
+  int32_t kv_row[kMaxItems];
+  int32_t n_items;
+  uint16_t *cache;
+  const uint16_t *k_new;
+  const uint16_t *v_new;
+};
+
+// Launchers (return the launch status).  D in {64, 128, 256}; G in
+// {1, 2, 4, 6, 8}.
+hipError_t launch_decode(int D, int G, const DecodeArgs &a, int n_splits,
+                         int n_combine_blocks, hipStream_t s);
+int decode_split_tokens();       // tokens per split (a multiple of 64)
+hipError_t launch_prefill_write(int D, const WriteArgs &a, int max_tiles,
+                                hipStream_t s);
+hipError_t launch_append(int D, const AppendArgs &a, hipStream_t s);
+
+}  // namespace hwkv
+
+// Kernel arguments travel by value; the kernarg segment is limited to 4 KiB.
+static_assert(sizeof(hwkv::DecodeArgs) <= 4096, "decode kernarg too large");
+static_assert(sizeof(hwkv::WriteArgs) <= 4096, "write kernarg too large");
+static_assert(sizeof(hwkv::AppendArgs) <= 4096, "append kernarg too large");

@@ -1,0 +1,257 @@
+"""ctypes binding of ``libhwkv.so`` (the C ABI in ``include/hwkv.h``).
+
+Argument marshalling only: every step of the data path runs in the HIP
+kernels behind the C ABI.  Functions keep the C names without the ``hwkv_``
+prefix.  Device arguments are torch tensors on the GPU (bf16 inputs, fp32
+outputs, contiguous); ``stream`` defaults to torch's current stream.  There is
+no fallback: if the library is missing, importing this module raises.
+"""
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "_lib", "libhwkv.so")
+
+OK, EINVAL, ENOMEM, ECAPACITY, ESTATE, EDEVICE = 0, 1, 2, 3, 4, 5
+_NAMES = {EINVAL: "EINVAL", ENOMEM: "ENOMEM", ECAPACITY: "ECAPACITY",
+          ESTATE: "ESTATE", EDEVICE: "EDEVICE"}
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(
+        f"{LIB_PATH} is missing: build it with paper_2609_02029_amd.build.build() "
+        "(or __graft_entry__.build()) first")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+_i32, _i64, _dbl, _flt, _vp, _sz = (ctypes.c_int32, ctypes.c_int64, ctypes.c_double,
+                                     ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t)
+_P = ctypes.POINTER
+
+SYMBOLS = {
+    "hwkv_last_error": ([], ctypes.c_char_p),
+    "hwkv_policy_set": ([_P(_vp), _i32, _i32, _i32, _i32, _i32, _i32, _P(_i64), _P(_i32)], ctypes.c_int),
+    "hwkv_policy_free": ([_vp], ctypes.c_int),
+    "hwkv_policy_bytes": ([_vp, _i64, _P(_dbl)], ctypes.c_int),
+    "hwkv_policy_rate": ([_vp, _i64, _P(_dbl)], ctypes.c_int),
+    "hwkv_cache_bytes": ([_vp, _i32, _i64, _P(_sz)], ctypes.c_int),
+    "hwkv_cache_alloc": ([_P(_vp), _vp, _i32, _i64, _vp, _sz], ctypes.c_int),
+    "hwkv_cache_free": ([_vp], ctypes.c_int),
+    "hwkv_cache_seq_len": ([_vp, _i32, _i32, _P(_i64)], ctypes.c_int),
+    "hwkv_cache_unit_info": ([_vp, _i32, _i32, _P(_i64), _P(_i64)], ctypes.c_int),
+    "hwkv_prefill_write": ([_vp, _i32, _i32, _i64, _i64, _vp, _vp, _vp], ctypes.c_int),
+    "hwkv_append": ([_vp, _i32, _vp, _vp, _vp], ctypes.c_int),
+    "hwkv_decode_workspace_bytes": ([_vp, _P(_sz)], ctypes.c_int),
+    "hwkv_decode_attn": ([_vp, _i32, _vp, _flt, _vp, _vp, _sz, _vp], ctypes.c_int),
+    "hwkv_append_decode_attn": ([_vp, _i32, _vp, _vp, _vp, _flt, _vp, _vp, _sz, _vp], ctypes.c_int),
+    "hwkv_cache_read_unit": ([_vp, _i32, _i32, _i32, _vp, _vp, _P(_i64)], ctypes.c_int),
+}
+for _name, (_args, _res) in SYMBOLS.items():
+    _f = getattr(_lib, _name)
+    _f.argtypes = _args
+    _f.restype = _res
+
+
+class HwkvError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"{_NAMES.get(code, code)}: {msg}")
+        self.code = code
+
+
+def last_error():
+    return _lib.hwkv_last_error().decode()
+
+
+def _check(rc):
+    if rc != OK:
+        raise HwkvError(rc, last_error())
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _dev(t, dtype_name, what):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{what} must be a device tensor")
+    if str(t.dtype) != f"torch.{dtype_name}":
+        raise ValueError(f"{what} must be {dtype_name}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    return t.data_ptr()
+
+
+class Policy:
+    """Owns an ``hwkv_policy*``."""
+
+    def __init__(self, handle):
+        self.handle = handle
+
+    def __del__(self):
+        if getattr(self, "handle", None):
+            _lib.hwkv_policy_free(self.handle)
+            self.handle = None
+
+
+class Cache:
+    """Owns an ``hwkv_cache*`` (and keeps its policy's Python object alive)."""
+
+    def __init__(self, handle, n_layers, n_kv_heads, n_q_heads, head_dim, batch):
+        self.handle = handle
+        self.n_layers, self.n_kv_heads, self.n_q_heads = n_layers, n_kv_heads, n_q_heads
+        self.head_dim, self.batch = head_dim, batch
+
+    def free(self):
+        if getattr(self, "handle", None):
+            h, self.handle = self.handle, None
+            _check(_lib.hwkv_cache_free(h))
+
+    def __del__(self):
+        if getattr(self, "handle", None):
+            _lib.hwkv_cache_free(self.handle)
+            self.handle = None
+
+
+# ---------------------------------------------------------------------------
+# policy
+# ---------------------------------------------------------------------------
+def policy_set(n_layers, n_kv_heads, n_q_heads, head_dim, n_sinks, level_window,
+               level_of_unit):
+    lw = (_i64 * len(level_window))(*[int(x) for x in level_window])
+    flat = [int(x) for row in level_of_unit for x in (row if hasattr(row, "__len__") else [row])]
+    lu = (_i32 * max(1, len(flat)))(*flat)
+    h = _vp()
+    _check(_lib.hwkv_policy_set(ctypes.byref(h), n_layers, n_kv_heads, n_q_heads, head_dim,
+                                n_sinks, len(level_window), lw, lu))
+    p = Policy(h)
+    p.n_layers, p.n_kv_heads, p.n_q_heads, p.head_dim = n_layers, n_kv_heads, n_q_heads, head_dim
+    return p
+
+
+def policy_free(policy):
+    if policy.handle:
+        _check(_lib.hwkv_policy_free(policy.handle))
+        policy.handle = None
+
+
+def policy_bytes(policy, ctx):
+    r = _dbl()
+    _check(_lib.hwkv_policy_bytes(policy.handle, ctx, ctypes.byref(r)))
+    return r.value
+
+
+def policy_rate(policy, ctx):
+    r = _dbl()
+    _check(_lib.hwkv_policy_rate(policy.handle, ctx, ctypes.byref(r)))
+    return r.value
+
+
+# ---------------------------------------------------------------------------
+# cache
+# ---------------------------------------------------------------------------
+def cache_bytes(policy, batch, max_ctx):
+    r = _sz()
+    _check(_lib.hwkv_cache_bytes(policy.handle, batch, max_ctx, ctypes.byref(r)))
+    return r.value
+
+
+def cache_alloc(policy, batch, max_ctx, dev_buf=None):
+    """``dev_buf``: optional uint8 device tensor to adopt (kept alive)."""
+    h = _vp()
+    ptr = None
+    nbytes = 0
+    if dev_buf is not None:
+        ptr = _dev(dev_buf, "uint8", "dev_buf")
+        nbytes = dev_buf.numel()
+    _check(_lib.hwkv_cache_alloc(ctypes.byref(h), policy.handle, batch, max_ctx, ptr, nbytes))
+    c = Cache(h, policy.n_layers, policy.n_kv_heads, policy.n_q_heads, policy.head_dim, batch)
+    c.dev_buf = dev_buf
+    return c
+
+
+def cache_free(cache):
+    cache.free()
+
+
+def cache_seq_len(cache, layer, seq):
+    r = _i64()
+    _check(_lib.hwkv_cache_seq_len(cache.handle, layer, seq, ctypes.byref(r)))
+    return r.value
+
+
+def cache_unit_info(cache, layer, kv_head):
+    cap, win = _i64(), _i64()
+    _check(_lib.hwkv_cache_unit_info(cache.handle, layer, kv_head, ctypes.byref(cap),
+                                     ctypes.byref(win)))
+    return cap.value, win.value
+
+
+def cache_read_unit(cache, layer, kv_head, seq):
+    """Returns (k, v, n_valid): numpy uint16 [capacity, head_dim] bf16 bits."""
+    import numpy as np
+    cap, _ = cache_unit_info(cache, layer, kv_head)
+    k = np.empty((cap, cache.head_dim), dtype=np.uint16)
+    v = np.empty((cap, cache.head_dim), dtype=np.uint16)
+    nv = _i64()
+    _check(_lib.hwkv_cache_read_unit(cache.handle, layer, kv_head, seq,
+                                     k.ctypes.data_as(_vp), v.ctypes.data_as(_vp),
+                                     ctypes.byref(nv)))
+    return k, v, nv.value
+
+
+# ---------------------------------------------------------------------------
+# data path
+# ---------------------------------------------------------------------------
+def prefill_write(cache, layer, seq, pos0, k, v, stream=None):
+    """``k``, ``v``: bf16 [n_tokens, n_kv_heads, head_dim] device tensors."""
+    n = k.shape[0]
+    if tuple(k.shape) != (n, cache.n_kv_heads, cache.head_dim) or tuple(v.shape) != tuple(k.shape):
+        raise ValueError("k and v must be [n_tokens, n_kv_heads, head_dim]")
+    _check(_lib.hwkv_prefill_write(cache.handle, layer, seq, pos0, n,
+                                   _dev(k, "bfloat16", "k"), _dev(v, "bfloat16", "v"),
+                                   _stream(stream)))
+
+
+def append(cache, layer, k_new, v_new, stream=None):
+    shp = (cache.batch, cache.n_kv_heads, cache.head_dim)
+    if tuple(k_new.shape) != shp or tuple(v_new.shape) != shp:
+        raise ValueError("k_new and v_new must be [batch, n_kv_heads, head_dim]")
+    _check(_lib.hwkv_append(cache.handle, layer, _dev(k_new, "bfloat16", "k_new"),
+                            _dev(v_new, "bfloat16", "v_new"), _stream(stream)))
+
+
+def decode_workspace_bytes(cache):
+    r = _sz()
+    _check(_lib.hwkv_decode_workspace_bytes(cache.handle, ctypes.byref(r)))
+    return r.value
+
+
+def _decode_shapes(cache, q, out, ws):
+    shp = (cache.batch, cache.n_q_heads, cache.head_dim)
+    if tuple(q.shape) != shp or tuple(out.shape) != shp:
+        raise ValueError("q and out must be [batch, n_q_heads, head_dim]")
+    return _dev(ws, "uint8", "ws"), ws.numel()
+
+
+def decode_attn(cache, layer, q, scale, out, ws, stream=None):
+    """``q`` bf16 and ``out`` fp32 [batch, n_q_heads, head_dim]; ``ws`` uint8."""
+    wp, wn = _decode_shapes(cache, q, out, ws)
+    _check(_lib.hwkv_decode_attn(cache.handle, layer, _dev(q, "bfloat16", "q"), float(scale),
+                                 _dev(out, "float32", "out"), wp, wn, _stream(stream)))
+
+
+def append_decode_attn(cache, layer, k_new, v_new, q, scale, out, ws, stream=None):
+    shp = (cache.batch, cache.n_kv_heads, cache.head_dim)
+    if tuple(k_new.shape) != shp or tuple(v_new.shape) != shp:
+        raise ValueError("k_new and v_new must be [batch, n_kv_heads, head_dim]")
+    wp, wn = _decode_shapes(cache, q, out, ws)
+    _check(_lib.hwkv_append_decode_attn(
+        cache.handle, layer, _dev(k_new, "bfloat16", "k_new"), _dev(v_new, "bfloat16", "v_new"),
+        _dev(q, "bfloat16", "q"), float(scale), _dev(out, "float32", "out"), wp, wn,
+        _stream(stream)))

@@ -1,0 +1,213 @@
+"""Shared driver for the GPU parity tests: runs a workload through the C ABI
+(via the ctypes binding) and checks it against the fp64 oracle.
+
+Inputs come from ``workloads`` (seeded, bf16).  Every comparison is made on
+the same bf16 bit patterns: residency bit-exact (slot j of a unit must hold
+the K and V rows of the position the oracle's slot table names), outputs
+within the stated tolerance.
+"""
+import math
+import sys
+import time
+
+import numpy as np
+import torch
+
+import oracle
+import workloads as W
+from paper_2609_02029_amd import hwkv
+
+REL_TOL = 1e-2     # the bar: max over rows of |o - ref|_inf / |ref|_inf
+TIGHT_TOL = 2e-4   # fp32 accumulation over bf16 inputs stays far below it
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def up(a, dev):
+    """Host bf16 bits (uint16) -> device torch.bfloat16."""
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+
+
+def down(t):
+    """Device torch.bfloat16 -> host uint16 bits."""
+    return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def rel_err(got, ref):
+    got = np.asarray(got, dtype=np.float64)
+    num = np.abs(got - ref).max(axis=-1)
+    den = np.abs(ref).max(axis=-1)
+    return float((num / den).max())
+
+
+class Run:
+    """One workload on one GPU: policy, cache, seeded inputs, host histories.
+
+    ``track``: layers whose full K/V history is kept on the host for the
+    oracle (``None`` = all).  ``device_gen``: draw prompts on the device
+    (large workloads) instead of on the host."""
+
+    def __init__(self, cfg, dev="cuda:0", fused=True, track=None, device_gen=False,
+                 levels=None, prompts=None):
+        self.cfg = cfg
+        self.dev = torch.device(dev)
+        self.fused = fused
+        self.device_gen = device_gen
+        c = cfg
+        self.L, self.B = c["n_layers"], c["batch"]
+        self.Hq, self.Hkv, self.D, self.S = c["n_q_heads"], c["n_kv_heads"], c["head_dim"], c["n_sinks"]
+        self.G = self.Hq // self.Hkv
+        self.levels = levels if levels is not None else W.levels(c)
+        self.windows = [[int(c["level_windows"][k]) for k in row] for row in self.levels]
+        self.prompts = prompts if prompts is not None else W.prompts(c)
+        self.max_ctx = c["max_ctx"]
+        self.hist_len = max(self.max_ctx, max(self.prompts)) + 256
+        self.scale = 1.0 / math.sqrt(self.D)
+        self.outliers = W.outlier_channels(c)
+        self.track = set(range(self.L)) if track is None else set(track)
+        self.pol = hwkv.policy_set(self.L, self.Hkv, self.Hq, self.D, self.S,
+                                   c["level_windows"], self.levels)
+        self.cache = hwkv.cache_alloc(self.pol, self.B, self.max_ctx)
+        self.ws = torch.empty(hwkv.decode_workspace_bytes(self.cache), dtype=torch.uint8,
+                              device=self.dev)
+        # host histories [layer][b] -> uint16 [max_ctx, Hkv, D]
+        self.kh = {l: [None] * self.B for l in self.track}
+        self.vh = {l: [None] * self.B for l in self.track}
+        self.n = np.zeros((self.L, self.B), dtype=np.int64)
+        self.step_no = np.zeros(self.L, dtype=np.int64)
+
+    # ---------------- inputs
+    def _kv(self, shape, layer, kind, idx):
+        seed = self.cfg["seed"]
+        if self.device_gen:
+            t = W.normal_bf16_device(shape, seed, layer, kind, idx, device=self.dev,
+                                     scale_channels=self.outliers, scale=self.cfg.get("outlier_scale", 1.0))
+            return t, None
+        a = W.normal_bf16(shape, seed, layer, kind, idx, scale_channels=self.outliers,
+                          scale=self.cfg.get("outlier_scale", 1.0))
+        return up(a, self.dev), a
+
+    def prompt_kv(self, layer, b, P):
+        k, kh = self._kv((P, self.Hkv, self.D), layer, W.K, b)
+        v, vh = self._kv((P, self.Hkv, self.D), layer, W.V, b)
+        return k, v, kh, vh
+
+    def _hist(self, layer, b):
+        if self.kh[layer][b] is None:
+            self.kh[layer][b] = np.zeros((self.hist_len, self.Hkv, self.D), dtype=np.uint16)
+            self.vh[layer][b] = np.zeros((self.hist_len, self.Hkv, self.D), dtype=np.uint16)
+        return self.kh[layer][b], self.vh[layer][b]
+
+    # ---------------- operations
+    def prefill(self, layer, b, P=None, chunks=None):
+        P = self.prompts[b] if P is None else P
+        k, v, kh, vh = self.prompt_kv(layer, b, P)
+        cuts = [0] + sorted(chunks or []) + [P]
+        for p0, p1 in zip(cuts[:-1], cuts[1:]):
+            if p1 > p0:
+                hwkv.prefill_write(self.cache, layer, b, p0, k[p0:p1], v[p0:p1])
+        if layer in self.track:
+            hk, hv = self._hist(layer, b)
+            hk[:P] = kh if kh is not None else down(k)
+            hv[:P] = vh if vh is not None else down(v)
+        self.n[layer, b] = P
+        del k, v
+
+    def step(self, layer, fused=None):
+        """Append one token to every sequence of ``layer`` and attend."""
+        fused = self.fused if fused is None else fused
+        st = int(self.step_no[layer])
+        seed = self.cfg["seed"]
+        qa = W.normal_bf16((self.B, self.Hq, self.D), seed, layer, W.Q, st)
+        ka = W.normal_bf16((self.B, self.Hkv, self.D), seed, layer, W.K_NEW, st,
+                           scale_channels=self.outliers, scale=self.cfg.get("outlier_scale", 1.0))
+        va = W.normal_bf16((self.B, self.Hkv, self.D), seed, layer, W.V_NEW, st,
+                           scale_channels=self.outliers, scale=self.cfg.get("outlier_scale", 1.0))
+        q, kn, vn = up(qa, self.dev), up(ka, self.dev), up(va, self.dev)
+        out = torch.empty((self.B, self.Hq, self.D), dtype=torch.float32, device=self.dev)
+        if fused:
+            hwkv.append_decode_attn(self.cache, layer, kn, vn, q, self.scale, out, self.ws)
+        else:
+            hwkv.append(self.cache, layer, kn, vn)
+            hwkv.decode_attn(self.cache, layer, q, self.scale, out, self.ws)
+        if layer in self.track:
+            for b in range(self.B):
+                hk, hv = self._hist(layer, b)
+                hk[self.n[layer, b]] = ka[b]
+                hv[self.n[layer, b]] = va[b]
+        self.n[layer] += 1
+        self.step_no[layer] += 1
+        return qa, out
+
+    # ---------------- checks
+    def history(self, layer, b):
+        """Regenerate the full K/V history of (layer, b) from the seeds:
+        the prompt plus every token appended so far."""
+        P = self.prompts[b]
+        k, v, kh, vh = self.prompt_kv(layer, b, P)
+        hk = np.zeros((self.hist_len, self.Hkv, self.D), dtype=np.uint16)
+        hv = np.zeros_like(hk)
+        hk[:P] = kh if kh is not None else down(k)
+        hv[:P] = vh if vh is not None else down(v)
+        del k, v
+        seed = self.cfg["seed"]
+        sc, s = self.outliers, self.cfg.get("outlier_scale", 1.0)
+        for st in range(int(self.step_no[layer])):
+            hk[P + st] = W.normal_bf16((self.B, self.Hkv, self.D), seed, layer, W.K_NEW, st,
+                                       scale_channels=sc, scale=s)[b]
+            hv[P + st] = W.normal_bf16((self.B, self.Hkv, self.D), seed, layer, W.V_NEW, st,
+                                       scale_channels=sc, scale=s)[b]
+        return hk, hv
+
+    def oracle_out(self, layer, qa, n_threads=8):
+        t = self.n[layer] - 1
+        return oracle.decode_layer(qa, [self.kh[layer][b][: t[b] + 1] for b in range(self.B)],
+                                   [self.vh[layer][b][: t[b] + 1] for b in range(self.B)], t,
+                                   self.S, self.windows[layer], self.scale, n_threads=n_threads)
+
+    def check_out(self, layer, qa, out, what=""):
+        torch.cuda.synchronize()
+        ref = self.oracle_out(layer, qa)
+        got = out.cpu().numpy()
+        e = rel_err(got.reshape(-1, self.D), ref.reshape(-1, self.D))
+        assert np.all(np.isfinite(got)), f"{what}: non-finite output"
+        assert e <= REL_TOL, f"{what}: max rel err {e} > {REL_TOL}"
+        assert e <= TIGHT_TOL, f"{what}: max rel err {e} > {TIGHT_TOL} (fp32 accumulation bound)"
+        return e
+
+    def check_unit(self, layer, h, b, hist=None):
+        """Bit-exact residency of one (unit, sequence) against the oracle."""
+        tab = oracle.UnitTable(self.S, self.windows[layer][h], self.max_ctx)
+        if self.n[layer, b] > 0:
+            tab.prefill(0, int(self.n[layer, b]))
+        k, v, nv = hwkv.cache_read_unit(self.cache, layer, h, b)
+        assert nv == tab.n_valid, (layer, h, b, nv, tab.n_valid)
+        assert k.shape[0] == tab.cap
+        occ = tab.table[:nv]
+        assert np.all(occ >= 0)
+        hk, hv = (self.kh[layer][b], self.vh[layer][b]) if hist is None else hist
+        assert np.array_equal(k[:nv], hk[occ, h]), f"K residency differs: layer {layer} head {h} seq {b}"
+        assert np.array_equal(v[:nv], hv[occ, h]), f"V residency differs: layer {layer} head {h} seq {b}"
+
+    def check_layer(self, layer, hist=None):
+        for b in range(self.B):
+            for h in range(self.Hkv):
+                self.check_unit(layer, h, b, hist=None if hist is None else hist[b])
+
+    def free(self):
+        self.cache.free()
+
+
+def timed(label):
+    class _T:
+        def __enter__(self):
+            self.t = time.time()
+            log(f"[{label}] start")
+            return self
+
+        def __exit__(self, *a):
+            log(f"[{label}] done in {time.time() - self.t:.1f}s")
+    return _T()

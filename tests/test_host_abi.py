@@ -1,0 +1,203 @@
+"""CPU tests of libhwkv's host side: exports, policy validation, accounting,
+layout sizes, and the error paths that return before any device work.
+
+No kernel is launched here.  Caches are created over a never-dereferenced
+fake device pointer (the adopt-a-buffer path makes no HIP call), which is
+enough to reach every host-side validation."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "hwkv.h")
+
+
+@pytest.fixture(scope="module")
+def hw():
+    from paper_2609_02029_amd import hwkv
+    return hwkv
+
+
+def header_symbols():
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(hwkv_[a-z_]+)\s*\(", txt)))
+
+
+def test_library_exports_every_declared_symbol(hw):
+    syms = header_symbols()
+    assert len(syms) >= 15
+    out = subprocess.run(["nm", "-D", "--defined-only", hw.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r" T (hwkv_[a-z_]+)$", out, flags=re.M))
+    missing = [s for s in syms if s not in exported]
+    assert not missing, missing
+    # the binding declares every one of them
+    assert set(syms) <= set(hw.SYMBOLS)
+
+
+def test_error_codes_match_header(hw):
+    txt = open(HEADER).read()
+    for name in ("OK", "EINVAL", "ENOMEM", "ECAPACITY", "ESTATE", "EDEVICE"):
+        v = int(re.search(rf"#define HWKV_{name} (\d+)", txt).group(1))
+        assert getattr(hw, name) == v
+
+
+def _pol(hw, **kw):
+    a = dict(n_layers=2, n_kv_heads=2, n_q_heads=8, head_dim=64, n_sinks=4,
+             level_window=[256, 0], level_of_unit=[[0, 1], [1, 0]])
+    a.update(kw)
+    return hw.policy_set(**a)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(n_q_heads=6),                  # not a multiple of n_kv_heads
+    dict(n_q_heads=6, n_kv_heads=2),    # group 3 unsupported
+    dict(head_dim=96),
+    dict(n_sinks=-1),
+    dict(level_window=[-5, 0]),
+    dict(level_of_unit=[[0, 2], [1, 0]]),
+    dict(level_of_unit=[[0, -1], [1, 0]]),
+    dict(n_layers=0),
+    dict(n_kv_heads=65, n_q_heads=65, level_of_unit=[[0] * 65] * 2),
+])
+def test_policy_validation(hw, kw):
+    with pytest.raises(hw.HwkvError) as e:
+        _pol(hw, **kw)
+    assert e.value.code == hw.EINVAL
+    assert hw.last_error()
+
+
+def test_policy_rate_matches_oracle_and_paper(hw, golden):
+    g = golden("accounting.json")["sink_recent_control"]
+    p = hw.policy_set(1, 1, 1, 64, g["n_sinks"], [g["window"]], [[0]])
+    assert hw.policy_rate(p, g["ctx"]) == g["cache_tokens"] / g["ctx"]
+    q = golden("accounting.json")["quarter_example"]
+    p = hw.policy_set(1, 1, 1, 128, 0, [q["window"]], [[0]])
+    assert hw.policy_rate(p, q["ctx"]) == q["rate"]
+    r = np.random.default_rng(0)
+    for _ in range(50):
+        L, H = int(r.integers(1, 5)), int(r.choice([1, 2, 4]))
+        lw = [int(x) for x in r.integers(1, 3000, size=3)] + [0]
+        lv = r.integers(0, 4, size=(L, H))
+        S = int(r.integers(0, 8))
+        ctx = int(r.integers(1, 5000))
+        p = hw.policy_set(L, H, H * 2, 64, S, lw, lv.tolist())
+        wins = np.array(lw)[lv].ravel()
+        assert hw.policy_rate(p, ctx) == pytest.approx(oracle.rate(ctx, S, wins), rel=1e-14)
+        assert hw.policy_bytes(p, ctx) == pytest.approx(
+            oracle.policy_bytes(ctx, S, wins, 64, 64, 2.0, 2.0), rel=1e-14)
+
+
+def test_cache_bytes_exact(hw):
+    r = np.random.default_rng(1)
+    for _ in range(50):
+        L, H, D = int(r.integers(1, 4)), int(r.choice([1, 2, 4])), int(r.choice([64, 128, 256]))
+        lw = [int(x) for x in r.integers(1, 3000, size=3)] + [0]
+        lv = r.integers(0, 4, size=(L, H))
+        S = int(r.integers(0, 8))
+        B = int(r.integers(1, 5))
+        max_ctx = int(r.integers(1, 6000))
+        p = hw.policy_set(L, H, H, D, S, lw, lv.tolist())
+        exp = 0
+        for w in np.array(lw)[lv].ravel():
+            cap = oracle.capacity(S, int(w), max_ctx)
+            exp += B * ((cap + 63) // 64 * 64) * D * 4
+        assert hw.cache_bytes(p, B, max_ctx) == exp
+
+
+def test_cache_bytes_errors(hw):
+    p = _pol(hw)
+    for B, ctx in ((0, 10), (1, 0), (1, 1 << 31)):
+        with pytest.raises(hw.HwkvError) as e:
+            hw.cache_bytes(p, B, ctx)
+        assert e.value.code == hw.EINVAL
+
+
+FAKE = 0x7F0000000000  # adopted, never dereferenced by host code
+
+
+def _fake_cache(hw, p, B, max_ctx):
+    h = ctypes.c_void_p()
+    nbytes = hw.cache_bytes(p, B, max_ctx)
+    rc = hw._lib.hwkv_cache_alloc(ctypes.byref(h), p.handle, B, max_ctx, FAKE, nbytes)
+    assert rc == hw.OK, hw.last_error()
+    return h
+
+
+def test_adopted_buffer_too_small(hw):
+    p = _pol(hw)
+    nbytes = hw.cache_bytes(p, 2, 1000)
+    h = ctypes.c_void_p()
+    assert hw._lib.hwkv_cache_alloc(ctypes.byref(h), p.handle, 2, 1000, FAKE, nbytes - 1) == hw.ENOMEM
+    assert not h.value
+
+
+def test_canonicalisation_and_capacity(hw):
+    # S + w >= max_ctx is full; capacity S + w otherwise
+    p = hw.policy_set(1, 4, 4, 64, 4, [96, 100, 200, 0], [[0, 1, 2, 3]])
+    h = _fake_cache(hw, p, 1, 104)
+    cap, win = ctypes.c_int64(), ctypes.c_int64()
+    exp = [(100, 96), (104, 0), (104, 0), (104, 0)]
+    for kv in range(4):
+        assert hw._lib.hwkv_cache_unit_info(h, 0, kv, ctypes.byref(cap), ctypes.byref(win)) == 0
+        assert (cap.value, win.value) == exp[kv]
+        assert cap.value == oracle.capacity(4, [96, 100, 200, 0][kv], 104)
+    hw._lib.hwkv_cache_free(h)
+
+
+def test_host_error_paths_change_no_state(hw):
+    p = _pol(hw)
+    h = _fake_cache(hw, p, 2, 300)
+    L = hw._lib
+    n = ctypes.c_int64()
+    # prefill must start at the current length
+    assert L.hwkv_prefill_write(h, 0, 0, 5, 10, FAKE, FAKE, None) == hw.ESTATE
+    # a full unit cannot pass max_ctx
+    assert L.hwkv_prefill_write(h, 0, 0, 0, 301, FAKE, FAKE, None) == hw.ECAPACITY
+    # bad indices and null inputs
+    assert L.hwkv_prefill_write(h, 2, 0, 0, 1, FAKE, FAKE, None) == hw.EINVAL
+    assert L.hwkv_prefill_write(h, 0, 2, 0, 1, FAKE, FAKE, None) == hw.EINVAL
+    assert L.hwkv_prefill_write(h, 0, 0, 0, 1, None, FAKE, None) == hw.EINVAL
+    assert L.hwkv_prefill_write(h, 0, 0, 0, -1, FAKE, FAKE, None) == hw.EINVAL
+    # empty chunk: no-op
+    assert L.hwkv_prefill_write(h, 0, 0, 0, 0, None, None, None) == hw.OK
+    # decode on empty sequences, short workspace, bad scale
+    ws = ctypes.c_size_t()
+    assert L.hwkv_decode_workspace_bytes(h, ctypes.byref(ws)) == hw.OK
+    assert ws.value > 0
+    assert L.hwkv_decode_attn(h, 0, FAKE, ctypes.c_float(0.125), FAKE, FAKE, ws.value, None) == hw.EINVAL
+    assert L.hwkv_decode_attn(h, 0, FAKE, ctypes.c_float(float("nan")), FAKE, FAKE, ws.value, None) == hw.EINVAL
+    assert L.hwkv_append_decode_attn(h, 0, FAKE, FAKE, FAKE, ctypes.c_float(0.125), FAKE, FAKE, 0,
+                                     None) == hw.EINVAL
+    assert L.hwkv_append_decode_attn(h, 0, None, FAKE, FAKE, ctypes.c_float(0.125), FAKE, FAKE,
+                                     ws.value, None) == hw.EINVAL
+    assert L.hwkv_append(h, 0, None, FAKE, None) == hw.EINVAL
+    assert L.hwkv_append(h, 3, FAKE, FAKE, None) == hw.EINVAL
+    for layer in range(2):
+        for seq in range(2):
+            assert L.hwkv_cache_seq_len(h, layer, seq, ctypes.byref(n)) == hw.OK
+            assert n.value == 0
+    assert L.hwkv_cache_seq_len(h, 2, 0, ctypes.byref(n)) == hw.EINVAL
+    L.hwkv_cache_free(h)
+
+
+def test_workspace_bytes_cover_full_capacity(hw):
+    p = hw.policy_set(2, 4, 24, 256, 4, [2048, 8192, 32768, 0], [[0, 1, 2, 3], [3, 3, 3, 3]])
+    h = _fake_cache(hw, p, 1, 114688)
+    ws = ctypes.c_size_t()
+    hw._lib.hwkv_decode_workspace_bytes(h, ctypes.byref(ws))
+    # at least one partial (6 heads x (256 + 2) fp32) per 64 tokens of the
+    # longest layer, at most one per 64 tokens plus one per unit
+    rows = 4 * 114688
+    part = 6 * 258 * 4
+    assert ws.value <= (rows // 64 + 4) * part
+    assert ws.value >= part * 4
+    hw._lib.hwkv_cache_free(h)
