@@ -1,0 +1,283 @@
+"""Decode-step benchmark of the grouped-cache runtime on one MI355X.
+
+A step is one pass of the decode hot path over every layer of the workload:
+for each layer, append the new token to every unit and attend with the
+layer's query (one ``hwkv_append_decode_attn`` call per layer).  The cache is
+materialised once before timing (``hwkv_prefill_write`` per layer); inputs
+are resident in HBM before the timed region starts.
+
+Default workload: 16 residual global layers at a 112K context (114,688
+tokens), batch 1, 24 query / 4 KV heads, head_dim 256, bf16 K/V, 4 sinks,
+per-unit levels over {2048, 8192, 32768, full} drawn at a 45-50% residency
+budget, 128 decode steps after a 114,560-token prompt.
+
+Prints ONE JSON line: resident-KV GB/s (``value``), microseconds per step,
+the roofline of the dominant kernel and the oracle's CPU baseline.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decode-attn µs/step + resident-KV HBM GB/s (% of peak) at 112K ctx, 1 GPU"
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--workload", default="ctx112k",
+                    choices=["ctx112k", "ctx32k", "batch16", "pr1"])
+    ap.add_argument("--unfused", action="store_true",
+                    help="time hwkv_append + hwkv_decode_attn instead of the fused call")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="approximate CPU time budget of the oracle sample")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the grouped-cache runtime is built and "
+              "timed on a single MI355X (no sharding, no collectives). Run with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import workloads as W
+    from paper_2609_02029_amd import hwkv
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cfg = W.CONFIGS[args.workload]
+    L, B = cfg["n_layers"], cfg["batch"]
+    Hq, Hkv, D, S = cfg["n_q_heads"], cfg["n_kv_heads"], cfg["head_dim"], cfg["n_sinks"]
+    levels = W.levels(cfg)
+    windows = W.windows_of(cfg, levels)
+    total_steps = args.warmup + args.steps
+    prompts = W.prompts(cfg)
+    max_ctx = cfg["max_ctx"]
+    if total_steps > cfg["steps"]:
+        # keep the final context at max_ctx: start from a shorter prompt
+        extra = total_steps - cfg["steps"]
+        prompts = [max(1, p - extra) for p in prompts]
+    scale = 1.0 / math.sqrt(D)
+
+    pol = hwkv.policy_set(L, Hkv, Hq, D, S, cfg["level_windows"], levels)
+    cache = hwkv.cache_alloc(pol, B, max_ctx)
+    ws = torch.empty(hwkv.decode_workspace_bytes(cache), dtype=torch.uint8, device=dev)
+    caps = [[hwkv.cache_unit_info(cache, l, h)[0] for h in range(Hkv)] for l in range(L)]
+    outl = W.outlier_channels(cfg)
+    osc = cfg.get("outlier_scale", 1.0)
+
+    t0 = time.time()
+    for l in range(L):
+        for b in range(B):
+            k = W.normal_bf16_device((prompts[b], Hkv, D), cfg["seed"], l, W.K, b, device=dev,
+                                     scale_channels=outl, scale=osc)
+            v = W.normal_bf16_device((prompts[b], Hkv, D), cfg["seed"], l, W.V, b, device=dev,
+                                     scale_channels=outl, scale=osc)
+            hwkv.prefill_write(cache, l, b, 0, k, v)
+            del k, v
+    torch.cuda.synchronize()
+    prefill_s = time.time() - t0
+
+    # per-step inputs, resident on the device before timing
+    def dev_bf16(a):
+        return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16)
+    qs = torch.stack([torch.stack([dev_bf16(W.normal_bf16((B, Hq, D), cfg["seed"], l, W.Q, s))
+                                   for l in range(L)]) for s in range(total_steps)]).to(dev)
+    kn = torch.stack([torch.stack([dev_bf16(W.normal_bf16((B, Hkv, D), cfg["seed"], l, W.K_NEW, s,
+                                                          scale_channels=outl, scale=osc))
+                                   for l in range(L)]) for s in range(total_steps)]).to(dev)
+    vn = torch.stack([torch.stack([dev_bf16(W.normal_bf16((B, Hkv, D), cfg["seed"], l, W.V_NEW, s,
+                                                          scale_channels=outl, scale=osc))
+                                   for l in range(L)]) for s in range(total_steps)]).to(dev)
+    out = torch.empty((L, B, Hq, D), dtype=torch.float32, device=dev)
+
+    def kv_bytes(step_idx):
+        """Algorithmic resident-KV bytes of step ``step_idx`` (per layer)."""
+        per_layer = []
+        for l in range(L):
+            tot = 0
+            for b in range(B):
+                n = prompts[b] + step_idx + 1
+                for h in range(Hkv):
+                    tot += min(n, caps[l][h]) * D * 2 * 2
+            per_layer.append(tot)
+        return per_layer
+
+    def run_step(s, ev=None):
+        for l in range(L):
+            if ev is not None:
+                ev[l][0].record()
+            if args.unfused:
+                hwkv.append(cache, l, kn[s, l], vn[s, l])
+                hwkv.decode_attn(cache, l, qs[s, l], scale, out[l], ws)
+            else:
+                hwkv.append_decode_attn(cache, l, kn[s, l], vn[s, l], qs[s, l], scale, out[l], ws)
+            if ev is not None:
+                ev[l][1].record()
+
+    for s in range(args.warmup):
+        run_step(s)
+    torch.cuda.synchronize()
+
+    evs = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
+            for _ in range(L)] for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(args.steps):
+        run_step(args.warmup + i, evs[i])
+    end.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    ms_per_step = total_ms / args.steps
+
+    bytes_steps = [sum(kv_bytes(args.warmup + i)) for i in range(args.steps)]
+    bytes_per_step = sum(bytes_steps) / args.steps
+    gbs = bytes_per_step / (ms_per_step * 1e-3) / 1e9
+
+    # per-call (one layer: fused append + split + combine) durations
+    call_ms, call_bytes = [], []
+    for i in range(args.steps):
+        per_layer = kv_bytes(args.warmup + i)
+        for l in range(L):
+            call_ms.append(evs[i][l][0].elapsed_time(evs[i][l][1]))
+            call_bytes.append(per_layer[l])
+    call_ms = np.array(call_ms)
+    call_bytes = np.array(call_bytes, dtype=np.float64)
+    achieved = float(call_bytes.mean() / (call_ms.mean() * 1e-3) / 1e9)
+
+    rate = hwkv.policy_rate(pol, max_ctx)
+    result = {
+        "metric": METRIC,
+        "value": round(gbs, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "us_per_step": round(ms_per_step * 1e3, 1),
+        "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 (fp32 accumulate)",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{cfg['name']}: {L} residual global layers, batch {B}, "
+                         f"{Hq} q / {Hkv} kv heads, head_dim {D}, {S} sinks, levels "
+                         f"{cfg['level_windows']} (0 = full), R={rate:.4f} at {max_ctx} tokens, "
+                         f"prompt {prompts[0] if B == 1 else 'ragged'}, "
+                         f"{'append+decode' if args.unfused else 'fused append+decode'} per layer"),
+            "max_ctx": max_ctx,
+            "resident_kv_bytes_per_step": int(bytes_per_step),
+            "prefill_write_s": round(prefill_s, 3),
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "one fused append+decode call per layer (decode_split + decode_combine)",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "call_us_mean": round(float(call_ms.mean()) * 1e3, 2),
+            "kv_bytes_per_call": int(call_bytes.mean()),
+        },
+    }
+
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(args, cfg, prompts, windows, caps, scale, outl, osc,
+                                              dev, ms_per_step, bytes_per_step)
+    cache.free()
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline(args, cfg, prompts, windows, caps, scale, outl, osc, dev, gpu_ms, step_bytes):
+    """The fp64 oracle timed on the host cores on a bounded sample of the same
+    step: whole layers of decode step 0 (every sequence and query head),
+    regenerated from the same seeds, until about ``--cpu-seconds`` of oracle
+    time; scaled to a full step by the sampled layers' share of the step's
+    resident bytes."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import workloads as W
+
+    L, B = cfg["n_layers"], cfg["batch"]
+    Hq, Hkv, D = cfg["n_q_heads"], cfg["n_kv_heads"], cfg["head_dim"]
+    threads = max(1, min(16, os.cpu_count() or 1))
+    done_bytes, spent, layers = 0, 0.0, 0
+    step = args.warmup  # the first timed step
+    for l in range(L):
+        kh, vh, t = [], [], []
+        for b in range(B):
+            P = prompts[b]
+            k = W.normal_bf16_device((P, Hkv, D), cfg["seed"], l, W.K, b, device=dev,
+                                     scale_channels=outl, scale=osc)
+            v = W.normal_bf16_device((P, Hkv, D), cfg["seed"], l, W.V, b, device=dev,
+                                     scale_channels=outl, scale=osc)
+            hk = np.empty((P + step + 1, Hkv, D), dtype=np.uint16)
+            hv = np.empty_like(hk)
+            hk[:P] = k.view(torch.int16).cpu().numpy().view(np.uint16)
+            hv[:P] = v.view(torch.int16).cpu().numpy().view(np.uint16)
+            del k, v
+            for s in range(step + 1):
+                hk[P + s] = W.normal_bf16((B, Hkv, D), cfg["seed"], l, W.K_NEW, s,
+                                          scale_channels=outl, scale=osc)[b]
+                hv[P + s] = W.normal_bf16((B, Hkv, D), cfg["seed"], l, W.V_NEW, s,
+                                          scale_channels=outl, scale=osc)[b]
+            kh.append(hk)
+            vh.append(hv)
+            t.append(P + step)
+        q = W.normal_bf16((B, Hq, D), cfg["seed"], l, W.Q, step)
+        t0 = time.perf_counter()
+        oracle.decode_layer(q, kh, vh, t, cfg["n_sinks"], windows[l], scale, n_threads=threads)
+        spent += time.perf_counter() - t0
+        layers += 1
+        for b in range(B):
+            for h in range(Hkv):
+                done_bytes += min(prompts[b] + step + 1, caps[l][h]) * D * 4
+        del kh, vh
+        if spent >= args.cpu_seconds:
+            break
+    us_per_step = spent / done_bytes * step_bytes * 1e6
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {
+        "value": round(us_per_step, 1),
+        "unit": "us/step",
+        "gbs": round(done_bytes / spent / 1e9, 3),
+        "cores": threads,
+        "cpu": model,
+        "kind": "oracle",
+        "sample": (f"decode step {step} (first timed step), layers 0..{layers - 1} of {L}, every "
+                   f"sequence and query head; fp64 masked-full-history oracle, "
+                   f"{spent:.1f} s of CPU time; scaled to the whole step by resident bytes"),
+        "gpu_speedup": round(us_per_step / (gpu_ms * 1e3), 1),
+    }
+
+
+if __name__ == "__main__":
+    main()

@@ -111,7 +111,9 @@ int hwkv_policy_rate(const hwkv_policy *policy, int64_t ctx, double *rate);
  * token rows (the K tile), times head_dim * (2 + 2) bytes, where cap = max_ctx
  * for full units (or S + w >= max_ctx) and S + w otherwise.  Equals
  * batch x Eq. nominal-storage at ctx = max_ctx up to that rounding.
- * 1 <= max_ctx <= 2^31 - 128.  EINVAL on overflow. */
+ * 1 <= max_ctx, and max_ctx (rounded up to 64) * head_dim * 2 < 2^31, the
+ * bytes of one unit's K or V per sequence (4,194,240 tokens at head_dim 256).
+ * EINVAL otherwise or on size_t overflow. */
 int hwkv_cache_bytes(const hwkv_policy *policy, int32_t batch, int64_t max_ctx,
                      size_t *bytes);
 

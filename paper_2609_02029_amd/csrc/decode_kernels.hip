@@ -15,31 +15,72 @@
 // (full and windowed heads of one layer differ by up to ~56x in length).  The
 // G query heads of an item share every K/V byte read.
 //
-// Inside a wave, per 64-slot tile:
+// Inside a wave, per 64-slot tile (one stream of 16-byte buffer loads per
+// lane, kPrefetch loads always in flight):
 //   q.k   one lane per slot: the K tile is stored slot-minor in 16-byte
 //         channel chunks, so chunk g of the tile is 1 KiB contiguous and lane
-//         t reads its own slot's chunk; q is staged once per workgroup in LDS
-//         and read as a broadcast, and v_dot2_f32_bf16 multiplies bf16 pairs
-//         with fp32 accumulate.
-//         No cross-lane reduction is needed for the logits.
+//         t reads its own slot's chunk; q is uniform and comes through scalar
+//         loads, and v_dot2_f32_bf16 multiplies bf16 pairs (q as an SGPR
+//         operand) with fp32 accumulate.  No cross-lane reduction is needed for the
+//         logits.
 //   softmax  online, base 2 (log2(e) folded into the scale); the tile max is
 //         one DPP row reduction plus four lane reads per head.
 //   p.v   lanes own 8 channels of one row (V row-major, a wave reads whole
-//         rows contiguously); p is broadcast through a per-wave LDS slice.
+//         rows contiguously); p stays fp32 and is broadcast through a
+//         per-wave LDS slice; one fp32 FMA per (row, channel, head).
+//         The V buffer descriptor ends at row n_valid, so rows past it read
+//         as zero (and their p is zero).
+// The fused append writes the new token into its slot at the start of the
+// one workgroup whose split holds that slot, before any of its waves read.
 // The waves of a workgroup are merged in LDS; a split either writes the final
 // output (single-split items) or a partial (m, l, acc) that the combine
 // kernel merges: m* = max m_j, l* = sum l_j 2^(m_j - m*),
 // out = sum acc_j 2^(m_j - m*) / l*.
+#include <utility>
+
 #include "hwkv_internal.h"
 
 namespace hwkv {
 namespace {
 
-constexpr int kWaves = 4;         // waves per workgroup
-constexpr int kTilesPerWave = 2;  // 64-slot tiles per wave per split
-constexpr int kMinWavesPerEU = 3; // register budget: <= 168 VGPRs per lane
+// Calls f(std::integral_constant<int, J>{}) for J = 0 .. N-1 (fully
+// unrolled: every index is a compile-time constant).
+template <typename F, int... Js>
+__device__ __forceinline__ void static_for_impl(F &f,
+                                                std::integer_sequence<int, Js...>) {
+  (f(std::integral_constant<int, Js>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+// Split geometry and load batching (compile-time; see decode_split_tokens).
+#ifndef HWKV_DECODE_WAVES
+#define HWKV_DECODE_WAVES 4
+#endif
+#ifndef HWKV_DECODE_TPW
+#define HWKV_DECODE_TPW 1
+#endif
+#ifndef HWKV_DECODE_PREFETCH
+#define HWKV_DECODE_PREFETCH 8
+#endif
+#ifndef HWKV_DECODE_AUX
+#define HWKV_DECODE_AUX 0  // cache-policy bits of the streaming loads
+#endif
+#ifndef HWKV_DECODE_MINWAVES
+#define HWKV_DECODE_MINWAVES 4
+#endif
+constexpr int kWaves = HWKV_DECODE_WAVES;        // waves per workgroup
+constexpr int kTilesPerWave = HWKV_DECODE_TPW;   // 64-slot tiles per wave
+constexpr int kPrefetch = HWKV_DECODE_PREFETCH;  // 16-byte loads in flight
+constexpr int kMinWavesPerEU = HWKV_DECODE_MINWAVES;  // VGPR budget
+constexpr int kCombineWaves = 16;
+constexpr int kCombineUnroll = 8;
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+typedef const __attribute__((address_space(4))) u32x4_t cu32x4_t;
 
 __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
   return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a),
@@ -52,6 +93,21 @@ __device__ __forceinline__ float bf_lo(uint32_t x) {
 }
 __device__ __forceinline__ float bf_hi(uint32_t x) {
   return __uint_as_float(x & 0xffff0000u);
+}
+
+// 16-byte raw buffer load: SGPR descriptor + 32-bit byte offset; reads past
+// the descriptor's num_records return zero.
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base,
+                                                            uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0,
+                                           (int)bytes, 0x00020000);
+}
+
+__device__ __forceinline__ uint4 bload(__amdgpu_buffer_rsrc_t r, int offset) {
+  const u32x4_t v =
+      __builtin_amdgcn_raw_buffer_load_b128(r, offset, 0, HWKV_DECODE_AUX);
+  return make_uint4(v.x, v.y, v.z, v.w);
 }
 
 template <int CTRL>
@@ -88,17 +144,29 @@ __device__ __forceinline__ float wave_sum(float v) {
 }
 
 template <int D, int G>
+struct SplitSmem {
+  static constexpr int NC = D / 8;
+  static constexpr int PST = (G + 3) & ~3;  // p stride per slot
+  float m[kWaves][G];
+  float l[kWaves][G];
+  union {
+    float p[kWaves][64 * PST];     // per-wave p broadcast, tile loop
+    float acc[kWaves][G][D];       // per-wave partials, merge
+  } u;
+};
+
+template <int D, int G>
 __global__ __launch_bounds__(kWaves * 64)
 __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
     DecodeArgs a) {
   constexpr int NC = D / 8;         // 16-byte chunks per row
   constexpr int RPS = 64 / NC;      // rows per wave step in p.v
-  constexpr int PST = (G + 3) & ~3; // p stride per slot in LDS
-  __shared__ uint4 q_lds[G * NC];
-  __shared__ float p_lds[kWaves][64 * PST];
-  __shared__ float mrg_acc[kWaves][G][D];
-  __shared__ float mrg_m[kWaves][G];
-  __shared__ float mrg_l[kWaves][G];
+  constexpr int PST = SplitSmem<D, G>::PST;
+  // loads in flight per lane (at most one tile's K chunks); the ring slot of
+  // a load is its step number mod PF across tiles, so PF must divide 2 NC
+  constexpr int PF = kPrefetch < NC ? kPrefetch : NC;
+  static_assert((2 * NC) % PF == 0, "prefetch depth must divide 2 NC");
+  __shared__ SplitSmem<D, G> sm;
 
   const DecodeItems &it = a.it;
   const int blk = blockIdx.x;
@@ -112,6 +180,7 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
   }
   const int item = lo;
   const int split = blk - it.split_begin[item];
+  const int nsplit = it.split_begin[item + 1] - it.split_begin[item];
   const int nv = it.n_valid[item];
   const int new_slot = it.new_slot[item];
   const int wave = threadIdx.x >> 6;
@@ -121,17 +190,34 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
 
   uint16_t *kbase = a.cache + it.k_off[item];
   uint16_t *vbase = a.cache + it.v_off[item];
-  {
-    const uint4 *qg =
-        reinterpret_cast<const uint4 *>(a.q + (size_t)it.q_row[item] * D);
-    for (int e = threadIdx.x; e < G * NC; e += kWaves * 64) q_lds[e] = qg[e];
+  // q is uniform across the workgroup: read it through the scalar path
+  // (constant address space), so v_dot2 takes it as an SGPR operand
+  const cu32x4_t *qc = (const cu32x4_t *)(a.q + (size_t)it.q_row[item] * D);
+  // Tiles of the item are dealt to its waves with a stride: wave wl of the
+  // item's nw waves takes tiles wl, wl + nw, ...  At any moment the item's
+  // waves then read a compact window of the cache instead of one far-apart
+  // region each, which keeps the DRAM traffic local.
+  const int n_tiles = (nv + 63) / 64;
+  const int nw = nsplit * kWaves;
+  const int wl = split * kWaves + wave;
+  // fused append: the workgroup that reads new_slot stores the new token
+  // first; its waves then read it from the cache like any other slot
+  const bool writes_new =
+      new_slot >= 0 && ((new_slot / 64) % nw) / kWaves == split;
+  if (writes_new && threadIdx.x < 2 * NC) {
+    const size_t src = (size_t)it.kv_row[item] * D;
+    if (threadIdx.x < NC) {
+      const int g = threadIdx.x;
+      *reinterpret_cast<uint4 *>(
+          kbase + (((size_t)(new_slot / 64) * NC + g) * 64 + new_slot % 64) * 8) =
+          *reinterpret_cast<const uint4 *>(a.k_new + src + g * 8);
+    } else {
+      const int g = threadIdx.x - NC;
+      *reinterpret_cast<uint4 *>(vbase + (size_t)new_slot * D + g * 8) =
+          *reinterpret_cast<const uint4 *>(a.v_new + src + g * 8);
+    }
+    __threadfence();
   }
-  // the fused append reads the new token from k_new / v_new (new_slot >= 0
-  // only when they are given)
-  const uint4 *knew = reinterpret_cast<const uint4 *>(
-      a.k_new + (size_t)(new_slot >= 0 ? it.kv_row[item] : 0) * D);
-  const uint4 *vnew = reinterpret_cast<const uint4 *>(
-      a.v_new + (size_t)(new_slot >= 0 ? it.kv_row[item] : 0) * D);
 
   float m[G], l[G], acc[G][8];
 #pragma unroll
@@ -141,38 +227,74 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
   }
-  float *pl = p_lds[wave];
+  float *pl = sm.u.p[wave];
   __syncthreads();
+  if (writes_new) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 
-  for (int k = 0; k < kTilesPerWave; ++k) {
-    const int tile = (split * kTilesPerWave + k) * kWaves + wave;
-    const int slot0 = tile * 64;
-    if (slot0 >= nv) break;
+  // K: every tile up to the last occupied one; V: rows [0, nv) only
+  const __amdgpu_buffer_rsrc_t krs =
+      make_rsrc(kbase, (uint32_t)(((nv + 63) / 64) * 64 * D * 2));
+  const __amdgpu_buffer_rsrc_t vrs = make_rsrc(vbase, (uint32_t)(nv * D * 2));
 
-    // ---- q.k: one lane per slot
+  // Each tile is a stream of 2 NC 16-byte loads per lane: NC K chunks (one
+  // lane per slot), then NC steps of V rows (lanes own channel slices).  It
+  // is consumed with PF loads always in flight, so the V loads of a tile are
+  // on their way while its last K chunks and the softmax are computed.
+  // Each tile is a stream of 2 NC 16-byte loads per lane: NC K chunks (one
+  // lane per slot), then NC steps of V rows (lanes own channel slices).  It
+  // is consumed with PF loads always in flight: the V loads of a tile are on
+  // their way while its last K chunks and the softmax are computed, and the
+  // first K loads of the wave's next tile while its last V rows are.
+  uint4 buf[PF];
+  int t = wl;
+  int kofs = t * 64 * D * 2 + lane * 16;
+  if (t < n_tiles) static_for<PF>([&](auto jc) {
+    buf[jc.value] = bload(krs, kofs + jc.value * 64 * 16);
+  });
+  for (int k = 0; k < kTilesPerWave && t < n_tiles; ++k) {
+    const int slot0 = t * 64;
     const int slot = slot0 + lane;
-    const bool is_new = slot == new_slot;
-    uint4 *kt = reinterpret_cast<uint4 *>(kbase + (size_t)tile * 64 * D) + lane;
-    const uint4 *ksrc = is_new ? knew : kt;
-    const int kstr = is_new ? 1 : 64;
+    const int tn = t + nw;
+    const bool has_next = k + 1 < kTilesPerWave && tn < n_tiles;
+    int vofs = (slot0 + rsub) * D * 2 + c8 * 16;
+    int kofs_n = tn * 64 * D * 2 + lane * 16;
+    uint64_t qaddr = (uint64_t)qc;
+    // load j of this tile's stream: K chunk j, or V step j - NC
+    auto ld = [&](auto jc) -> uint4 {
+      constexpr int j = decltype(jc)::value;
+      if constexpr (j < NC)
+        return bload(krs, kofs + j * 64 * 16);
+      else
+        return bload(vrs, vofs + (j - NC) * RPS * D * 2);
+    };
     float s[G];
 #pragma unroll
     for (int h = 0; h < G; ++h) s[h] = 0.f;
-#pragma unroll 2
-    for (int g = 0; g < NC; ++g) {
-      const uint4 kk = ksrc[g * kstr];
-      if (is_new) kt[g * 64] = kk;
+
+    // ---- q.k, one K chunk per step.  The empty asm statements make the
+    // accumulators, the offsets and the q address opaque at each step
+    // boundary, so that every step issues its own loads (one load PF steps
+    // ahead, the step's q chunk) and does its own arithmetic, instead of the
+    // compiler hoisting the loads of the whole tile and spilling.
+    static_for<NC>([&](auto jc) {
+      constexpr int j = decltype(jc)::value;
+#pragma unroll
+      for (int h = 0; h < G; ++h) asm volatile("" : "+v"(s[h]));
+      asm volatile("" : "+v"(kofs), "+v"(vofs), "+s"(qaddr));
+      const uint4 x = buf[j % PF];
+      buf[j % PF] = ld(std::integral_constant<int, j + PF>{});
+      const cu32x4_t *qj = (const cu32x4_t *)qaddr;
 #pragma unroll
       for (int h = 0; h < G; ++h) {
-        const uint4 qq = q_lds[h * NC + g];
-        s[h] = dot2(qq.x, kk.x, s[h]);
-        s[h] = dot2(qq.y, kk.y, s[h]);
-        s[h] = dot2(qq.z, kk.z, s[h]);
-        s[h] = dot2(qq.w, kk.w, s[h]);
+        const u32x4_t qq = qj[h * NC + j];
+        s[h] = dot2(qq.x, x.x, s[h]);
+        s[h] = dot2(qq.y, x.y, s[h]);
+        s[h] = dot2(qq.z, x.z, s[h]);
+        s[h] = dot2(qq.w, x.w, s[h]);
       }
-    }
+    });
 
-    // ---- online softmax, base 2
+    // ---- online softmax, base 2 (the first V loads are already in flight)
     const bool valid = slot < nv;
 #pragma unroll
     for (int h = 0; h < G; ++h) {
@@ -190,29 +312,40 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
       pl[lane * PST + h] = p;
     }
 
-    // ---- p.v: lanes own channels [8 c8, 8 c8 + 8) of row rsub of a step
-    const int rows = min(64, nv - slot0);
-    uint4 *vt = reinterpret_cast<uint4 *>(vbase + (size_t)slot0 * D);
-#pragma unroll 4
-    for (int st = 0; st < 64 / RPS; ++st) {
-      if (st * RPS >= rows) break;
-      const int r = st * RPS + rsub;
-      const bool rv = r < rows;
-      const int rc = rv ? r : rows - 1;
-      const bool rn = (slot0 + rc) == new_slot;
-      const uint4 *vsrc = rn ? vnew + c8 : vt + rc * NC + c8;
-      const uint4 vv = *vsrc;
-      if (rn) vt[rc * NC + c8] = vv;
+    // ---- p.v, one step of RPS rows per step; lanes own channels 8 c8 ..
+    auto issue = [&](auto jc) {  // the load PF steps after step j
+      constexpr int j = decltype(jc)::value;
+      constexpr int jn = j + PF;
+      if constexpr (jn < 2 * NC) {
+        buf[j % PF] = ld(std::integral_constant<int, jn>{});
+      } else {
+        if (has_next) buf[j % PF] = bload(krs, kofs_n + (jn - 2 * NC) * 64 * 16);
+      }
+    };
+    static_for<NC>([&](auto jc) {
+      constexpr int js = decltype(jc)::value;
+      constexpr int j = NC + js;
+#pragma unroll
+      for (int h = 0; h < G; ++h)
+#pragma unroll
+        for (int e = 0; e < 8; e += 2)
+          asm volatile("" : "+v"(acc[h][e]), "+v"(acc[h][e + 1]));
+      asm volatile("" : "+v"(vofs), "+v"(kofs_n));
+      const uint4 x = buf[j % PF];
+      issue(std::integral_constant<int, j>{});
+      const int r = js * RPS + rsub;
       float pv[G];
 #pragma unroll
-      for (int h = 0; h < G; ++h) pv[h] = rv ? pl[r * PST + h] : 0.f;
-      const float vf[8] = {bf_lo(vv.x), bf_hi(vv.x), bf_lo(vv.y), bf_hi(vv.y),
-                           bf_lo(vv.z), bf_hi(vv.z), bf_lo(vv.w), bf_hi(vv.w)};
+      for (int h = 0; h < G; ++h) pv[h] = pl[r * PST + h];
+      const float vf[8] = {bf_lo(x.x), bf_hi(x.x), bf_lo(x.y), bf_hi(x.y),
+                           bf_lo(x.z), bf_hi(x.z), bf_lo(x.w), bf_hi(x.w)};
 #pragma unroll
       for (int h = 0; h < G; ++h)
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pv[h], vf[e], acc[h][e]);
-    }
+    });
+    t = tn;
+    kofs = kofs_n;
   }
 
   // ---- wave partials: l over all lanes, acc over lanes sharing a chunk
@@ -226,35 +359,35 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
         acc[h][e] += __shfl_xor(acc[h][e], off);
     }
   }
+  __syncthreads();  // every wave is done with its p slice
   if (rsub == 0) {
 #pragma unroll
     for (int h = 0; h < G; ++h)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) mrg_acc[wave][h][c8 * 8 + e] = acc[h][e];
+      for (int e = 0; e < 8; ++e) sm.u.acc[wave][h][c8 * 8 + e] = acc[h][e];
   }
   if (lane == 0) {
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-      mrg_m[wave][h] = m[h];
-      mrg_l[wave][h] = l[h];
+      sm.m[wave][h] = m[h];
+      sm.l[wave][h] = l[h];
     }
   }
   __syncthreads();
 
-  // ---- merge the waves (every split has a valid tile in wave 0)
-  const int nsplit = it.split_begin[item + 1] - it.split_begin[item];
+  // ---- merge the waves (wave 0 of every split has at least one tile)
   float *part = a.ws + (size_t)(it.ws_split0 + blk) * (G * (D + 2));
   for (int idx = threadIdx.x; idx < G * D; idx += kWaves * 64) {
     const int h = idx / D, c = idx % D;
-    float M = mrg_m[0][h];
+    float M = sm.m[0][h];
 #pragma unroll
-    for (int w = 1; w < kWaves; ++w) M = fmaxf(M, mrg_m[w][h]);
+    for (int w = 1; w < kWaves; ++w) M = fmaxf(M, sm.m[w][h]);
     float L = 0.f, A = 0.f;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) {
-      const float f = exp2f(mrg_m[w][h] - M);
-      L += mrg_l[w][h] * f;
-      A += mrg_acc[w][h][c] * f;
+      const float f = exp2f(sm.m[w][h] - M);
+      L += sm.l[w][h] * f;
+      A += sm.u.acc[w][h][c] * f;
     }
     if (nsplit == 1) {
       a.out[((size_t)it.q_row[item] + h) * D + c] = A / L;
@@ -268,13 +401,18 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
   }
 }
 
-// One workgroup per (item, query head of the group, 64-channel chunk).
+// One workgroup per (item, query head of the group, 64-channel chunk).  Wave
+// w merges splits w, w + kCombineWaves, ...; each round issues the loads of
+// kCombineUnroll splits before using any of them, so a round costs one memory
+// round trip.  The waves are then merged in LDS.
 template <int D, int G>
-__global__ __launch_bounds__(256) void decode_combine(DecodeArgs a) {
+__global__ __launch_bounds__(kCombineWaves * 64) void decode_combine(
+    DecodeArgs a) {
   constexpr int CH = D / 64;
   constexpr int PS = G * (D + 2);
-  __shared__ float sl[4][64];
-  __shared__ float sa[4][64];
+  constexpr int U = kCombineUnroll;
+  __shared__ float sM[kCombineWaves], sL[kCombineWaves];
+  __shared__ float sA[kCombineWaves][64];
   const DecodeItems &it = a.it;
   const int bid = blockIdx.x;
   const int item = bid / (G * CH);
@@ -288,23 +426,55 @@ __global__ __launch_bounds__(256) void decode_combine(DecodeArgs a) {
   const int c = ch * 64 + lane;
   const float *base = a.ws + (size_t)(it.ws_split0 + sb) * PS;
 
-  float M = -INFINITY;
-  for (int j = lane; j < ns; j += 64) M = fmaxf(M, base[(size_t)j * PS + h]);
-  M = wave_max(M);
-  float L = 0.f, A = 0.f;
-  for (int j = wave; j < ns; j += 4) {
-    const float *pj = base + (size_t)j * PS;
-    const float f = exp2f(pj[h] - M);
-    L += pj[G + h] * f;
-    A += pj[2 * G + h * D + c] * f;
+  float M = -INFINITY, L = 0.f, A = 0.f;
+  for (int j0 = wave; j0 < ns; j0 += kCombineWaves * U) {
+    float mj[U], lj[U], aj[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int j = j0 + u * kCombineWaves;
+      if (j < ns) {
+        const float *pj = base + (size_t)j * PS;
+        mj[u] = pj[h];
+        lj[u] = pj[G + h];
+        aj[u] = pj[2 * G + h * D + c];
+      } else {
+        mj[u] = -INFINITY;
+        lj[u] = 0.f;
+        aj[u] = 0.f;
+      }
+    }
+    float Mn = M;
+#pragma unroll
+    for (int u = 0; u < U; ++u) Mn = fmaxf(Mn, mj[u]);
+    const float f = exp2f(M - Mn);
+    L *= f;
+    A *= f;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float e = exp2f(mj[u] - Mn);
+      L += lj[u] * e;
+      A += aj[u] * e;
+    }
+    M = Mn;
   }
-  sl[wave][lane] = L;
-  sa[wave][lane] = A;
+  if (lane == 0) {
+    sM[wave] = M;
+    sL[wave] = L;
+  }
+  sA[wave][lane] = A;
   __syncthreads();
   if (wave == 0) {
-    L = (sl[0][lane] + sl[1][lane]) + (sl[2][lane] + sl[3][lane]);
-    A = (sa[0][lane] + sa[1][lane]) + (sa[2][lane] + sa[3][lane]);
-    a.out[((size_t)it.q_row[item] + h) * D + c] = A / L;
+    float Mx = sM[0];
+#pragma unroll
+    for (int w = 1; w < kCombineWaves; ++w) Mx = fmaxf(Mx, sM[w]);
+    float Lx = 0.f, Ax = 0.f;
+#pragma unroll
+    for (int w = 0; w < kCombineWaves; ++w) {
+      const float f = exp2f(sM[w] - Mx);
+      Lx += sL[w] * f;
+      Ax += sA[w][lane] * f;
+    }
+    a.out[((size_t)it.q_row[item] + h) * D + c] = Ax / Lx;
   }
 }
 
@@ -315,8 +485,8 @@ hipError_t launch_dg(const DecodeArgs &a, int n_splits, int n_combine,
                      0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || n_combine == 0) return e;
-  hipLaunchKernelGGL((decode_combine<D, G>), dim3(n_combine), dim3(256), 0, s,
-                     a);
+  hipLaunchKernelGGL((decode_combine<D, G>), dim3(n_combine),
+                     dim3(kCombineWaves * 64), 0, s, a);
   return hipGetLastError();
 }
 

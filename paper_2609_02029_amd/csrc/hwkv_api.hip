@@ -77,8 +77,12 @@ void unit_shape(const hwkv_policy &p, int32_t u, int64_t max_ctx,
 int layout(const hwkv_policy &p, int32_t batch, int64_t max_ctx, size_t *bytes,
            hwkv_cache *c) {
   if (batch < 1) return fail(HWKV_EINVAL, "batch must be >= 1");
-  if (max_ctx < 1 || max_ctx > (int64_t(1) << 31) - 128)
-    return fail(HWKV_EINVAL, "max_ctx must be in [1, 2^31 - 128]");
+  // the decode kernels address one (unit, sequence) region with 32-bit byte
+  // offsets: round_tile(max_ctx) * head_dim * 2 must stay below 2^31
+  if (max_ctx < 1 ||
+      round_tile(max_ctx) * (int64_t)p.head_dim * 2 > (int64_t)INT32_MAX)
+    return fail(HWKV_EINVAL, "max_ctx must be >= 1 and max_ctx * head_dim * 2 "
+                             "below 2^31 (bytes of one unit's K or V)");
   const int32_t U = p.n_layers * p.n_kv_heads;
   const uint64_t D = (uint64_t)p.head_dim;
   std::vector<int64_t> win(U), cap(U), capp(U), koff(U), voff(U);

@@ -90,17 +90,21 @@ def _dev(t, dtype_name, what):
 class Policy:
     """Owns an ``hwkv_policy*``."""
 
+    _free = _lib.hwkv_policy_free  # kept alive until interpreter shutdown
+
     def __init__(self, handle):
         self.handle = handle
 
     def __del__(self):
         if getattr(self, "handle", None):
-            _lib.hwkv_policy_free(self.handle)
+            self._free(self.handle)
             self.handle = None
 
 
 class Cache:
-    """Owns an ``hwkv_cache*`` (and keeps its policy's Python object alive)."""
+    """Owns an ``hwkv_cache*``."""
+
+    _free = _lib.hwkv_cache_free
 
     def __init__(self, handle, n_layers, n_kv_heads, n_q_heads, head_dim, batch):
         self.handle = handle
@@ -114,7 +118,7 @@ class Cache:
 
     def __del__(self):
         if getattr(self, "handle", None):
-            _lib.hwkv_cache_free(self.handle)
+            self._free(self.handle)
             self.handle = None
 
 

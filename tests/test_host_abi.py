@@ -115,7 +115,7 @@ def test_cache_bytes_exact(hw):
 
 def test_cache_bytes_errors(hw):
     p = _pol(hw)
-    for B, ctx in ((0, 10), (1, 0), (1, 1 << 31)):
+    for B, ctx in ((0, 10), (1, 0), (1, 1 << 31), (1, (1 << 24) + 1)):
         with pytest.raises(hw.HwkvError) as e:
             hw.cache_bytes(p, B, ctx)
         assert e.value.code == hw.EINVAL
