@@ -31,7 +31,7 @@ HBM_PEAK_GBS = 8000.0
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--steps", type=int, default=60)
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--workload", default="ctx112k",
                     choices=["ctx112k", "ctx32k", "batch16", "pr1"])
@@ -40,6 +40,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time budget of the oracle sample")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="first run a plain device copy of MIB MiB three times, so that "
+                         "a counter run (rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE) sees a "
+                         "kernel of known traffic beside the decode kernels")
     return ap.parse_args()
 
 
@@ -59,12 +63,21 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.copy_calibration:
+        n = args.copy_calibration << 20
+        src = torch.ones(n // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     cfg = W.CONFIGS[args.workload]
     L, B = cfg["n_layers"], cfg["batch"]
     Hq, Hkv, D, S = cfg["n_q_heads"], cfg["n_kv_heads"], cfg["head_dim"], cfg["n_sinks"]
     levels = W.levels(cfg)
     windows = W.windows_of(cfg, levels)
-    total_steps = args.warmup + args.steps
+    # warmup, the timed region, then the kernel-timing region (same length)
+    total_steps = args.warmup + 2 * args.steps
     prompts = W.prompts(cfg)
     max_ctx = cfg["max_ctx"]
     if total_steps > cfg["steps"]:
@@ -75,7 +88,7 @@ def main():
 
     pol = hwkv.policy_set(L, Hkv, Hq, D, S, cfg["level_windows"], levels)
     cache = hwkv.cache_alloc(pol, B, max_ctx)
-    ws = torch.empty(hwkv.decode_workspace_bytes(cache), dtype=torch.uint8, device=dev)
+    ws = torch.zeros(hwkv.decode_workspace_bytes(cache), dtype=torch.uint8, device=dev)
     caps = [[hwkv.cache_unit_info(cache, l, h)[0] for h in range(Hkv)] for l in range(L)]
     outl = W.outlier_channels(cfg)
     osc = cfg.get("outlier_scale", 1.0)
@@ -117,29 +130,25 @@ def main():
             per_layer.append(tot)
         return per_layer
 
-    def run_step(s, ev=None):
+    def run_step(s):
         for l in range(L):
-            if ev is not None:
-                ev[l][0].record()
             if args.unfused:
                 hwkv.append(cache, l, kn[s, l], vn[s, l])
                 hwkv.decode_attn(cache, l, qs[s, l], scale, out[l], ws)
             else:
                 hwkv.append_decode_attn(cache, l, kn[s, l], vn[s, l], qs[s, l], scale, out[l], ws)
-            if ev is not None:
-                ev[l][1].record()
 
     for s in range(args.warmup):
         run_step(s)
     torch.cuda.synchronize()
 
-    evs = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)]
-            for _ in range(L)] for _ in range(args.steps)]
+    # the timed region: K steps, bracketed by events on the stream the
+    # kernels are launched on (torch's current stream)
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record()
     for i in range(args.steps):
-        run_step(args.warmup + i, evs[i])
+        run_step(args.warmup + i)
     end.record()
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(end)
@@ -149,18 +158,23 @@ def main():
     bytes_per_step = sum(bytes_steps) / args.steps
     gbs = bytes_per_step / (ms_per_step * 1e-3) / 1e9
 
-    # per-call (one layer: fused append + split + combine) durations
-    call_ms, call_bytes = [], []
+    # Kernel-timing region: the next K steps again, with the library
+    # recording HIP events on the same stream around each decode call's
+    # split kernel (the dominant kernel: it streams every resident K/V byte)
+    # and its merge kernel.
+    hwkv.decode_timing(cache, True)
     for i in range(args.steps):
-        per_layer = kv_bytes(args.warmup + i)
-        for l in range(L):
-            call_ms.append(evs[i][l][0].elapsed_time(evs[i][l][1]))
-            call_bytes.append(per_layer[l])
-    call_ms = np.array(call_ms)
-    call_bytes = np.array(call_bytes, dtype=np.float64)
-    achieved = float(call_bytes.mean() / (call_ms.mean() * 1e-3) / 1e9)
+        run_step(args.warmup + args.steps + i)
+    split_ms, merge_ms, launches = hwkv.decode_timing_read(cache)
+    hwkv.decode_timing(cache, False)
+    bytes_t = [sum(kv_bytes(args.warmup + args.steps + i)) for i in range(args.steps)]
+    split_avg_ms = split_ms / launches
+    merge_avg_ms = merge_ms / launches
+    launch_bytes = sum(bytes_t) / launches
+    achieved = launch_bytes / (split_avg_ms * 1e-3) / 1e9
 
     rate = hwkv.policy_rate(pol, max_ctx)
+    traffic, traffic_detail = measured_traffic(args)
     result = {
         "metric": METRIC,
         "value": round(gbs, 1),
@@ -188,14 +202,17 @@ def main():
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "one fused append+decode call per layer (decode_split + decode_combine)",
+            "kernel": "decode_split (split-K attention over one layer's resident K/V)",
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": None,
-            "call_us_mean": round(float(call_ms.mean()) * 1e3, 2),
-            "kv_bytes_per_call": int(call_bytes.mean()),
+            "traffic": traffic,
+            "traffic_detail": traffic_detail,
+            "launch_us_mean": round(split_avg_ms * 1e3, 2),
+            "merge_us_mean": round(merge_avg_ms * 1e3, 2),
+            "kv_bytes_per_launch": int(launch_bytes),
+            "launches_timed": int(launches),
         },
     }
 
@@ -204,6 +221,27 @@ def main():
                                               dev, ms_per_step, bytes_per_step)
     cache.free()
     print(json.dumps(result), flush=True)
+
+
+def measured_traffic(args):
+    """HBM bytes per decode_split launch from the committed counter record
+    (FETCH_SIZE + WRITE_SIZE, copy-calibrated), if it was taken on the current
+    kernel source and on this workload; otherwise None."""
+    if args.workload != "ctx112k" or args.unfused:
+        return None, None
+    from paper_2609_02029_amd import profiling
+    path = os.path.join(ROOT, "profiles", "decode_split_ctx112k_traffic.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None, None
+    if rec.get("kernel_source_sha256_16") != profiling.kernel_source_hash():
+        return None, "counter record is stale: decode kernel source changed"
+    total = rec["fetch_bytes"] + rec["write_bytes"]
+    return round(total), {"fetch_bytes": round(rec["fetch_bytes"]),
+                          "write_bytes": round(rec["write_bytes"]),
+                          "source": "profiles/decode_split_ctx112k_traffic.json"}
 
 
 def cpu_baseline(args, cfg, prompts, windows, caps, scale, outl, osc, dev, gpu_ms, step_bytes):

@@ -191,6 +191,20 @@ int hwkv_append_decode_attn(hwkv_cache *cache, int32_t layer,
                             const void *q, float scale, void *out, void *ws,
                             size_t ws_bytes, void *stream);
 
+/* Kernel timing, for profiling.  While enabled (enable != 0) on a cache,
+ * every hwkv_decode_attn / hwkv_append_decode_attn call records HIP events
+ * on its stream before its split kernel, between the split and the merge
+ * kernel, and after the merge kernel (per launch group).  The events add
+ * work to the stream; leave timing disabled when measuring end-to-end time.
+ * Disabling keeps what was recorded. */
+int hwkv_decode_timing(hwkv_cache *cache, int32_t enable);
+
+/* Waits for the recorded calls to complete and returns the summed durations
+ * of their split kernels and merge kernels in milliseconds and the number
+ * of kernel launch groups recorded, then clears the record. */
+int hwkv_decode_timing_read(hwkv_cache *cache, double *split_ms,
+                            double *merge_ms, int64_t *launches);
+
 /* Test hook: synchronously copy unit (layer, kv_head) of sequence `seq` to
  * the host after all device work completes.  host_k, host_v receive
  * [capacity][head_dim] bf16 in slot order; *n_valid = min(n, capacity), the

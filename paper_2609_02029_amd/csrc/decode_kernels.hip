@@ -75,8 +75,14 @@ constexpr int kWaves = HWKV_DECODE_WAVES;        // waves per workgroup
 constexpr int kTilesPerWave = HWKV_DECODE_TPW;   // 64-slot tiles per wave
 constexpr int kPrefetch = HWKV_DECODE_PREFETCH;  // 16-byte loads in flight
 constexpr int kMinWavesPerEU = HWKV_DECODE_MINWAVES;  // VGPR budget
-constexpr int kCombineWaves = 16;
-constexpr int kCombineUnroll = 8;
+#ifndef HWKV_COMBINE_WAVES
+#define HWKV_COMBINE_WAVES 16
+#endif
+#ifndef HWKV_COMBINE_UNROLL
+#define HWKV_COMBINE_UNROLL 8
+#endif
+constexpr int kCombineWaves = HWKV_COMBINE_WAVES;    // waves per merge group
+constexpr int kCombineUnroll = HWKV_COMBINE_UNROLL;  // splits per wave per round
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
@@ -276,6 +282,14 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
     // boundary, so that every step issues its own loads (one load PF steps
     // ahead, the step's q chunk) and does its own arithmetic, instead of the
     // compiler hoisting the loads of the whole tile and spilling.
+    // q chunks are read one step ahead of their use (qc: this step's chunk,
+    // qn: the next one), so the scalar-load latency overlaps a step of work.
+    u32x4_t qc[G];
+    {
+      const cu32x4_t *q0 = (const cu32x4_t *)qaddr;
+#pragma unroll
+      for (int h = 0; h < G; ++h) qc[h] = q0[h * NC];
+    }
     static_for<NC>([&](auto jc) {
       constexpr int j = decltype(jc)::value;
 #pragma unroll
@@ -283,14 +297,22 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
       asm volatile("" : "+v"(kofs), "+v"(vofs), "+s"(qaddr));
       const uint4 x = buf[j % PF];
       buf[j % PF] = ld(std::integral_constant<int, j + PF>{});
-      const cu32x4_t *qj = (const cu32x4_t *)qaddr;
+      u32x4_t qn[G];
+      if constexpr (j + 1 < NC) {
+        const cu32x4_t *qj = (const cu32x4_t *)qaddr;
+#pragma unroll
+        for (int h = 0; h < G; ++h) qn[h] = qj[h * NC + j + 1];
+      }
 #pragma unroll
       for (int h = 0; h < G; ++h) {
-        const u32x4_t qq = qj[h * NC + j];
-        s[h] = dot2(qq.x, x.x, s[h]);
-        s[h] = dot2(qq.y, x.y, s[h]);
-        s[h] = dot2(qq.z, x.z, s[h]);
-        s[h] = dot2(qq.w, x.w, s[h]);
+        s[h] = dot2(qc[h].x, x.x, s[h]);
+        s[h] = dot2(qc[h].y, x.y, s[h]);
+        s[h] = dot2(qc[h].z, x.z, s[h]);
+        s[h] = dot2(qc[h].w, x.w, s[h]);
+      }
+      if constexpr (j + 1 < NC) {
+#pragma unroll
+        for (int h = 0; h < G; ++h) qc[h] = qn[h];
       }
     });
 
@@ -322,6 +344,12 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
         if (has_next) buf[j % PF] = bload(krs, kofs_n + (jn - 2 * NC) * 64 * 16);
       }
     };
+    // p of a step's rows is read from LDS one step ahead (pc: this step,
+    // pn: the next), so the LDS latency overlaps a step of work.
+    int pofs = rsub * PST;
+    float pc[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) pc[h] = pl[pofs + h];
     static_for<NC>([&](auto jc) {
       constexpr int js = decltype(jc)::value;
       constexpr int j = NC + js;
@@ -330,19 +358,24 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
 #pragma unroll
         for (int e = 0; e < 8; e += 2)
           asm volatile("" : "+v"(acc[h][e]), "+v"(acc[h][e + 1]));
-      asm volatile("" : "+v"(vofs), "+v"(kofs_n));
+      asm volatile("" : "+v"(vofs), "+v"(kofs_n), "+v"(pofs));
       const uint4 x = buf[j % PF];
       issue(std::integral_constant<int, j>{});
-      const int r = js * RPS + rsub;
-      float pv[G];
+      float pn[G];
+      if constexpr (js + 1 < NC) {
 #pragma unroll
-      for (int h = 0; h < G; ++h) pv[h] = pl[r * PST + h];
+        for (int h = 0; h < G; ++h) pn[h] = pl[pofs + (js + 1) * RPS * PST + h];
+      }
       const float vf[8] = {bf_lo(x.x), bf_hi(x.x), bf_lo(x.y), bf_hi(x.y),
                            bf_lo(x.z), bf_hi(x.z), bf_lo(x.w), bf_hi(x.w)};
 #pragma unroll
       for (int h = 0; h < G; ++h)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pv[h], vf[e], acc[h][e]);
+        for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pc[h], vf[e], acc[h][e]);
+      if constexpr (js + 1 < NC) {
+#pragma unroll
+        for (int h = 0; h < G; ++h) pc[h] = pn[h];
+      }
     });
     t = tn;
     kofs = kofs_n;
@@ -403,8 +436,11 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
 
 // One workgroup per (item, query head of the group, 64-channel chunk).  Wave
 // w merges splits w, w + kCombineWaves, ...; each round issues the loads of
-// kCombineUnroll splits before using any of them, so a round costs one memory
-// round trip.  The waves are then merged in LDS.
+// kCombineUnroll splits before using any of them, so a round (up to 512
+// splits per workgroup) costs one memory round trip.  The waves are then
+// merged in LDS.  The merge is a kernel of its own: ordering the partials of
+// other workgroups inside the split kernel would need device-scope fences,
+// which write back and invalidate the L2 under every workgroup's stream.
 template <int D, int G>
 __global__ __launch_bounds__(kCombineWaves * 64) void decode_combine(
     DecodeArgs a) {
@@ -430,19 +466,16 @@ __global__ __launch_bounds__(kCombineWaves * 64) void decode_combine(
   for (int j0 = wave; j0 < ns; j0 += kCombineWaves * U) {
     float mj[U], lj[U], aj[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int j = j0 + u * kCombineWaves;
-      if (j < ns) {
-        const float *pj = base + (size_t)j * PS;
-        mj[u] = pj[h];
-        lj[u] = pj[G + h];
-        aj[u] = pj[2 * G + h * D + c];
-      } else {
-        mj[u] = -INFINITY;
-        lj[u] = 0.f;
-        aj[u] = 0.f;
-      }
+    for (int u = 0; u < U; ++u) {  // every load of the round is in flight
+      const int j = min(j0 + u * kCombineWaves, ns - 1);
+      const float *pj = base + (size_t)j * PS;
+      mj[u] = pj[h];
+      lj[u] = pj[G + h];
+      aj[u] = pj[2 * G + h * D + c];
     }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (j0 + u * kCombineWaves >= ns) mj[u] = -INFINITY;
     float Mn = M;
 #pragma unroll
     for (int u = 0; u < U; ++u) Mn = fmaxf(Mn, mj[u]);
@@ -479,42 +512,66 @@ __global__ __launch_bounds__(kCombineWaves * 64) void decode_combine(
 }
 
 template <int D, int G>
-hipError_t launch_dg(const DecodeArgs &a, int n_splits, int n_combine,
-                     hipStream_t s) {
+hipError_t launch_split_dg(const DecodeArgs &a, int n_splits, hipStream_t s) {
   hipLaunchKernelGGL((decode_split<D, G>), dim3(n_splits), dim3(kWaves * 64),
                      0, s, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || n_combine == 0) return e;
+  return hipGetLastError();
+}
+
+template <int D, int G>
+hipError_t launch_combine_dg(const DecodeArgs &a, int n_combine,
+                             hipStream_t s) {
   hipLaunchKernelGGL((decode_combine<D, G>), dim3(n_combine),
                      dim3(kCombineWaves * 64), 0, s, a);
   return hipGetLastError();
 }
 
-template <int D>
-hipError_t launch_d(int G, const DecodeArgs &a, int n_splits, int n_combine,
-                    hipStream_t s) {
-  switch (G) {
-    case 1: return launch_dg<D, 1>(a, n_splits, n_combine, s);
-    case 2: return launch_dg<D, 2>(a, n_splits, n_combine, s);
-    case 4: return launch_dg<D, 4>(a, n_splits, n_combine, s);
-    case 6: return launch_dg<D, 6>(a, n_splits, n_combine, s);
-    case 8: return launch_dg<D, 8>(a, n_splits, n_combine, s);
+// Calls f<D, G>() for the runtime (D, G) of a cache.
+template <template <int, int> class F, typename... Args>
+hipError_t dispatch_dg(int D, int G, Args &&...args) {
+#define HWKV_G(DD)                                                   \
+  switch (G) {                                                       \
+    case 1: return F<DD, 1>::run(args...);                           \
+    case 2: return F<DD, 2>::run(args...);                           \
+    case 4: return F<DD, 4>::run(args...);                           \
+    case 6: return F<DD, 6>::run(args...);                           \
+    case 8: return F<DD, 8>::run(args...);                           \
+    default: return hipErrorInvalidValue;                            \
+  }
+  switch (D) {
+    case 64: HWKV_G(64)
+    case 128: HWKV_G(128)
+    case 256: HWKV_G(256)
     default: return hipErrorInvalidValue;
   }
+#undef HWKV_G
 }
+
+template <int D, int G>
+struct SplitLaunch {
+  static hipError_t run(const DecodeArgs &a, int n, hipStream_t s) {
+    return launch_split_dg<D, G>(a, n, s);
+  }
+};
+template <int D, int G>
+struct CombineLaunch {
+  static hipError_t run(const DecodeArgs &a, int n, hipStream_t s) {
+    return launch_combine_dg<D, G>(a, n, s);
+  }
+};
 
 }  // namespace
 
 int decode_split_tokens() { return kWaves * kTilesPerWave * kTile; }
 
-hipError_t launch_decode(int D, int G, const DecodeArgs &a, int n_splits,
-                         int n_combine_blocks, hipStream_t s) {
-  switch (D) {
-    case 64: return launch_d<64>(G, a, n_splits, n_combine_blocks, s);
-    case 128: return launch_d<128>(G, a, n_splits, n_combine_blocks, s);
-    case 256: return launch_d<256>(G, a, n_splits, n_combine_blocks, s);
-    default: return hipErrorInvalidValue;
-  }
+hipError_t launch_decode_split(int D, int G, const DecodeArgs &a, int n_splits,
+                               hipStream_t s) {
+  return dispatch_dg<SplitLaunch>(D, G, a, n_splits, s);
+}
+
+hipError_t launch_decode_combine(int D, int G, const DecodeArgs &a,
+                                 int n_combine_blocks, hipStream_t s) {
+  return dispatch_dg<CombineLaunch>(D, G, a, n_combine_blocks, s);
 }
 
 }  // namespace hwkv

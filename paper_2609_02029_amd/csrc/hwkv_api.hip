@@ -36,6 +36,10 @@ struct hwkv_cache {
   size_t bytes = 0;
   bool owned = false;
   size_t ws_bytes = 0;
+  // kernel timing (profiling): events recorded by decode calls
+  bool timing = false;
+  std::vector<hipEvent_t> ev_pool;   // created events, reused
+  size_t ev_used = 0;                // events recorded since the last read
 };
 
 namespace {
@@ -147,6 +151,18 @@ int check_device(hipError_t e, const char *what) {
   return fail(HWKV_EDEVICE, std::string(what) + ": " + hipGetErrorString(e));
 }
 
+// Records the next timing event of the cache on stream s.
+int record_event(hwkv_cache *c, hipStream_t s) {
+  if (c->ev_used == c->ev_pool.size()) {
+    hipEvent_t e;
+    const int rc = check_device(hipEventCreate(&e), "hipEventCreate");
+    if (rc != HWKV_OK) return rc;
+    c->ev_pool.push_back(e);
+  }
+  return check_device(hipEventRecord(c->ev_pool[c->ev_used++], s),
+                      "hipEventRecord");
+}
+
 // Shared validation of a decode call; fills per-item lengths.
 int decode_impl(hwkv_cache *c, int32_t layer, const void *k_new,
                 const void *v_new, const void *q, float scale, void *out,
@@ -223,10 +239,17 @@ int decode_impl(hwkv_cache *c, int32_t layer, const void *k_new,
     a.ws = static_cast<float *>(ws);
     a.scale_log2 = scale * 1.4426950408889634f;
     const int n_combine = cnt * G * (p.head_dim / 64);
-    const int rc = check_device(
-        hwkv::launch_decode(p.head_dim, G, a, splits, n_combine, s),
-        "decode launch");
+    int rc;
+    if (c->timing && (rc = record_event(c, s)) != HWKV_OK) return rc;
+    rc = check_device(hwkv::launch_decode_split(p.head_dim, G, a, splits, s),
+                      "decode split launch");
     if (rc != HWKV_OK) return rc;  // earlier launches of this call may run
+    if (c->timing && (rc = record_event(c, s)) != HWKV_OK) return rc;
+    rc = check_device(
+        hwkv::launch_decode_combine(p.head_dim, G, a, n_combine, s),
+        "decode merge launch");
+    if (rc != HWKV_OK) return rc;
+    if (c->timing && (rc = record_event(c, s)) != HWKV_OK) return rc;
     ws_split += splits;
   }
   if (fused)
@@ -386,6 +409,7 @@ int hwkv_cache_alloc(hwkv_cache **out, const hwkv_policy *p, int32_t batch,
 int hwkv_cache_free(hwkv_cache *c) {
   if (!c) return ok();
   int rc = HWKV_OK;
+  for (hipEvent_t e : c->ev_pool) (void)hipEventDestroy(e);
   if (c->owned && c->base) {
     hipError_t e = hipFree(c->base);
     if (e != hipSuccess) rc = check_device(e, "hipFree");
@@ -562,6 +586,43 @@ int hwkv_append_decode_attn(hwkv_cache *c, int32_t layer, const void *k_new,
                             void *stream) {
   return decode_impl(c, layer, k_new, v_new, q, scale, out, ws, ws_bytes,
                      stream, true);
+}
+
+int hwkv_decode_timing(hwkv_cache *c, int32_t enable) {
+  if (!c) return fail(HWKV_EINVAL, "cache is null");
+  c->timing = enable != 0;
+  return ok();
+}
+
+int hwkv_decode_timing_read(hwkv_cache *c, double *split_ms, double *merge_ms,
+                            int64_t *launches) {
+  if (!c || !split_ms || !merge_ms || !launches)
+    return fail(HWKV_EINVAL, "null argument");
+  double sp = 0.0, mg = 0.0;
+  const size_t n = c->ev_used / 3;
+  if (n > 0) {
+    int rc = check_device(hipEventSynchronize(c->ev_pool[c->ev_used - 1]),
+                          "hipEventSynchronize");
+    if (rc != HWKV_OK) return rc;
+    for (size_t i = 0; i < n; ++i) {
+      float t0 = 0.f, t1 = 0.f;
+      rc = check_device(hipEventElapsedTime(&t0, c->ev_pool[3 * i],
+                                            c->ev_pool[3 * i + 1]),
+                        "hipEventElapsedTime");
+      if (rc != HWKV_OK) return rc;
+      rc = check_device(hipEventElapsedTime(&t1, c->ev_pool[3 * i + 1],
+                                            c->ev_pool[3 * i + 2]),
+                        "hipEventElapsedTime");
+      if (rc != HWKV_OK) return rc;
+      sp += t0;
+      mg += t1;
+    }
+  }
+  *split_ms = sp;
+  *merge_ms = mg;
+  *launches = (int64_t)n;
+  c->ev_used = 0;
+  return ok();
 }
 
 int hwkv_cache_read_unit(const hwkv_cache *c, int32_t layer, int32_t kv_head,

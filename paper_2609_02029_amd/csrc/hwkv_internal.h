@@ -80,8 +80,10 @@ struct AppendArgs {
 
 // Launchers (return the launch status).  D in {64, 128, 256}; G in
 // {1, 2, 4, 6, 8}.
-hipError_t launch_decode(int D, int G, const DecodeArgs &a, int n_splits,
-                         int n_combine_blocks, hipStream_t s);
+hipError_t launch_decode_split(int D, int G, const DecodeArgs &a, int n_splits,
+                               hipStream_t s);
+hipError_t launch_decode_combine(int D, int G, const DecodeArgs &a,
+                                 int n_combine_blocks, hipStream_t s);
 int decode_split_tokens();       // tokens per split (a multiple of 64)
 hipError_t launch_prefill_write(int D, const WriteArgs &a, int max_tiles,
                                 hipStream_t s);

@@ -44,6 +44,8 @@ SYMBOLS = {
     "hwkv_decode_attn": ([_vp, _i32, _vp, _flt, _vp, _vp, _sz, _vp], ctypes.c_int),
     "hwkv_append_decode_attn": ([_vp, _i32, _vp, _vp, _vp, _flt, _vp, _vp, _sz, _vp], ctypes.c_int),
     "hwkv_cache_read_unit": ([_vp, _i32, _i32, _i32, _vp, _vp, _P(_i64)], ctypes.c_int),
+    "hwkv_decode_timing": ([_vp, _i32], ctypes.c_int),
+    "hwkv_decode_timing_read": ([_vp, _P(_dbl), _P(_dbl), _P(_i64)], ctypes.c_int),
 }
 for _name, (_args, _res) in SYMBOLS.items():
     _f = getattr(_lib, _name)
@@ -259,3 +261,15 @@ def append_decode_attn(cache, layer, k_new, v_new, q, scale, out, ws, stream=Non
         cache.handle, layer, _dev(k_new, "bfloat16", "k_new"), _dev(v_new, "bfloat16", "v_new"),
         _dev(q, "bfloat16", "q"), float(scale), _dev(out, "float32", "out"), wp, wn,
         _stream(stream)))
+
+
+def decode_timing(cache, enable):
+    _check(_lib.hwkv_decode_timing(cache.handle, 1 if enable else 0))
+
+
+def decode_timing_read(cache):
+    """Returns (split_ms, merge_ms, launches) summed since the last read."""
+    sp, mg, n = _dbl(), _dbl(), _i64()
+    _check(_lib.hwkv_decode_timing_read(cache.handle, ctypes.byref(sp), ctypes.byref(mg),
+                                        ctypes.byref(n)))
+    return sp.value, mg.value, n.value

@@ -71,7 +71,7 @@ class Run:
         self.pol = hwkv.policy_set(self.L, self.Hkv, self.Hq, self.D, self.S,
                                    c["level_windows"], self.levels)
         self.cache = hwkv.cache_alloc(self.pol, self.B, self.max_ctx)
-        self.ws = torch.empty(hwkv.decode_workspace_bytes(self.cache), dtype=torch.uint8,
+        self.ws = torch.zeros(hwkv.decode_workspace_bytes(self.cache), dtype=torch.uint8,
                               device=self.dev)
         # host histories [layer][b] -> uint16 [max_ctx, Hkv, D]
         self.kh = {l: [None] * self.B for l in self.track}

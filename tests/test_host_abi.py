@@ -201,3 +201,15 @@ def test_workspace_bytes_cover_full_capacity(hw):
     assert ws.value <= (rows // 64 + 4) * part
     assert ws.value >= part * 4
     hw._lib.hwkv_cache_free(h)
+
+
+def test_decode_timing_without_calls(hw):
+    p = _pol(hw)
+    h = _fake_cache(hw, p, 1, 100)
+    L = hw._lib
+    assert L.hwkv_decode_timing(h, 1) == hw.OK
+    sp, mg, n = ctypes.c_double(), ctypes.c_double(), ctypes.c_int64()
+    assert L.hwkv_decode_timing_read(h, ctypes.byref(sp), ctypes.byref(mg), ctypes.byref(n)) == hw.OK
+    assert (sp.value, mg.value, n.value) == (0.0, 0.0, 0)
+    assert L.hwkv_decode_timing(None, 1) == hw.EINVAL
+    L.hwkv_cache_free(h)
