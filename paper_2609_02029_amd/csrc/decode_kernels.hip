@@ -75,13 +75,17 @@ constexpr int kWaves = HWKV_DECODE_WAVES;        // waves per workgroup
 constexpr int kTilesPerWave = HWKV_DECODE_TPW;   // 64-slot tiles per wave
 constexpr int kPrefetch = HWKV_DECODE_PREFETCH;  // 16-byte loads in flight
 constexpr int kMinWavesPerEU = HWKV_DECODE_MINWAVES;  // VGPR budget
-#ifndef HWKV_COMBINE_WAVES
-#define HWKV_COMBINE_WAVES 16
+#ifndef HWKV_COMBINE_THREADS
+#define HWKV_COMBINE_THREADS 1024
+#endif
+#ifndef HWKV_COMBINE_CHAN
+#define HWKV_COMBINE_CHAN 64
 #endif
 #ifndef HWKV_COMBINE_UNROLL
 #define HWKV_COMBINE_UNROLL 8
 #endif
-constexpr int kCombineWaves = HWKV_COMBINE_WAVES;    // waves per merge group
+constexpr int kCombineThreads = HWKV_COMBINE_THREADS;  // per merge workgroup
+constexpr int kCombineChan = HWKV_COMBINE_CHAN;        // channels per workgroup
 constexpr int kCombineUnroll = HWKV_COMBINE_UNROLL;  // splits per wave per round
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
@@ -434,21 +438,24 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
   }
 }
 
-// One workgroup per (item, query head of the group, 64-channel chunk).  Wave
-// w merges splits w, w + kCombineWaves, ...; each round issues the loads of
-// kCombineUnroll splits before using any of them, so a round (up to 512
-// splits per workgroup) costs one memory round trip.  The waves are then
-// merged in LDS.  The merge is a kernel of its own: ordering the partials of
-// other workgroups inside the split kernel would need device-scope fences,
-// which write back and invalidate the L2 under every workgroup's stream.
+// One workgroup per (item, query head of the group, kCombineChan-channel
+// chunk).  Thread (r, c) merges channel c of splits r, r + R, r + 2R, ...
+// (R = rows of the workgroup); each round issues the loads of kCombineUnroll
+// splits before using any of them, so a round costs one memory round trip.
+// The rows are then merged in LDS.  The merge is a kernel of its own:
+// ordering the partials of other workgroups inside the split kernel would
+// need device-scope fences, which write back and invalidate the L2 under
+// every workgroup's stream.
 template <int D, int G>
-__global__ __launch_bounds__(kCombineWaves * 64) void decode_combine(
+__global__ __launch_bounds__(kCombineThreads) void decode_combine(
     DecodeArgs a) {
-  constexpr int CH = D / 64;
+  constexpr int CW = kCombineChan < D ? kCombineChan : D;
+  constexpr int CH = D / CW;
+  constexpr int R = kCombineThreads / CW;
   constexpr int PS = G * (D + 2);
   constexpr int U = kCombineUnroll;
-  __shared__ float sM[kCombineWaves], sL[kCombineWaves];
-  __shared__ float sA[kCombineWaves][64];
+  __shared__ float sM[R], sL[R];
+  __shared__ float sA[R][CW];
   const DecodeItems &it = a.it;
   const int bid = blockIdx.x;
   const int item = bid / (G * CH);
@@ -458,16 +465,16 @@ __global__ __launch_bounds__(kCombineWaves * 64) void decode_combine(
   const int sb = it.split_begin[item];
   const int ns = it.split_begin[item + 1] - sb;
   if (ns <= 1) return;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int c = ch * 64 + lane;
+  const int r = threadIdx.x / CW, cl = threadIdx.x % CW;
+  const int c = ch * CW + cl;
   const float *base = a.ws + (size_t)(it.ws_split0 + sb) * PS;
 
   float M = -INFINITY, L = 0.f, A = 0.f;
-  for (int j0 = wave; j0 < ns; j0 += kCombineWaves * U) {
+  for (int j0 = r; j0 < ns; j0 += R * U) {
     float mj[U], lj[U], aj[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {  // every load of the round is in flight
-      const int j = min(j0 + u * kCombineWaves, ns - 1);
+      const int j = min(j0 + u * R, ns - 1);
       const float *pj = base + (size_t)j * PS;
       mj[u] = pj[h];
       lj[u] = pj[G + h];
@@ -475,7 +482,7 @@ __global__ __launch_bounds__(kCombineWaves * 64) void decode_combine(
     }
 #pragma unroll
     for (int u = 0; u < U; ++u)
-      if (j0 + u * kCombineWaves >= ns) mj[u] = -INFINITY;
+      if (j0 + u * R >= ns) mj[u] = -INFINITY;
     float Mn = M;
 #pragma unroll
     for (int u = 0; u < U; ++u) Mn = fmaxf(Mn, mj[u]);
@@ -490,22 +497,20 @@ __global__ __launch_bounds__(kCombineWaves * 64) void decode_combine(
     }
     M = Mn;
   }
-  if (lane == 0) {
-    sM[wave] = M;
-    sL[wave] = L;
+  if (cl == 0) {
+    sM[r] = M;
+    sL[r] = L;
   }
-  sA[wave][lane] = A;
+  sA[r][cl] = A;
   __syncthreads();
-  if (wave == 0) {
+  if (threadIdx.x < CW) {
     float Mx = sM[0];
-#pragma unroll
-    for (int w = 1; w < kCombineWaves; ++w) Mx = fmaxf(Mx, sM[w]);
+    for (int w = 1; w < R; ++w) Mx = fmaxf(Mx, sM[w]);
     float Lx = 0.f, Ax = 0.f;
-#pragma unroll
-    for (int w = 0; w < kCombineWaves; ++w) {
+    for (int w = 0; w < R; ++w) {
       const float f = exp2f(sM[w] - Mx);
       Lx += sL[w] * f;
-      Ax += sA[w][lane] * f;
+      Ax += sA[w][threadIdx.x] * f;
     }
     a.out[((size_t)it.q_row[item] + h) * D + c] = Ax / Lx;
   }
@@ -522,7 +527,7 @@ template <int D, int G>
 hipError_t launch_combine_dg(const DecodeArgs &a, int n_combine,
                              hipStream_t s) {
   hipLaunchKernelGGL((decode_combine<D, G>), dim3(n_combine),
-                     dim3(kCombineWaves * 64), 0, s, a);
+                     dim3(kCombineThreads), 0, s, a);
   return hipGetLastError();
 }
 
@@ -563,6 +568,9 @@ struct CombineLaunch {
 }  // namespace
 
 int decode_split_tokens() { return kWaves * kTilesPerWave * kTile; }
+int decode_combine_blocks_per_item(int D, int G) {
+  return G * (D / (kCombineChan < D ? kCombineChan : D));
+}
 
 hipError_t launch_decode_split(int D, int G, const DecodeArgs &a, int n_splits,
                                hipStream_t s) {

@@ -238,7 +238,8 @@ int decode_impl(hwkv_cache *c, int32_t layer, const void *k_new,
     a.out = static_cast<float *>(out);
     a.ws = static_cast<float *>(ws);
     a.scale_log2 = scale * 1.4426950408889634f;
-    const int n_combine = cnt * G * (p.head_dim / 64);
+    const int n_combine =
+        cnt * hwkv::decode_combine_blocks_per_item(p.head_dim, G);
     int rc;
     if (c->timing && (rc = record_event(c, s)) != HWKV_OK) return rc;
     rc = check_device(hwkv::launch_decode_split(p.head_dim, G, a, splits, s),

@@ -85,6 +85,7 @@ hipError_t launch_decode_split(int D, int G, const DecodeArgs &a, int n_splits,
 hipError_t launch_decode_combine(int D, int G, const DecodeArgs &a,
                                  int n_combine_blocks, hipStream_t s);
 int decode_split_tokens();       // tokens per split (a multiple of 64)
+int decode_combine_blocks_per_item(int D, int G);  // merge workgroups
 hipError_t launch_prefill_write(int D, const WriteArgs &a, int max_tiles,
                                 hipStream_t s);
 hipError_t launch_append(int D, const AppendArgs &a, hipStream_t s);
