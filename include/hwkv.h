@@ -156,6 +156,27 @@ int hwkv_prefill_write(hwkv_cache *cache, int32_t layer, int32_t seq,
                        int64_t pos0, int64_t n_tokens, const void *k,
                        const void *v, void *stream);
 
+/* Prefill attention of tokens [pos0, pos0 + n_tokens) of sequence `seq` in
+ * `layer`, before they are materialised: query token t (t in the chunk) of
+ * query head qh attends over R(t + 1) restricted to [0, t] of KV head
+ * qh / G -- positions s <= t with s < S or s >= t + 1 - w, every s <= t for a
+ * full unit (Eqs. conditional-attention-weight and conditional-attention,
+ * z = scale * q.k, with the sink prefix).  Keys below pos0 are read from the
+ * cache in its current state; keys in [pos0, t] from k and v.  The cache is
+ * not changed: follow with hwkv_prefill_write of the same chunk.
+ *   q     device bf16 [n_tokens][n_q_heads][head_dim], post-RoPE
+ *   k, v  device bf16 [n_tokens][n_kv_heads][head_dim], post-RoPE keys
+ *   out   device fp32 [n_tokens][n_q_heads][head_dim] (pre-gate)
+ * bf16 MFMA products with fp32 accumulation; the softmax weights enter the
+ * value product rounded to bf16.  ESTATE if pos0 != n(layer, seq);
+ * ECAPACITY if pos0 + n_tokens > max_ctx; EINVAL on bad indices, null
+ * pointers or a non-finite or non-positive scale; n_tokens == 0 is a
+ * no-op. */
+int hwkv_prefill_attn(hwkv_cache *cache, int32_t layer, int32_t seq,
+                      int64_t pos0, int64_t n_tokens, const void *q,
+                      const void *k, const void *v, float scale, void *out,
+                      void *stream);
+
 /* Append one token to every sequence of `layer`: token n_b of sequence b
  * goes to slot(n_b) of each unit (once n_b >= S + w this overwrites token
  * n_b - w, the one leaving the window), then n_b += 1.

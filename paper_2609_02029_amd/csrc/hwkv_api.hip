@@ -528,6 +528,70 @@ int hwkv_prefill_write(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0,
   return ok();
 }
 
+int hwkv_prefill_attn(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0,
+                      int64_t n_tokens, const void *q, const void *k,
+                      const void *v, float scale, void *out, void *stream) {
+  if (!c) return fail(HWKV_EINVAL, "cache is null");
+  const hwkv_policy &p = c->pol;
+  if (layer < 0 || layer >= p.n_layers || seq < 0 || seq >= c->batch)
+    return fail(HWKV_EINVAL, "layer or seq out of range");
+  if (n_tokens < 0) return fail(HWKV_EINVAL, "n_tokens must be >= 0");
+  if (!std::isfinite(scale) || !(scale > 0.0f))
+    return fail(HWKV_EINVAL, "scale must be finite and > 0");
+  if (pos0 != seq_len(c, layer, seq))
+    return fail(HWKV_ESTATE, "pos0 " + std::to_string(pos0) +
+                                 " != sequence length " +
+                                 std::to_string(seq_len(c, layer, seq)));
+  if (pos0 + n_tokens > c->max_ctx)
+    return fail(HWKV_ECAPACITY, "prefill past max_ctx");
+  if (n_tokens == 0) return ok();
+  if (!q || !k || !v || !out)
+    return fail(HWKV_EINVAL, "q, k, v and out must be non-null");
+  const int32_t H = p.n_kv_heads;
+  const int32_t G = (int32_t)group_size(p);
+  hwkv::PrefillAttnArgs a;
+  std::memset(&a, 0, sizeof a);
+  const int64_t p1 = pos0 + n_tokens;
+  std::vector<std::pair<int64_t, int32_t>> work;  // (keys of the last token, h)
+  for (int32_t h = 0; h < H; ++h) {
+    const int32_t u = layer * H + h;
+    const int64_t seq_off = (int64_t)seq * c->cap_pad[u] * p.head_dim;
+    a.head[h].k_off = c->k_off[u] + seq_off;
+    a.head[h].v_off = c->v_off[u] + seq_off;
+    a.head[h].window = (int32_t)c->window[u];
+    const int64_t w = c->window[u];
+    work.push_back({w == 0 ? p1 : std::min(p1, (int64_t)p.n_sinks + w), h});
+  }
+  std::stable_sort(work.begin(), work.end(),
+                   [](const std::pair<int64_t, int32_t> &x,
+                      const std::pair<int64_t, int32_t> &y) {
+                     return x.first > y.first;
+                   });
+  for (int32_t r = 0; r < H; ++r) a.head_order[r] = work[r].second;
+  const int64_t cols = n_tokens * G;
+  const int64_t per = hwkv::prefill_attn_columns_per_block();
+  const int64_t nb = (cols + per - 1) / per;
+  if (nb * H > (int64_t)INT32_MAX)
+    return fail(HWKV_EINVAL, "n_tokens too large for one launch");
+  a.cache = c->base;
+  a.q = static_cast<const uint16_t *>(q);
+  a.k = static_cast<const uint16_t *>(k);
+  a.v = static_cast<const uint16_t *>(v);
+  a.out = static_cast<float *>(out);
+  a.p0 = (int32_t)pos0;
+  a.n_tokens = (int32_t)n_tokens;
+  a.n_kv_heads = H;
+  a.group = G;
+  a.n_sinks = p.n_sinks;
+  a.n_col_blocks = (int32_t)nb;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  return check_device(
+             hwkv::launch_prefill_attn(p.head_dim, a, (hipStream_t)stream),
+             "prefill_attn launch") == HWKV_OK
+             ? ok()
+             : HWKV_EDEVICE;
+}
+
 int hwkv_append(hwkv_cache *c, int32_t layer, const void *k_new,
                 const void *v_new, void *stream) {
   if (!c) return fail(HWKV_EINVAL, "cache is null");

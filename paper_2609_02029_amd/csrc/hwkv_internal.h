@@ -78,6 +78,39 @@ struct AppendArgs {
   const uint16_t *v_new;
 };
 
+// Prefill attention of one chunk [p0, p0 + n_tokens) of one sequence: per
+// kv head the (unit, sequence) region offsets and canonical window; the
+// kernel's workgroups visit heads in head_order (most keys first) and each
+// head's column blocks from the last token down.
+struct PrefillAttnHead {
+  int64_t k_off;                 // element offset of the (unit, seq) K tiles
+  int64_t v_off;                 // element offset of its V rows
+  int32_t window;                // 0 = full
+  int32_t pad;
+};
+
+struct PrefillAttnArgs {
+  PrefillAttnHead head[kMaxItems];
+  int32_t head_order[kMaxItems];
+  const uint16_t *cache;
+  const uint16_t *q;             // [n_tokens][Hq][D]
+  const uint16_t *k;             // [n_tokens][Hkv][D]
+  const uint16_t *v;
+  float *out;                    // [n_tokens][Hq][D]
+  int32_t p0;
+  int32_t n_tokens;
+  int32_t n_kv_heads;
+  int32_t group;                 // G = Hq / Hkv
+  int32_t n_sinks;
+  int32_t n_col_blocks;          // per head: ceil(n_tokens * G / columns)
+  float scale_log2;              // scale * log2(e)
+};
+
+#ifndef HWKV_PREFILL_WAVES
+#define HWKV_PREFILL_WAVES 4
+#endif
+constexpr int kPrefillWaves = HWKV_PREFILL_WAVES;
+
 // Launchers (return the launch status).  D in {64, 128, 256}; G in
 // {1, 2, 4, 6, 8}.
 hipError_t launch_decode_split(int D, int G, const DecodeArgs &a, int n_splits,
@@ -89,6 +122,8 @@ int decode_combine_blocks_per_item(int D, int G);  // merge workgroups
 hipError_t launch_prefill_write(int D, const WriteArgs &a, int max_tiles,
                                 hipStream_t s);
 hipError_t launch_append(int D, const AppendArgs &a, hipStream_t s);
+int prefill_attn_columns_per_block();   // (token, q head) columns
+hipError_t launch_prefill_attn(int D, const PrefillAttnArgs &a, hipStream_t s);
 
 }  // namespace hwkv
 
@@ -96,3 +131,4 @@ hipError_t launch_append(int D, const AppendArgs &a, hipStream_t s);
 static_assert(sizeof(hwkv::DecodeArgs) <= 4096, "decode kernarg too large");
 static_assert(sizeof(hwkv::WriteArgs) <= 4096, "write kernarg too large");
 static_assert(sizeof(hwkv::AppendArgs) <= 4096, "append kernarg too large");
+static_assert(sizeof(hwkv::PrefillAttnArgs) <= 4096, "prefill kernarg too large");

@@ -39,6 +39,8 @@ SYMBOLS = {
     "hwkv_cache_seq_len": ([_vp, _i32, _i32, _P(_i64)], ctypes.c_int),
     "hwkv_cache_unit_info": ([_vp, _i32, _i32, _P(_i64), _P(_i64)], ctypes.c_int),
     "hwkv_prefill_write": ([_vp, _i32, _i32, _i64, _i64, _vp, _vp, _vp], ctypes.c_int),
+    "hwkv_prefill_attn": ([_vp, _i32, _i32, _i64, _i64, _vp, _vp, _vp, ctypes.c_float, _vp,
+                           _vp], ctypes.c_int),
     "hwkv_append": ([_vp, _i32, _vp, _vp, _vp], ctypes.c_int),
     "hwkv_decode_workspace_bytes": ([_vp, _P(_sz)], ctypes.c_int),
     "hwkv_decode_attn": ([_vp, _i32, _vp, _flt, _vp, _vp, _sz, _vp], ctypes.c_int),
@@ -222,6 +224,21 @@ def prefill_write(cache, layer, seq, pos0, k, v, stream=None):
     _check(_lib.hwkv_prefill_write(cache.handle, layer, seq, pos0, n,
                                    _dev(k, "bfloat16", "k"), _dev(v, "bfloat16", "v"),
                                    _stream(stream)))
+
+
+def prefill_attn(cache, layer, seq, pos0, q, k, v, scale, out, stream=None):
+    """``q``: bf16 [n_tokens, n_q_heads, head_dim]; ``k``, ``v``: bf16
+    [n_tokens, n_kv_heads, head_dim]; ``out``: fp32 like ``q`` (device)."""
+    n = q.shape[0]
+    if tuple(q.shape) != (n, cache.n_q_heads, cache.head_dim):
+        raise ValueError("q must be [n_tokens, n_q_heads, head_dim]")
+    if tuple(k.shape) != (n, cache.n_kv_heads, cache.head_dim) or tuple(v.shape) != tuple(k.shape):
+        raise ValueError("k and v must be [n_tokens, n_kv_heads, head_dim]")
+    if tuple(out.shape) != tuple(q.shape):
+        raise ValueError("out must be [n_tokens, n_q_heads, head_dim]")
+    _check(_lib.hwkv_prefill_attn(cache.handle, layer, seq, pos0, n, _dev(q, "bfloat16", "q"),
+                                  _dev(k, "bfloat16", "k"), _dev(v, "bfloat16", "v"),
+                                  float(scale), _dev(out, "float32", "out"), _stream(stream)))
 
 
 def append(cache, layer, k_new, v_new, stream=None):

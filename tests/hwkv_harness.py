@@ -95,6 +95,15 @@ class Run:
         v, vh = self._kv((P, self.Hkv, self.D), layer, W.V, b)
         return k, v, kh, vh
 
+    def prompt_q(self, layer, b, P):
+        """Queries of the prompt tokens, [P, Hq, D] (device, host or None)."""
+        seed = self.cfg["seed"]
+        if self.device_gen:
+            return W.normal_bf16_device((P, self.Hq, self.D), seed, layer, W.Q_PROMPT, b,
+                                        device=self.dev), None
+        a = W.normal_bf16((P, self.Hq, self.D), seed, layer, W.Q_PROMPT, b)
+        return up(a, self.dev), a
+
     def _hist(self, layer, b):
         if self.kh[layer][b] is None:
             self.kh[layer][b] = np.zeros((self.hist_len, self.Hkv, self.D), dtype=np.uint16)
@@ -115,6 +124,51 @@ class Run:
             hv[:P] = vh if vh is not None else down(v)
         self.n[layer, b] = P
         del k, v
+
+    def prefill_with_attn(self, layer, b, P=None, chunks=None, check_untouched=False):
+        """Chunked prefill with attention: per chunk [p0, p1), prefill_attn
+        of its queries over the cache as it stands plus the chunk, then
+        prefill_write of the chunk.  Returns (q device, q host or None,
+        out fp32 device [P, Hq, D])."""
+        P = self.prompts[b] if P is None else P
+        k, v, kh, vh = self.prompt_kv(layer, b, P)
+        q, qh = self.prompt_q(layer, b, P)
+        out = torch.full((P, self.Hq, self.D), float("nan"), dtype=torch.float32, device=self.dev)
+        cuts = [0] + sorted(chunks or []) + [P]
+        for p0, p1 in zip(cuts[:-1], cuts[1:]):
+            if p1 <= p0:
+                continue
+            before = self._snapshot(layer, b) if check_untouched else None
+            hwkv.prefill_attn(self.cache, layer, b, p0, q[p0:p1], k[p0:p1], v[p0:p1],
+                              self.scale, out[p0:p1])
+            if check_untouched:
+                after = self._snapshot(layer, b)
+                for x, y in zip(before, after):
+                    assert np.array_equal(x, y), "prefill_attn changed the cache"
+            hwkv.prefill_write(self.cache, layer, b, p0, k[p0:p1], v[p0:p1])
+        if layer in self.track:
+            hk, hv = self._hist(layer, b)
+            hk[:P] = kh if kh is not None else down(k)
+            hv[:P] = vh if vh is not None else down(v)
+        self.n[layer, b] = P
+        del k, v
+        return q, qh, out
+
+    def _snapshot(self, layer, b):
+        res = []
+        for h in range(self.Hkv):
+            k, v, nv = hwkv.cache_read_unit(self.cache, layer, h, b)
+            res += [k[:nv], v[:nv]]
+        return res
+
+    def oracle_rows(self, layer, b, rows, q_rows, n_threads=16):
+        """Masked-full-cache oracle for query tokens ``rows`` of sequence b:
+        each row attends over the retained set at its own position within
+        the full host history.  ``q_rows`` [len(rows), Hq, D] bf16 bits."""
+        rows = np.asarray(rows, dtype=np.int64)
+        hk, hv = self.kh[layer][b], self.vh[layer][b]
+        return oracle.decode_layer(q_rows, [hk] * len(rows), [hv] * len(rows), rows, self.S,
+                                   self.windows[layer], self.scale, n_threads=n_threads)
 
     def step(self, layer, fused=None):
         """Append one token to every sequence of ``layer`` and attend."""

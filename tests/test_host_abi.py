@@ -189,6 +189,45 @@ def test_host_error_paths_change_no_state(hw):
     L.hwkv_cache_free(h)
 
 
+def test_prefill_attn_host_errors(hw):
+    p = _pol(hw)
+    h = _fake_cache(hw, p, 2, 300)
+    L = hw._lib
+    sc = ctypes.c_float(0.125)
+    args = lambda layer=0, seq=0, pos0=0, n=10, q=FAKE, scale=sc: (
+        h, layer, seq, pos0, n, q, FAKE, FAKE, scale, FAKE, None)
+    assert L.hwkv_prefill_attn(None, 0, 0, 0, 1, FAKE, FAKE, FAKE, sc, FAKE, None) == hw.EINVAL
+    assert L.hwkv_prefill_attn(*args(layer=2)) == hw.EINVAL
+    assert L.hwkv_prefill_attn(*args(seq=2)) == hw.EINVAL
+    assert L.hwkv_prefill_attn(*args(seq=-1)) == hw.EINVAL
+    assert L.hwkv_prefill_attn(*args(n=-1)) == hw.EINVAL
+    for bad in (float("nan"), float("inf"), 0.0, -0.5):
+        assert L.hwkv_prefill_attn(*args(scale=ctypes.c_float(bad))) == hw.EINVAL
+    assert L.hwkv_prefill_attn(*args(pos0=3)) == hw.ESTATE
+    assert L.hwkv_prefill_attn(*args(n=301)) == hw.ECAPACITY
+    assert L.hwkv_prefill_attn(*args(q=None)) == hw.EINVAL
+    # an empty chunk is a no-op, null pointers allowed
+    assert L.hwkv_prefill_attn(h, 0, 0, 0, 0, None, None, None, sc, None, None) == hw.OK
+    n = ctypes.c_int64()
+    for layer in range(2):
+        for seq in range(2):
+            assert L.hwkv_cache_seq_len(h, layer, seq, ctypes.byref(n)) == hw.OK
+            assert n.value == 0
+    L.hwkv_cache_free(h)
+
+
+def test_prefill_sample_rows_rule():
+    cfg = W.CONFIGS["prefill128k"]
+    rows = W.prefill_sample_rows(cfg)
+    assert len(rows) == 512 and len(set(rows)) == 512 and rows == sorted(rows)
+    assert 0 <= rows[0] and rows[-1] < cfg["prompt"][0]
+    N, C, S = cfg["prompt"][0], cfg["chunk"], cfg["n_sinks"]
+    must = {x for p0 in range(0, N, C) for x in (p0, p0 + C - 1)}
+    must |= {S + w + d for w in (2048, 8192, 32768) for d in (-1, 0, 1)} | {S - 1, S}
+    assert must <= set(rows)
+    assert rows == W.prefill_sample_rows(cfg)
+
+
 def test_workspace_bytes_cover_full_capacity(hw):
     p = hw.policy_set(2, 4, 24, 256, 4, [2048, 8192, 32768, 0], [[0, 1, 2, 3], [3, 3, 3, 3]])
     h = _fake_cache(hw, p, 1, 114688)

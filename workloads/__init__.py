@@ -19,8 +19,9 @@ import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 
-# kinds of seeded tensors
-Q, K, V, K_NEW, V_NEW, LEVELS, PROMPTS, OUTLIERS, SAMPLE = range(9)
+# kinds of seeded tensors (Q_PROMPT: queries of the prompt tokens, for
+# prefill attention)
+Q, K, V, K_NEW, V_NEW, LEVELS, PROMPTS, OUTLIERS, SAMPLE, Q_PROMPT = range(10)
 
 FULL = 0  # window encoding: 0 = full history
 
@@ -151,6 +152,26 @@ def prompts(cfg):
     lo, hi = cfg["prompt_range"]
     r = rng(cfg["seed"], 0, PROMPTS, 0)
     return [int(x) for x in r.integers(lo, hi, size=cfg["batch"], endpoint=True)]
+
+
+def prefill_sample_rows(cfg, n_rows=512):
+    """Query rows of the long-prefill workload checked against the oracle:
+    boundary rows (each chunk's first and last token; S - 1, S, S + w - 1,
+    S + w and S + w + 1 for every finite window) and, to make up ``n_rows``,
+    rows drawn uniformly without replacement from the rest of [0, N)."""
+    N = cfg["prompt"][0]
+    S = cfg["n_sinks"]
+    edge = set()
+    for p0 in range(0, N, cfg["chunk"]):
+        edge.update((p0, min(p0 + cfg["chunk"], N) - 1))
+    for w in cfg["level_windows"]:
+        if w:
+            edge.update(t for t in (S - 1, S, S + w - 1, S + w, S + w + 1) if 0 <= t < N)
+    edge = sorted(edge)
+    rest = np.setdiff1d(np.arange(N), np.asarray(edge))
+    r = rng(cfg["seed"], 0, SAMPLE, 0)
+    extra = r.choice(rest, size=max(0, n_rows - len(edge)), replace=False)
+    return sorted(edge + [int(x) for x in extra])
 
 
 def windows_of(cfg, lv=None):
