@@ -13,6 +13,12 @@ budget, 128 decode steps after a 114,560-token prompt.
 
 Prints ONE JSON line: resident-KV GB/s (``value``), microseconds per step,
 the roofline of the dominant kernel and the oracle's CPU baseline.
+
+``--workload prefill128k`` instead times the long-prefill path: a step is a
+131,072-token prompt processed in 8,192-token chunks, each chunk's sink +
+window causal attention (``hwkv_prefill_attn``, bf16 MFMA) followed by its
+materialisation (``hwkv_prefill_write``), over KV heads with windows
+{2048, 8192, 32768, full}; ``value`` is algorithmic attention TFLOP/s.
 """
 import argparse
 import json
@@ -25,7 +31,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "decode-attn µs/step + resident-KV HBM GB/s (% of peak) at 112K ctx, 1 GPU"
+PREFILL_METRIC = "prefill-attn TFLOP/s (128K prompt in 8K chunks, sink+window causal, 1 GPU)"
 HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFS = 2500.0
 
 
 def parse():
@@ -34,7 +42,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=60)
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--workload", default="ctx112k",
-                    choices=["ctx112k", "ctx32k", "batch16", "pr1"])
+                    choices=["ctx112k", "ctx32k", "batch16", "pr1", "prefill128k"])
     ap.add_argument("--unfused", action="store_true",
                     help="time hwkv_append + hwkv_decode_attn instead of the fused call")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -63,6 +71,9 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.workload == "prefill128k":
+        prefill_main(args, dev)
+        return
     if args.copy_calibration:
         n = args.copy_calibration << 20
         src = torch.ones(n // 4, dtype=torch.float32, device=dev)
@@ -314,6 +325,168 @@ def cpu_baseline(args, cfg, prompts, windows, caps, scale, outl, osc, dev, gpu_m
                    f"sequence and query head; fp64 masked-full-history oracle, "
                    f"{spent:.1f} s of CPU time; scaled to the whole step by resident bytes"),
         "gpu_speedup": round(us_per_step / (gpu_ms * 1e3), 1),
+    }
+
+
+def prefill_pairs(N, p0, p1, S, w):
+    """Sum over query tokens t in [p0, p1) of |R(t + 1) restricted to [0, t]|:
+    t + 1 keys while t + 1 <= S + w (always for a full unit), S + w after."""
+    def upto(n):   # sum over t < n
+        if w == 0 or n <= S + w:
+            return n * (n + 1) // 2
+        c = S + w
+        return c * (c + 1) // 2 + (n - c) * c
+    return upto(p1) - upto(p0)
+
+
+def prefill_main(args, dev):
+    import numpy as np
+    import torch
+
+    import workloads as W
+    from paper_2609_02029_amd import hwkv
+
+    cfg = W.CONFIGS["prefill128k"]
+    Hq, Hkv, D, S = cfg["n_q_heads"], cfg["n_kv_heads"], cfg["head_dim"], cfg["n_sinks"]
+    G = Hq // Hkv
+    N, C = cfg["prompt"][0], cfg["chunk"]
+    windows = W.windows_of(cfg)[0]
+    scale = 1.0 / math.sqrt(D)
+    cuts = list(range(0, N, C)) + [N]
+    chunk_flop = [sum(G * prefill_pairs(N, a, b, S, w) * 4 * D for w in windows)
+                  for a, b in zip(cuts[:-1], cuts[1:])]
+    step_flop = sum(chunk_flop)
+    steps, warmup = max(1, args.steps), max(0, args.warmup)
+    if steps > 5:        # a step is a whole 128K prefill: keep the run short
+        steps = 3
+    if warmup > 2:
+        warmup = 1
+
+    pol = hwkv.policy_set(1, Hkv, Hq, D, S, cfg["level_windows"], cfg["levels"])
+    q = W.normal_bf16_device((N, Hq, D), cfg["seed"], 0, W.Q_PROMPT, 0, device=dev)
+    k = W.normal_bf16_device((N, Hkv, D), cfg["seed"], 0, W.K, 0, device=dev)
+    v = W.normal_bf16_device((N, Hkv, D), cfg["seed"], 0, W.V, 0, device=dev)
+    out = torch.empty((N, Hq, D), dtype=torch.float32, device=dev)
+    # one fresh cache per step (prefill fills it), allocated before timing
+    caches = [hwkv.cache_alloc(pol, 1, cfg["max_ctx"]) for _ in range(warmup + 2 * steps)]
+    torch.cuda.synchronize()
+
+    def run_step(cache, events=None):
+        for i, (a, b) in enumerate(zip(cuts[:-1], cuts[1:])):
+            if events is not None:
+                events[i][0].record()
+            hwkv.prefill_attn(cache, 0, 0, a, q[a:b], k[a:b], v[a:b], scale, out[a:b])
+            if events is not None:
+                events[i][1].record()
+            hwkv.prefill_write(cache, 0, 0, a, k[a:b], v[a:b])
+
+    for s in range(warmup):
+        run_step(caches[s])
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for s in range(steps):
+        run_step(caches[warmup + s])
+    end.record()
+    torch.cuda.synchronize()
+    ms_per_step = start.elapsed_time(end) / steps
+
+    # kernel-timing region: events around every attention launch
+    n_chunks = len(cuts) - 1
+    attn_ms = np.zeros(n_chunks)
+    for s in range(steps):
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(n_chunks)]
+        run_step(caches[warmup + steps + s], ev)
+        torch.cuda.synchronize()
+        attn_ms += np.array([a.elapsed_time(b) for a, b in ev])
+    attn_ms /= steps
+    attn_total_ms = float(attn_ms.sum())
+    achieved = step_flop / (attn_total_ms * 1e-3) / 1e12
+    tfs = step_flop / (ms_per_step * 1e-3) / 1e12
+
+    result = {
+        "metric": PREFILL_METRIC,
+        "value": round(tfs, 1),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 (fp32 accumulate)",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"prefill128k: {N}-token prompt in {C}-token chunks, 1 layer, batch 1, "
+                         f"{Hq} q / {Hkv} kv heads, head_dim {D}, {S} sinks, kv head windows "
+                         f"{windows} (0 = full); per chunk prefill_attn then prefill_write"),
+            "algorithmic_flop_per_step": step_flop,
+        },
+        "roofline": {
+            "bound": "mfma",
+            "kernel": "prefill_attn (bf16 MFMA sink+window causal attention of one chunk)",
+            "achieved": round(achieved, 1),
+            "peak": MFMA_BF16_PEAK_TFS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / MFMA_BF16_PEAK_TFS, 4),
+            "traffic": None,
+            "launch_ms_mean": round(attn_total_ms / n_chunks, 3),
+            "launch_ms_per_chunk": [round(x, 3) for x in attn_ms],
+            "flop_per_launch_mean": step_flop / n_chunks,
+            "launches_timed": n_chunks * steps,
+        },
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = prefill_cpu_baseline(args, cfg, q, k, v, windows, scale,
+                                                      step_flop, ms_per_step)
+    for c in caches:
+        c.free()
+    print(json.dumps(result), flush=True)
+
+
+def prefill_cpu_baseline(args, cfg, q, k, v, windows, scale, step_flop, gpu_ms):
+    """The fp64 oracle on the host cores over the parity sample rows of the
+    same workload (in order, until about ``--cpu-seconds``), scaled to the
+    whole prefill by the sampled rows' share of the algorithmic FLOP."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import workloads as W
+
+    Hq, Hkv, D, S = cfg["n_q_heads"], cfg["n_kv_heads"], cfg["head_dim"], cfg["n_sinks"]
+    G = Hq // Hkv
+    threads = max(1, min(16, os.cpu_count() or 1))
+    rows = W.prefill_sample_rows(cfg)
+    kh = k.view(torch.int16).cpu().numpy().view(np.uint16)
+    vh = v.view(torch.int16).cpu().numpy().view(np.uint16)
+    spent, flop, done = 0.0, 0, 0
+    batch = 16
+    for i in range(0, len(rows), batch):
+        rr = np.asarray(rows[i:i + batch], dtype=np.int64)
+        qr = q[torch.from_numpy(rr).to(q.device)].view(torch.int16).cpu().numpy().view(np.uint16)
+        t0 = time.perf_counter()
+        oracle.decode_layer(qr, [kh] * len(rr), [vh] * len(rr), rr, S, windows, scale,
+                            n_threads=threads)
+        spent += time.perf_counter() - t0
+        for t in rr:
+            flop += sum(G * prefill_pairs(0, int(t), int(t) + 1, S, w) * 4 * D for w in windows)
+        done += len(rr)
+        if spent >= args.cpu_seconds:
+            break
+    ms = spent / flop * step_flop * 1e3
+    return {
+        "value": round(flop / spent / 1e9, 3),
+        "unit": "GFLOP/s",
+        "ms_per_step": round(ms, 1),
+        "cores": threads,
+        "kind": "oracle",
+        "sample": (f"{done} query rows (all {Hq} heads) of the parity sample of the 128K prefill, "
+                   f"fp64 masked-full-history oracle, {spent:.1f} s of CPU time; "
+                   f"scaled to the whole prefill by algorithmic FLOP"),
+        "gpu_speedup": round(ms / gpu_ms, 1),
     }
 
 

@@ -15,14 +15,30 @@
 // 32-column block per wavefront.  Per key tile of 32 positions it computes
 //     S^T = K Q^T           (v_mfma_f32_32x32x16_bf16, K from LDS, Q^T held
 //                            in registers for the whole kernel)
-//     O^T += V^T P^T        (V^T from LDS, P^T straight from the S^T
-//                            accumulator registers)
+//     O^T += V^T P^T        (V^T from LDS by transposing reads, P^T straight
+//                            from the S^T accumulator registers)
 // In the 32x32 accumulator layout a lane owns one column and 16 key rows, so
 // the softmax max and sum are in-lane plus one swap between the two lane
 // halves.  The P^T operand needs 8 keys per lane in MFMA k order; instead of
 // moving P, the keys of each 16-key step are permuted (k index 8*half + j is
-// key 16*step + 8*(j/4) + 4*half + j%4, exactly the rows a lane already holds)
-// and V^T is stored in LDS in that permuted key order.
+// key 16*step + 8*(j/4) + 4*half + j%4, exactly the rows a lane already
+// holds), and the V^T operand is read in that key order.
+//
+// Data movement.  K and V tiles go from global memory straight into LDS
+// (global_load_lds_dwordx4: lane i of an instruction fills bytes
+// [16i, 16i + 16) of the instruction's LDS block; each lane picks its own
+// source), double-buffered, one barrier per tile, no staging registers.
+//   K tile: [D/8 chunks][32 keys][8 ch], the cache's own tile order, read as
+//           16-byte A operands (a lane's key, 8 channels) without conflicts.
+//   V tile: groups of KPG = 64 / (D/8) consecutive keys, one load
+//           instruction each, laid out [chunk][key in group][8 ch] and
+//           spaced 1 KiB + 64 B apart.  ds_read_b64_tr_b16 over a 16-lane
+//           group turns 4 keys x 16 channels of V into 4 keys of one channel
+//           per lane -- the V^T operand; the interleave and the group pad put
+//           the 4 keys' 32-byte pieces on distinct banks, and every operand
+//           address is a per-lane base plus a compile-time offset.
+// Keys past the tile's range read a zero block, so they are exact zeros
+// (and masked).
 //
 // Online softmax in base 2 with a lazy rescale: the running shift m only
 // moves when a tile's maximum exceeds it by more than 8 (log2 units), so the
@@ -32,6 +48,10 @@
 #include "hwkv_internal.h"
 
 namespace hwkv {
+
+// 16 zero bytes: the source of every key past a tile's range
+__device__ __attribute__((aligned(16))) uint32_t g_zero16[4] = {0, 0, 0, 0};
+
 namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
@@ -39,9 +59,11 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
+typedef __attribute__((address_space(3))) void lds_void_t;
 
 constexpr int kKeys = 32;                  // keys per tile
-constexpr int kVRow = kKeys * 2 + 16;      // bytes per V^T row in LDS (odd x 16)
 
 __device__ __forceinline__ u32x4_t ld16(const uint16_t *p) {
   return *reinterpret_cast<const u32x4_t *>(p);
@@ -52,10 +74,13 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
 }
 
-// Byte offset, within a V^T row, of the 4-key quad kq (keys 4kq .. 4kq+3):
-// key 16s + 8jh + 4h + jl is stored at 16s + 8h + 4jh + jl.
-__device__ __forceinline__ int quad_pos(int kq) {
-  return (4 * (kq >> 2) + 2 * (kq & 1) + ((kq >> 1) & 1)) * 8;
+// 16 bytes from global memory into the LDS block of the issuing instruction
+__device__ __forceinline__ void g2lds(const void *src, uint8_t *lds_block) {
+  __builtin_amdgcn_global_load_lds(src, (lds_void_t *)lds_block, 16, 0, 0);
+}
+
+__device__ __forceinline__ void wait_loads() {
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
 template <int D, int NW>
@@ -64,18 +89,30 @@ struct Prefill {
   static constexpr int DC = D / 8;                 // 16-byte channel chunks
   static constexpr int KS = D / 16;                // k-steps of S^T
   static constexpr int DB = D / 32;                // 32-channel blocks of O^T
-  static constexpr int KBYTES = DC * kKeys * 16;   // K tile [DC][32][8]
-  static constexpr int VBYTES = D * kVRow;         // V^T tile [D][permuted 32]
+  static constexpr int KBYTES = DC * kKeys * 16;   // K tile
+  static constexpr int NINST = KBYTES / 1024;      // 64-lane loads per tile (K or V)
+  static constexpr int KPG = 64 / DC;              // keys per V load group
+  static constexpr int VGROUP = 1024 + 64;         // bytes per V group (padded)
+  static constexpr int VBYTES = NINST * VGROUP;    // V tile
   static constexpr int STAGE = KBYTES + VBYTES;
-  static constexpr int KLD = (DC * kKeys + NT - 1) / NT;   // K chunks / thread
-  static constexpr int VLD = (D + NT - 1) / NT;            // V groups / thread
+  static_assert(NINST * KPG == kKeys, "V groups must tile the keys");
+  static_assert(NINST % NW == 0, "tile loads must split evenly over waves");
+  static constexpr int IPW = NINST / NW;           // per wave, per tile, each of K, V
 };
 
+// byte offset of (key, chunk) in a V tile
 template <int D, int NW>
-__global__ __launch_bounds__(NW * 64) void prefill_attn(const PrefillAttnArgs a) {
+__device__ __forceinline__ int vpos(int key, int chunk) {
   using P = Prefill<D, NW>;
-  constexpr int NT = P::NT, DC = P::DC, KS = P::KS, DB = P::DB;
-  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * P::STAGE];
+  return (key / P::KPG) * P::VGROUP + chunk * (16 * P::KPG) + (key % P::KPG) * 16;
+}
+
+template <int D, int NW>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
+void prefill_attn(const PrefillAttnArgs a) {
+  using P = Prefill<D, NW>;
+  constexpr int KS = P::KS, DB = P::DB, DC = P::DC, KPG = P::KPG;
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * P::STAGE];
 
   const int nb = a.n_col_blocks;
   const int h = a.head_order[blockIdx.x / nb];
@@ -113,7 +150,7 @@ __global__ __launch_bounds__(NW * 64) void prefill_attn(const PrefillAttnArgs a)
   for (int ks = 0; ks < KS; ++ks)
     qv[ks] = col_ok ? ld16(a.q + q_row + 16 * ks + 8 * half) : u32x4_t{0, 0, 0, 0};
 
-  // key ranges: [ra0, ra1) then [rb0, rb1)
+  // key ranges: [0, ra1) then [rb0, rb1)
   const int lo = (W == 0) ? 0 : max(0, ta + 1 - W);
   int ra1, rb0 = 0, rb1 = 0;
   if (lo <= S) {
@@ -131,6 +168,7 @@ __global__ __launch_bounds__(NW * 64) void prefill_attn(const PrefillAttnArgs a)
   const size_t in_stride = (size_t)a.n_kv_heads * D;
   const uint16_t *kin = a.k + (size_t)h * D;
   const uint16_t *vin = a.v + (size_t)h * D;
+  const uint16_t *zero = reinterpret_cast<const uint16_t *>(g_zero16);
 
   auto tile_range = [&](int i, int *s0, int *se) {
     if (i < na) {
@@ -141,97 +179,65 @@ __global__ __launch_bounds__(NW * 64) void prefill_attn(const PrefillAttnArgs a)
       *se = rb1;
     }
   };
-  // Cache slot of position s < p0 of a tile starting at s0: sinks and full
-  // units map to themselves; ring positions s >= b0 = max(s0, S) sit at
-  // S + ((b0 - S) mod W + (s - b0)) mod W, with s - b0 < 32.
-  struct Ring {
-    int b0, rb;
-  };
-  auto ring_of = [&](int s0) -> Ring {
-    Ring r;
-    r.b0 = max(s0, S);
-    r.rb = (W == 0) ? 0 : (r.b0 - S) % W;
-    return r;
-  };
-  auto slot_of = [&](const Ring &r, int s) -> int {
-    if (W == 0 || s < S) return s;
-    int off = r.rb + (s - r.b0);
-    while (off >= W) off -= W;
-    return S + off;
-  };
 
-  // staging registers of the next tile
-  u32x4_t kreg[P::KLD];
-  u32x4_t vreg[P::VLD][4];
-
-  auto stage_load = [&](int i) {
+  // Issues this wave's share of tile i's K and V loads into stage buf.
+  // Cache slot of a position s < p0 of a tile starting at s0: sinks and
+  // full units map to themselves; ring positions s >= b0 = max(s0, S) sit
+  // at S + ((b0 - S) mod W + (s - b0)) mod W, with s - b0 < 32.
+  auto issue_loads = [&](int i, int buf) {
     int s0, se;
     tile_range(i, &s0, &se);
-    const Ring rg = ring_of(s0);
-#pragma unroll
-    for (int j = 0; j < P::KLD; ++j) {
-      const int e = tid + j * NT;
-      const int key = e & (kKeys - 1), dc = e / kKeys;
-      const int s = s0 + key;
-      u32x4_t x = {0, 0, 0, 0};
-      if (e < DC * kKeys && s < se) {
-        if (s >= p0) {
-          x = ld16(kin + (size_t)(s - p0) * in_stride + dc * 8);
-        } else {
-          const int sl = slot_of(rg, s);
-          x = ld16(kc + ((sl >> 6) * DC + dc) * (kTile * 8) + (sl & 63) * 8);
-        }
-      }
-      kreg[j] = x;
-    }
-#pragma unroll
-    for (int j = 0; j < P::VLD; ++j) {
-      const int gi = tid + j * NT;
-      const int kq = gi & 7, dc = gi >> 3;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int s = s0 + 4 * kq + e;
-        u32x4_t x = {0, 0, 0, 0};
-        if (gi < D && s < se) {
-          if (s >= p0)
-            x = ld16(vin + (size_t)(s - p0) * in_stride + dc * 8);
-          else
-            x = ld16(vc + slot_of(rg, s) * D + dc * 8);
-        }
-        vreg[j][e] = x;
-      }
-    }
-  };
-
-  auto stage_store = [&](int buf) {
+    const int b0 = max(s0, S);
+    const int rb = (W == 0) ? 0 : (b0 - S) % W;
+    auto slot_of = [&](int s) -> int {
+      if (W == 0 || s < S) return s;
+      int off = rb + (s - b0);                     // < W + 32
+      if (off >= W) off -= W;
+      if (W < kKeys)                               // uniform: tiny windows only
+        while (off >= W) off -= W;
+      return S + off;
+    };
     uint8_t *kl = smem + buf * P::STAGE;
     uint8_t *vl = kl + P::KBYTES;
-#pragma unroll
-    for (int j = 0; j < P::KLD; ++j) {
-      const int e = tid + j * NT;
-      if (e < DC * kKeys)
-        *reinterpret_cast<u32x4_t *>(kl + e * 16) = kreg[j];
-    }
-#pragma unroll
-    for (int j = 0; j < P::VLD; ++j) {
-      const int gi = tid + j * NT;
-      if (gi < D) {
-        const int kq = gi & 7, dc = gi >> 3;
-        uint8_t *dst = vl + (dc * 8) * kVRow + quad_pos(kq);
-#pragma unroll
-        for (int m = 0; m < 4; ++m) {
-          // channels 2m (low halves) and 2m + 1 (high halves) of 4 keys
-          uint32_t x0 = vreg[j][0][m], x1 = vreg[j][1][m];
-          uint32_t x2 = vreg[j][2][m], x3 = vreg[j][3][m];
-          uint2 lo2, hi2;
-          lo2.x = (x0 & 0xFFFFu) | (x1 << 16);
-          lo2.y = (x2 & 0xFFFFu) | (x3 << 16);
-          hi2.x = (x0 >> 16) | (x1 & 0xFFFF0000u);
-          hi2.y = (x2 >> 16) | (x3 & 0xFFFF0000u);
-          *reinterpret_cast<uint2 *>(dst + (2 * m) * kVRow) = lo2;
-          *reinterpret_cast<uint2 *>(dst + (2 * m + 1) * kVRow) = hi2;
-        }
+    // K: instruction n covers chunks 2n, 2n + 1 of the 32 keys; this lane's
+    // key is cl, its chunk 2n + half.
+    {
+      const int s = s0 + cl;
+      const uint16_t *base;
+      int step;
+      if (s >= se) {
+        base = zero;
+        step = 0;
+      } else if (s >= p0) {
+        base = kin + (size_t)(s - p0) * in_stride;
+        step = 8;
+      } else {
+        const int sl = slot_of(s);
+        base = kc + (size_t)((sl >> 6) * DC) * (kTile * 8) + (sl & 63) * 8;
+        step = kTile * 8;
       }
+#pragma unroll
+      for (int j = 0; j < P::IPW; ++j) {
+        const int n = wave + j * NW;
+        g2lds(base + (2 * n + half) * step, kl + n * 1024);
+      }
+    }
+    // V: instruction n fills group n: key KPG * n + lane % KPG, chunk
+    // lane / KPG.
+#pragma unroll
+    for (int j = 0; j < P::IPW; ++j) {
+      const int n = wave + j * NW;
+      const int key = KPG * n + lane % KPG;
+      const int ch = lane / KPG;
+      const int s = s0 + key;
+      const uint16_t *src;
+      if (s >= se)
+        src = zero;
+      else if (s >= p0)
+        src = vin + (size_t)(s - p0) * in_stride + ch * 8;
+      else
+        src = vc + (size_t)slot_of(s) * D + ch * 8;
+      g2lds(src, vl + n * P::VGROUP);
     }
   };
 
@@ -245,89 +251,100 @@ __global__ __launch_bounds__(NW * 64) void prefill_attn(const PrefillAttnArgs a)
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[db][r] = 0.0f;
 
-  if (ntiles > 0) {
-    stage_load(0);
-    stage_store(0);
-  }
-  __syncthreads();
+  // V^T operand addressing: 16-lane group gq = lane / 16, local lane mq.
+  // For k-step s and half hh of the 8 keys, lane (gq, mq) reads 8 bytes of
+  // key 16s + 8hh + 4(gq / 2) + mq / 4 at channel 32db + 16(gq % 2) + 4(mq % 4);
+  // the lane-dependent part of the address is fixed, the rest a constant.
+  const int gq = lane >> 4, mq = lane & 15;
+  const int vkey0 = 4 * (gq >> 1) + (mq >> 2);
+  const int vch = 16 * (gq & 1) + 4 * (mq & 3);            // channel within the 32-block
+  const int vlane = vpos<D, NW>(vkey0, vch >> 3) + (vch & 7) * 2;
+
+  if (ntiles > 0) issue_loads(0, 0);
 
   for (int i = 0; i < ntiles; ++i) {
-    if (i + 1 < ntiles) stage_load(i + 1);
+    wait_loads();
+    __syncthreads();
+    if (i + 1 < ntiles) issue_loads(i + 1, (i + 1) & 1);
     int s0, se;
     tile_range(i, &s0, &se);
     const int slast = min(s0 + kKeys, se) - 1;
     const bool skip = !wave_live || s0 > t_hi ||
                       (W != 0 && s0 >= S && slast < t_lo + 1 - W);
-    if (!skip) {
-      const uint8_t *kl = smem + (i & 1) * P::STAGE;
-      const uint8_t *vl = kl + P::KBYTES;
-      f32x16_t st;
+    if (skip) continue;
+    const uint8_t *kl = smem + (i & 1) * P::STAGE;
+    const uint8_t *vl = kl + P::KBYTES + vlane;
+    f32x16_t st;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) st[r] = 0.0f;
+    for (int r = 0; r < 16; ++r) st[r] = 0.0f;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const u32x4_t kx =
-            *reinterpret_cast<const u32x4_t *>(kl + ((2 * ks + half) * kKeys + cl) * 16);
-        st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            __builtin_bit_cast(bf16x8_t, kx), __builtin_bit_cast(bf16x8_t, qv[ks]), st, 0,
-            0, 0);
-      }
-      const bool full_vis = s0 + kKeys <= se && slast <= t_lo &&
-                            (W == 0 || slast < S || s0 >= t_hi + 1 - W);
-      if (!full_vis) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int s = s0 + (r >> 2) * 8 + half * 4 + (r & 3);
-          const bool vis = s < se && s <= t && (W == 0 || s < S || s >= t + 1 - W);
-          if (!vis) st[r] = -__builtin_inff();
-        }
-      }
-      float mx = st[0];
-#pragma unroll
-      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, st[r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      if (__any(mx > m + tau)) {
-        const float mn = fmaxf(m, mx);
-        const float alpha = __builtin_amdgcn_exp2f((m - mn) * c2);
-        m = mn;
-        l *= alpha;
-#pragma unroll
-        for (int db = 0; db < DB; ++db)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
-      }
-      const float mc = m * c2;
-      float pr[16];
+    for (int ks = 0; ks < KS; ++ks) {
+      const u32x4_t kx =
+          *reinterpret_cast<const u32x4_t *>(kl + ((2 * ks + half) * kKeys + cl) * 16);
+      st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+          __builtin_bit_cast(bf16x8_t, kx), __builtin_bit_cast(bf16x8_t, qv[ks]), st, 0, 0, 0);
+    }
+    const bool full_vis = s0 + kKeys <= se && slast <= t_lo &&
+                          (W == 0 || slast < S || s0 >= t_hi + 1 - W);
+    if (!full_vis) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        pr[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(st[r], c2, -mc));
-        l += pr[r];
-      }
-      u32x4_t pb[2];
-#pragma unroll
-      for (int s = 0; s < 2; ++s)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) pb[s][j] = pack_bf16(pr[8 * s + 2 * j], pr[8 * s + 2 * j + 1]);
-#pragma unroll
-      for (int db = 0; db < DB; ++db) {
-#pragma unroll
-        for (int s = 0; s < 2; ++s) {
-          const u32x4_t vx = *reinterpret_cast<const u32x4_t *>(
-              vl + (32 * db + cl) * kVRow + 32 * s + 16 * half);
-          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              __builtin_bit_cast(bf16x8_t, vx), __builtin_bit_cast(bf16x8_t, pb[s]), o[db],
-              0, 0, 0);
-        }
+        const int s = s0 + (r >> 2) * 8 + half * 4 + (r & 3);
+        const bool vis = s < se && s <= t && (W == 0 || s < S || s >= t + 1 - W);
+        if (!vis) st[r] = -__builtin_inff();
       }
     }
-    if (i + 1 < ntiles) stage_store((i + 1) & 1);
-    __syncthreads();
+    float mx = st[0];
+#pragma unroll
+    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, st[r]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    if (__any(mx > m + tau)) {
+      const float mn = fmaxf(m, mx);
+      const float alpha = __builtin_amdgcn_exp2f((m - mn) * c2);
+      m = mn;
+      l *= alpha;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+    }
+    const float mc = m * c2;
+    float pr[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      pr[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(st[r], c2, -mc));
+      l += pr[r];
+    }
+    u32x4_t pb[2];
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) pb[s][j] = pack_bf16(pr[8 * s + 2 * j], pr[8 * s + 2 * j + 1]);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        i16x4_t v2[2];
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
+          v2[hh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (lds_i16x4_t *)(vl + vpos<D, NW>(16 * s + 8 * hh, 4 * db)));
+        const bf16x8_t va = __builtin_bit_cast(
+            bf16x8_t, __builtin_shufflevector(v2[0], v2[1], 0, 1, 2, 3, 4, 5, 6, 7));
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            va, __builtin_bit_cast(bf16x8_t, pb[s]), o[db], 0, 0, 0);
+      }
+    }
   }
 
   if (!col_ok) return;
   const float lt = l + __shfl_xor(l, 32);
   const float inv = 1.0f / lt;
-  float *orow = a.out + q_row;
+  // the output row, recomputed here rather than kept live through the loop
+  int c_out = c;
+  asm volatile("" : "+v"(c_out));
+  const int tl_o = c_out / G, g_o = c_out - tl_o * G;
+  float *orow = a.out + ((size_t)tl_o * Hq + (size_t)h * G + g_o) * D;
 #pragma unroll
   for (int db = 0; db < DB; ++db)
 #pragma unroll
