@@ -226,7 +226,6 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
       *reinterpret_cast<uint4 *>(vbase + (size_t)new_slot * D + g * 8) =
           *reinterpret_cast<const uint4 *>(a.v_new + src + g * 8);
     }
-    __threadfence();
   }
 
   float m[G], l[G], acc[G][8];
@@ -238,8 +237,12 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
     for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
   }
   float *pl = sm.u.p[wave];
+  // Only this workgroup reads the new slot in this launch: a workgroup-scope
+  // release/acquire around the barrier orders the store before its loads
+  // (agent scope would write back and invalidate the whole L2).
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
   __syncthreads();
-  if (writes_new) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 
   // K: every tile up to the last occupied one; V: rows [0, nv) only
   const __amdgpu_buffer_rsrc_t krs =

@@ -28,17 +28,22 @@
 // (global_load_lds_dwordx4: lane i of an instruction fills bytes
 // [16i, 16i + 16) of the instruction's LDS block; each lane picks its own
 // source), double-buffered, one barrier per tile, no staging registers.
-//   K tile: [D/8 chunks][32 keys][8 ch], the cache's own tile order, read as
-//           16-byte A operands (a lane's key, 8 channels) without conflicts.
-//   V tile: groups of KPG = 64 / (D/8) consecutive keys, one load
-//           instruction each, laid out [chunk][key in group][8 ch] and
-//           spaced 1 KiB + 64 B apart.  ds_read_b64_tr_b16 over a 16-lane
-//           group turns 4 keys x 16 channels of V into 4 keys of one channel
-//           per lane -- the V^T operand; the interleave and the group pad put
-//           the 4 keys' 32-byte pieces on distinct banks, and every operand
-//           address is a per-lane base plus a compile-time offset.
-// Keys past the tile's range read a zero block, so they are exact zeros
-// (and masked).
+// Both tiles are stored as rows of one 16-byte channel chunk for the 32
+// keys (512 B), two rows per load instruction; in odd rows key k sits at
+// position k ^ 4.  Lane L of every load then fetches key (L % 32) ^
+// (4 (L / 32)) -- one key per lane and tile, so its cache slot and row
+// addresses are worked out once per tile -- at chunk 2n + L / 32.
+//   K tile: rows contiguous.  The S^T operand (a lane's key, 8 channels of
+//           one chunk) is one 16-byte read; a half-wave reads a whole row.
+//   V tile: row pairs spaced 1 KiB + 128 B apart.  ds_read_b64_tr_b16 over
+//           a 16-lane group turns 4 keys x 16 channels of V into 4 keys of
+//           one channel per lane -- the V^T operand.  A half-wave (two
+//           16-lane groups: the same 4 keys, adjacent 16-channel pieces)
+//           touches four 64-byte pieces that the odd-row swizzle and the pair
+//           pad place on disjoint banks of the 256-byte-wide LDS.
+// Every operand address is a per-lane base plus a compile-time offset.
+// Keys past the tile's range read a zero row, so they are exact zeros (and
+// masked).
 //
 // Online softmax in base 2 with a lazy rescale: the running shift m only
 // moves when a tile's maximum exceeds it by more than 8 (log2 units), so the
@@ -49,8 +54,8 @@
 
 namespace hwkv {
 
-// 16 zero bytes: the source of every key past a tile's range
-__device__ __attribute__((aligned(16))) uint32_t g_zero16[4] = {0, 0, 0, 0};
+// A zero row (head_dim <= 256): the source of every key past a tile's range
+__device__ __attribute__((aligned(16))) uint32_t g_zero_row[128] = {};
 
 namespace {
 
@@ -85,33 +90,23 @@ __device__ __forceinline__ void wait_loads() {
 
 template <int D, int NW>
 struct Prefill {
-  static constexpr int NT = NW * 64;
   static constexpr int DC = D / 8;                 // 16-byte channel chunks
   static constexpr int KS = D / 16;                // k-steps of S^T
   static constexpr int DB = D / 32;                // 32-channel blocks of O^T
-  static constexpr int KBYTES = DC * kKeys * 16;   // K tile
-  static constexpr int NINST = KBYTES / 1024;      // 64-lane loads per tile (K or V)
-  static constexpr int KPG = 64 / DC;              // keys per V load group
-  static constexpr int VGROUP = 1024 + 64;         // bytes per V group (padded)
-  static constexpr int VBYTES = NINST * VGROUP;    // V tile
+  static constexpr int NINST = DC / 2;             // loads per tile (K or V), 2 rows each
+  static constexpr int KBYTES = NINST * 1024;      // K tile
+  static constexpr int VPAIR = 1024 + 128;         // bytes per V row pair (padded)
+  static constexpr int VBYTES = NINST * VPAIR;     // V tile
   static constexpr int STAGE = KBYTES + VBYTES;
-  static_assert(NINST * KPG == kKeys, "V groups must tile the keys");
   static_assert(NINST % NW == 0, "tile loads must split evenly over waves");
-  static constexpr int IPW = NINST / NW;           // per wave, per tile, each of K, V
+  static constexpr int IPW = NINST / NW;           // per wave and tile, each of K, V
 };
-
-// byte offset of (key, chunk) in a V tile
-template <int D, int NW>
-__device__ __forceinline__ int vpos(int key, int chunk) {
-  using P = Prefill<D, NW>;
-  return (key / P::KPG) * P::VGROUP + chunk * (16 * P::KPG) + (key % P::KPG) * 16;
-}
 
 template <int D, int NW>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void prefill_attn(const PrefillAttnArgs a) {
   using P = Prefill<D, NW>;
-  constexpr int KS = P::KS, DB = P::DB, DC = P::DC, KPG = P::KPG;
+  constexpr int KS = P::KS, DB = P::DB, DC = P::DC;
   __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * P::STAGE];
 
   const int nb = a.n_col_blocks;
@@ -168,7 +163,7 @@ void prefill_attn(const PrefillAttnArgs a) {
   const size_t in_stride = (size_t)a.n_kv_heads * D;
   const uint16_t *kin = a.k + (size_t)h * D;
   const uint16_t *vin = a.v + (size_t)h * D;
-  const uint16_t *zero = reinterpret_cast<const uint16_t *>(g_zero16);
+  const uint16_t *zero = reinterpret_cast<const uint16_t *>(g_zero_row);
 
   auto tile_range = [&](int i, int *s0, int *se) {
     if (i < na) {
@@ -180,64 +175,59 @@ void prefill_attn(const PrefillAttnArgs a) {
     }
   };
 
-  // Issues this wave's share of tile i's K and V loads into stage buf.
-  // Cache slot of a position s < p0 of a tile starting at s0: sinks and
-  // full units map to themselves; ring positions s >= b0 = max(s0, S) sit
-  // at S + ((b0 - S) mod W + (s - b0)) mod W, with s - b0 < 32.
+  // The key this lane loads in every tile.
+  const int lkey = cl ^ (4 * half);
+  // Ring slot of the load tile's positions: positions s >= b0 = max(s0, S)
+  // sit at S + (rb + s - b0) mod W with rb = (b0 - S) mod W; rb follows b0
+  // from tile to tile (b0 never decreases).
+  int ld_b0 = S, ld_rb = 0;
   auto issue_loads = [&](int i, int buf) {
     int s0, se;
     tile_range(i, &s0, &se);
     const int b0 = max(s0, S);
-    const int rb = (W == 0) ? 0 : (b0 - S) % W;
-    auto slot_of = [&](int s) -> int {
-      if (W == 0 || s < S) return s;
-      int off = rb + (s - b0);                     // < W + 32
-      if (off >= W) off -= W;
-      if (W < kKeys)                               // uniform: tiny windows only
-        while (off >= W) off -= W;
-      return S + off;
-    };
+    if (W != 0) {
+      const int step = b0 - ld_b0;
+      int rb = ld_rb + step;
+      if (step > kKeys || W < kKeys)
+        rb %= W;                                   // range switch, tiny windows
+      else
+        rb = rb >= W ? rb - W : rb;
+      ld_rb = rb;
+    }
+    ld_b0 = b0;
+    const int s = s0 + lkey;
+    const uint16_t *kp, *vp;
+    int kstep;                                     // elements per K chunk
+    if (s >= se) {
+      kp = zero;
+      vp = zero;
+      kstep = 8;
+    } else if (s >= p0) {
+      kp = kin + (size_t)(s - p0) * in_stride;
+      vp = vin + (size_t)(s - p0) * in_stride;
+      kstep = 8;
+    } else {
+      int sl = s;
+      if (W != 0 && s >= S) {
+        int off = ld_rb + (s - b0);                // < W + 32
+        if (W >= kKeys)
+          off = off >= W ? off - W : off;
+        else
+          off = off % W;                           // tiny windows only
+        sl = S + off;
+      }
+      kp = kc + (size_t)((sl >> 6) * DC) * (kTile * 8) + (sl & 63) * 8;
+      vp = vc + (size_t)sl * D;
+      kstep = kTile * 8;
+    }
     uint8_t *kl = smem + buf * P::STAGE;
     uint8_t *vl = kl + P::KBYTES;
-    // K: instruction n covers chunks 2n, 2n + 1 of the 32 keys; this lane's
-    // key is cl, its chunk 2n + half.
-    {
-      const int s = s0 + cl;
-      const uint16_t *base;
-      int step;
-      if (s >= se) {
-        base = zero;
-        step = 0;
-      } else if (s >= p0) {
-        base = kin + (size_t)(s - p0) * in_stride;
-        step = 8;
-      } else {
-        const int sl = slot_of(s);
-        base = kc + (size_t)((sl >> 6) * DC) * (kTile * 8) + (sl & 63) * 8;
-        step = kTile * 8;
-      }
-#pragma unroll
-      for (int j = 0; j < P::IPW; ++j) {
-        const int n = wave + j * NW;
-        g2lds(base + (2 * n + half) * step, kl + n * 1024);
-      }
-    }
-    // V: instruction n fills group n: key KPG * n + lane % KPG, chunk
-    // lane / KPG.
 #pragma unroll
     for (int j = 0; j < P::IPW; ++j) {
       const int n = wave + j * NW;
-      const int key = KPG * n + lane % KPG;
-      const int ch = lane / KPG;
-      const int s = s0 + key;
-      const uint16_t *src;
-      if (s >= se)
-        src = zero;
-      else if (s >= p0)
-        src = vin + (size_t)(s - p0) * in_stride + ch * 8;
-      else
-        src = vc + (size_t)slot_of(s) * D + ch * 8;
-      g2lds(src, vl + n * P::VGROUP);
+      const int ch = 2 * n + half;
+      g2lds(kp + ch * kstep, kl + n * 1024);
+      g2lds(vp + ch * 8, vl + n * P::VPAIR);
     }
   };
 
@@ -251,14 +241,16 @@ void prefill_attn(const PrefillAttnArgs a) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[db][r] = 0.0f;
 
-  // V^T operand addressing: 16-lane group gq = lane / 16, local lane mq.
-  // For k-step s and half hh of the 8 keys, lane (gq, mq) reads 8 bytes of
-  // key 16s + 8hh + 4(gq / 2) + mq / 4 at channel 32db + 16(gq % 2) + 4(mq % 4);
-  // the lane-dependent part of the address is fixed, the rest a constant.
+  // S^T operand: key cl of chunk row 2ks + half (odd rows swizzled).
+  const int klane = half * 512 + lkey * 16;
+  // V^T operand: 16-lane group gq = lane / 16, local lane mq.  For k-step s
+  // and half hh of its 8 keys, lane (gq, mq) reads 8 bytes of key
+  // 16s + 8hh + 4(gq / 2) + mq / 4 at channel 32db + 16(gq % 2) + 4(mq % 4),
+  // i.e. in chunk row 4db + 2(gq % 2) + (mq % 4) / 2 of parity (mq / 2) % 2.
   const int gq = lane >> 4, mq = lane & 15;
+  const int vpar = (mq >> 1) & 1;
   const int vkey0 = 4 * (gq >> 1) + (mq >> 2);
-  const int vch = 16 * (gq & 1) + 4 * (mq & 3);            // channel within the 32-block
-  const int vlane = vpos<D, NW>(vkey0, vch >> 3) + (vch & 7) * 2;
+  const int vlane = (gq & 1) * P::VPAIR + vpar * 512 + (vkey0 ^ (4 * vpar)) * 16 + (mq & 1) * 8;
 
   if (ntiles > 0) issue_loads(0, 0);
 
@@ -272,15 +264,14 @@ void prefill_attn(const PrefillAttnArgs a) {
     const bool skip = !wave_live || s0 > t_hi ||
                       (W != 0 && s0 >= S && slast < t_lo + 1 - W);
     if (skip) continue;
-    const uint8_t *kl = smem + (i & 1) * P::STAGE;
-    const uint8_t *vl = kl + P::KBYTES + vlane;
+    const uint8_t *kl = smem + (i & 1) * P::STAGE + klane;
+    const uint8_t *vl = smem + (i & 1) * P::STAGE + P::KBYTES + vlane;
     f32x16_t st;
 #pragma unroll
     for (int r = 0; r < 16; ++r) st[r] = 0.0f;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      const u32x4_t kx =
-          *reinterpret_cast<const u32x4_t *>(kl + ((2 * ks + half) * kKeys + cl) * 16);
+      const u32x4_t kx = *reinterpret_cast<const u32x4_t *>(kl + ks * 1024);
       st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
           __builtin_bit_cast(bf16x8_t, kx), __builtin_bit_cast(bf16x8_t, qv[ks]), st, 0, 0, 0);
     }
@@ -328,7 +319,7 @@ void prefill_attn(const PrefillAttnArgs a) {
 #pragma unroll
         for (int hh = 0; hh < 2; ++hh)
           v2[hh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (lds_i16x4_t *)(vl + vpos<D, NW>(16 * s + 8 * hh, 4 * db)));
+              (lds_i16x4_t *)(vl + 2 * db * P::VPAIR + (16 * s + 8 * hh) * 16));
         const bf16x8_t va = __builtin_bit_cast(
             bf16x8_t, __builtin_shufflevector(v2[0], v2[1], 0, 1, 2, 3, 4, 5, 6, 7));
         o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(

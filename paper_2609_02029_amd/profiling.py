@@ -1,14 +1,23 @@
-"""Summaries of rocprofv3 results databases for the decode kernels.
+"""Summaries of rocprofv3 results databases for the hwkv kernels.
 
 ``python -m paper_2609_02029_amd.profiling kernels DB``     per-kernel durations
 ``python -m paper_2609_02029_amd.profiling traffic DB_FETCH DB_WRITE MIB``
-``python -m paper_2609_02029_amd.profiling record DB_FETCH DB_WRITE MIB``
-    the decode_split line of the traffic table as JSON, with the hash of the
-    kernel source it was measured on
     HBM traffic per dispatch of each kernel from a FETCH_SIZE run and a
     WRITE_SIZE run, each scaled by what the counter reads for the plain copy
     of MIB MiB that ``bench.py --copy-calibration MIB`` performs first
     (expected: MIB MiB read and MIB MiB written per copy).
+``python -m paper_2609_02029_amd.profiling record DB_FETCH DB_WRITE MIB [KERNEL]``
+    one kernel's line of the traffic table as JSON (default the decode split
+    kernel; ``prefill_attn`` for the prefill attention kernel), with the hash
+    of the kernel source it was measured on
+``python -m paper_2609_02029_amd.profiling mfma DB``
+    MFMA busy fraction and bf16 MFMA FLOP per dispatch of every kernel that
+    issued MFMA, from a run with SQ_VALU_MFMA_BUSY_CYCLES,
+    SQ_INSTS_VALU_MFMA_MOPS_BF16 and GRBM_GUI_ACTIVE (busy cycles summed over
+    the 1024 SIMDs over the GPU's active cycles; one MOP = 512 FLOP)
+``python -m paper_2609_02029_amd.profiling lds DB``
+    LDS bank-conflict and LDS-active cycles per dispatch (SQ_LDS_BANK_CONFLICT,
+    SQ_LDS_IDX_ACTIVE, GRBM_GUI_ACTIVE), as fractions of CU cycles
 """
 import collections
 import hashlib
@@ -19,7 +28,13 @@ import sqlite3
 import statistics
 import sys
 
-KERNELS = r"(decode_split<[^>]*>|decode_combine<[^>]*>|prefill_write<[^>]*>|append_token<[^>]*>)"
+KERNELS = (r"(decode_split<[^>]*>|decode_combine<[^>]*>|prefill_write<[^>]*>|append_token<[^>]*>"
+           r"|prefill_attn<[^>]*>)")
+N_SIMD = 1024   # 256 CUs x 4 SIMDs
+N_CU = 256
+# GRBM_GUI_ACTIVE comes back as one value per dispatch that sums the active
+# cycles of the 8 XCDs (an 8.9 ms dispatch reads 1.59e8 = 8 x 2.2 GHz x 8.9 ms)
+N_XCD = 8
 
 
 def short(name):
@@ -43,17 +58,50 @@ def kernels(db):
     return out
 
 
-def counter(db, name):
-    """{dispatch id: (kernel, value summed over the counter's instances)}."""
+def counter(db, name, reduce="sum"):
+    """{dispatch id: (kernel, value reduced over the counter's instances)}."""
     cur = sqlite3.connect(db).cursor()
-    vals = collections.defaultdict(float)
+    vals = {}
     kern = {}
     for did, kn, cn, v in cur.execute(
             "select dispatch_id, kernel_name, counter_name, value from counters_collection"):
         if cn == name:
-            vals[did] += v
+            if did not in vals:
+                vals[did] = v
+            elif reduce == "sum":
+                vals[did] += v
+            else:
+                vals[did] = max(vals[did], v)
             kern[did] = short(kn)
     return {d: (kern[d], vals[d]) for d in vals}
+
+
+def mfma(db):
+    busy = counter(db, "SQ_VALU_MFMA_BUSY_CYCLES")
+    mops = counter(db, "SQ_INSTS_VALU_MFMA_MOPS_BF16")
+    act = counter(db, "GRBM_GUI_ACTIVE", reduce="max")
+    rows = []
+    for d in sorted(busy):
+        k, b = busy[d]
+        if b <= 0 or d not in act:
+            continue
+        cyc = act[d][1] / N_XCD
+        rows.append((d, k, b / (cyc * N_SIMD), mops.get(d, (k, 0.0))[1] * 512, cyc))
+    return rows
+
+
+def lds(db):
+    conf = counter(db, "SQ_LDS_BANK_CONFLICT")
+    idx = counter(db, "SQ_LDS_IDX_ACTIVE")
+    act = counter(db, "GRBM_GUI_ACTIVE", reduce="max")
+    rows = []
+    for d in sorted(idx):
+        k, a = idx[d]
+        if a <= 0 or d not in act:
+            continue
+        cyc = act[d][1] / N_XCD * N_CU
+        rows.append((d, k, a / cyc, conf.get(d, (k, 0.0))[1] / cyc))
+    return rows
 
 
 def traffic(db_fetch, db_write, mib):
@@ -73,11 +121,15 @@ def traffic(db_fetch, db_write, mib):
     return scale_f, scale_w, per
 
 
-def kernel_source_hash():
-    """Hash of the decode kernel source: a traffic record is current only
-    while the kernel it was measured on is unchanged."""
+SOURCES = {"decode_split<256, 6>": "decode_kernels.hip",
+           "prefill_attn<256, 4>": "prefill_attn_kernels.hip"}
+
+
+def kernel_source_hash(kernel="decode_split<256, 6>"):
+    """Hash of a kernel's source file: a traffic record is current only while
+    the kernel it was measured on is unchanged."""
     path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc",
-                        "decode_kernels.hip")
+                        SOURCES[kernel])
     with open(path, "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
@@ -88,7 +140,7 @@ def traffic_record(db_fetch, db_write, mib, kernel="decode_split<256, 6>"):
     wv, _ = per["write"].get(kernel, (0.0, 0))
     return {"kernel": kernel, "dispatches": fn, "fetch_bytes": fv * sf * 1024,
             "write_bytes": wv * sw * 1024, "fetch_scale": sf, "write_scale": sw,
-            "copy_mib": mib, "kernel_source_sha256_16": kernel_source_hash()}
+            "copy_mib": mib, "kernel_source_sha256_16": kernel_source_hash(kernel)}
 
 
 def main(argv):
@@ -111,7 +163,29 @@ def main(argv):
             ws = wv * (sw or 0) * 1024 / 1e6
             print(f"| {k} | {fn} | {fv:.0f} | {fs:.2f} | {wv:.0f} | {ws:.2f} |")
     elif argv[0] == "record":
-        print(json.dumps(traffic_record(argv[1], argv[2], float(argv[3])), indent=1))
+        kernel = "decode_split<256, 6>"
+        if len(argv) > 4 and argv[4] == "prefill_attn":
+            kernel = "prefill_attn<256, 4>"
+        print(json.dumps(traffic_record(argv[1], argv[2], float(argv[3]), kernel), indent=1))
+    elif argv[0] == "mfma":
+        rows = mfma(argv[1])
+        print("| dispatch | kernel | MFMA busy (of SIMD cycles) | bf16 MFMA TFLOP | GPU cycles |")
+        print("|---|---|---|---|---|")
+        for d, k, u, fl, a in rows:
+            print(f"| {d} | {k} | {u:.3f} | {fl / 1e12:.3f} | {a:.0f} |")
+        by = collections.defaultdict(list)
+        for d, k, u, fl, a in rows:
+            by[k].append((u, fl, a))
+        for k, v in by.items():
+            tot_a = sum(x[2] for x in v)
+            print(f"\n{k}: {len(v)} dispatches, cycle-weighted MFMA busy "
+                  f"{sum(x[0] * x[2] for x in v) / tot_a:.3f}, bf16 MFMA FLOP "
+                  f"{sum(x[1] for x in v) / 1e12:.2f} T")
+    elif argv[0] == "lds":
+        print("| dispatch | kernel | LDS active (of CU cycles) | bank conflict (of CU cycles) |")
+        print("|---|---|---|---|")
+        for d, k, a, c in lds(argv[1]):
+            print(f"| {d} | {k} | {a:.3f} | {c:.4f} |")
     else:
         raise SystemExit(__doc__)
 
