@@ -107,7 +107,7 @@ struct PrefillAttnArgs {
 };
 
 #ifndef HWKV_PREFILL_WAVES
-#define HWKV_PREFILL_WAVES 4
+#define HWKV_PREFILL_WAVES 8
 #endif
 constexpr int kPrefillWaves = HWKV_PREFILL_WAVES;
 

@@ -88,6 +88,15 @@ __device__ __forceinline__ void wait_loads() {
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
+// x of lane l and x of lane l ^ 32 in both lanes (VALU lane swap)
+__device__ __forceinline__ void halves(float x, float *a, float *b) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(int, x),
+                                                  __builtin_bit_cast(int, x), false, false);
+  *a = __builtin_bit_cast(float, (int)r[0]);      // x of the lower-half lane
+  *b = __builtin_bit_cast(float, (int)r[1]);      // x of the upper-half lane
+}
+
+
 template <int D, int NW>
 struct Prefill {
   static constexpr int DC = D / 8;                 // 16-byte channel chunks
@@ -98,8 +107,7 @@ struct Prefill {
   static constexpr int VPAIR = 1024 + 128;         // bytes per V row pair (padded)
   static constexpr int VBYTES = NINST * VPAIR;     // V tile
   static constexpr int STAGE = KBYTES + VBYTES;
-  static_assert(NINST % NW == 0, "tile loads must split evenly over waves");
-  static constexpr int IPW = NINST / NW;           // per wave and tile, each of K, V
+  static constexpr int IPW = (NINST + NW - 1) / NW;   // per wave and tile, each of K, V
 };
 
 template <int D, int NW>
@@ -125,7 +133,10 @@ void prefill_attn(const PrefillAttnArgs a) {
   const int ta = p0 + c_first / G, tb = p0 + c_last / G;
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63;
+  // uniform across the wavefront: keeps the per-wave tile tests and the LDS
+  // block of every load in scalar registers
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int half = lane >> 5, cl = lane & 31;
 
   // this wavefront's columns and this lane's column
@@ -225,6 +236,7 @@ void prefill_attn(const PrefillAttnArgs a) {
 #pragma unroll
     for (int j = 0; j < P::IPW; ++j) {
       const int n = wave + j * NW;
+      if (P::NINST % NW != 0 && n >= P::NINST) break;   // uniform per wave
       const int ch = 2 * n + half;
       g2lds(kp + ch * kstep, kl + n * 1024);
       g2lds(vp + ch * 8, vl + n * P::VPAIR);
@@ -278,17 +290,27 @@ void prefill_attn(const PrefillAttnArgs a) {
     const bool full_vis = s0 + kKeys <= se && slast <= t_lo &&
                           (W == 0 || slast < S || s0 >= t_hi + 1 - W);
     if (!full_vis) {
+      // key of row r: e + cr, cr = 8 (r / 4) + r % 4; e and e - t are made
+      // opaque so the per-row offsets stay compile-time constants on the
+      // uniform side of each comparison
+      int e = s0 + 4 * half, d = e - t;
+      asm volatile("" : "+v"(e), "+v"(d));
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int s = s0 + (r >> 2) * 8 + half * 4 + (r & 3);
-        const bool vis = s < se && s <= t && (W == 0 || s < S || s >= t + 1 - W);
+        const int cr = (r >> 2) * 8 + (r & 3);
+        const bool vis = (e < se - cr) & (d <= -cr) &
+                         ((W == 0) | (e < S - cr) | (d >= 1 - W - cr));
         if (!vis) st[r] = -__builtin_inff();
       }
     }
     float mx = st[0];
 #pragma unroll
     for (int r = 1; r < 16; ++r) mx = fmaxf(mx, st[r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    {
+      float lo_half, hi_half;
+      halves(mx, &lo_half, &hi_half);
+      mx = fmaxf(lo_half, hi_half);
+    }
     if (__any(mx > m + tau)) {
       const float mn = fmaxf(m, mx);
       const float alpha = __builtin_amdgcn_exp2f((m - mn) * c2);
@@ -328,8 +350,10 @@ void prefill_attn(const PrefillAttnArgs a) {
     }
   }
 
+  float l_lo, l_hi;
+  halves(l, &l_lo, &l_hi);
   if (!col_ok) return;
-  const float lt = l + __shfl_xor(l, 32);
+  const float lt = l_lo + l_hi;
   const float inv = 1.0f / lt;
   // the output row, recomputed here rather than kept live through the loop
   int c_out = c;

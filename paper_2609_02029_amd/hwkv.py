@@ -21,6 +21,11 @@ if not os.path.exists(LIB_PATH):
         f"{LIB_PATH} is missing: build it with paper_2609_02029_amd.build.build() "
         "(or __graft_entry__.build()) first")
 
+# torch owns device memory and streams: load it (and the HIP runtime it
+# initialises) before the library, so both use that one runtime whatever the
+# caller's import order.
+import torch  # noqa: E402,F401
+
 _lib = ctypes.CDLL(LIB_PATH)
 
 _i32, _i64, _dbl, _flt, _vp, _sz = (ctypes.c_int32, ctypes.c_int64, ctypes.c_double,
