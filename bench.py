@@ -71,9 +71,6 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    if args.workload == "prefill128k":
-        prefill_main(args, dev)
-        return
     if args.copy_calibration:
         n = args.copy_calibration << 20
         src = torch.ones(n // 4, dtype=torch.float32, device=dev)
@@ -82,6 +79,9 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    if args.workload == "prefill128k":
+        prefill_main(args, dev)
+        return
     cfg = W.CONFIGS[args.workload]
     L, B = cfg["n_layers"], cfg["batch"]
     Hq, Hkv, D, S = cfg["n_q_heads"], cfg["n_kv_heads"], cfg["head_dim"], cfg["n_sinks"]
@@ -431,7 +431,7 @@ def prefill_main(args, dev):
             "peak": MFMA_BF16_PEAK_TFS,
             "unit": "TFLOP/s",
             "frac": round(achieved / MFMA_BF16_PEAK_TFS, 4),
-            "traffic": None,
+            "traffic": prefill_traffic(n_chunks),
             "launch_ms_mean": round(attn_total_ms / n_chunks, 3),
             "launch_ms_per_chunk": [round(x, 3) for x in attn_ms],
             "flop_per_launch_mean": step_flop / n_chunks,
@@ -444,6 +444,21 @@ def prefill_main(args, dev):
     for c in caches:
         c.free()
     print(json.dumps(result), flush=True)
+
+
+def prefill_traffic(n_chunks):
+    """HBM bytes per prefill_attn launch (mean over the chunks) from the
+    committed counter record, if it was taken on the current kernel source."""
+    from paper_2609_02029_amd import profiling
+    path = os.path.join(ROOT, "profiles", "prefill_attn_prefill128k_traffic.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_sha256_16") != profiling.kernel_source_hash(rec["kernel"]):
+        return None
+    return round(rec["fetch_bytes"] + rec["write_bytes"])
 
 
 def prefill_cpu_baseline(args, cfg, q, k, v, windows, scale, step_flop, gpu_ms):

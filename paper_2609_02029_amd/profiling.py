@@ -7,9 +7,9 @@
     of MIB MiB that ``bench.py --copy-calibration MIB`` performs first
     (expected: MIB MiB read and MIB MiB written per copy).
 ``python -m paper_2609_02029_amd.profiling record DB_FETCH DB_WRITE MIB [KERNEL]``
-    one kernel's line of the traffic table as JSON (default the decode split
-    kernel; ``prefill_attn`` for the prefill attention kernel), with the hash
-    of the kernel source it was measured on
+    the head_dim-256 line of one kernel in the traffic table as JSON
+    (``decode_split`` by default, or ``prefill_attn``), with the hash of the
+    kernel source it was measured on
 ``python -m paper_2609_02029_amd.profiling mfma DB``
     MFMA busy fraction and bf16 MFMA FLOP per dispatch of every kernel that
     issued MFMA, from a run with SQ_VALU_MFMA_BUSY_CYCLES,
@@ -121,15 +121,15 @@ def traffic(db_fetch, db_write, mib):
     return scale_f, scale_w, per
 
 
-SOURCES = {"decode_split<256, 6>": "decode_kernels.hip",
-           "prefill_attn<256, 4>": "prefill_attn_kernels.hip"}
+SOURCES = {"decode_split<": "decode_kernels.hip",
+           "prefill_attn<": "prefill_attn_kernels.hip"}
 
 
 def kernel_source_hash(kernel="decode_split<256, 6>"):
     """Hash of a kernel's source file: a traffic record is current only while
     the kernel it was measured on is unchanged."""
-    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc",
-                        SOURCES[kernel])
+    src = next(f for k, f in SOURCES.items() if kernel.startswith(k))
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc", src)
     with open(path, "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
@@ -163,9 +163,9 @@ def main(argv):
             ws = wv * (sw or 0) * 1024 / 1e6
             print(f"| {k} | {fn} | {fv:.0f} | {fs:.2f} | {wv:.0f} | {ws:.2f} |")
     elif argv[0] == "record":
-        kernel = "decode_split<256, 6>"
-        if len(argv) > 4 and argv[4] == "prefill_attn":
-            kernel = "prefill_attn<256, 4>"
+        prefix = argv[4] + "<" if len(argv) > 4 else "decode_split<"
+        _, _, per = traffic(argv[1], argv[2], float(argv[3]))
+        kernel = next(k for k in per["fetch"] if k.startswith(prefix + "256"))
         print(json.dumps(traffic_record(argv[1], argv[2], float(argv[3]), kernel), indent=1))
     elif argv[0] == "mfma":
         rows = mfma(argv[1])
