@@ -159,11 +159,17 @@ struct SplitSmem {
   static constexpr int PST = (G + 3) & ~3;  // p stride per slot
   float m[kWaves][G];
   float l[kWaves][G];
-  union {
-    float p[kWaves][64 * PST];     // per-wave p broadcast, tile loop
-    float acc[kWaves][G][D];       // per-wave partials, merge
-  } u;
+  float p[kWaves][64 * PST];                // per-wave p broadcast, tile loop
+  __attribute__((aligned(16))) float acc[kWaves][G][D];   // per-wave partials
 };
+
+// x of lane l and x of lane l ^ 32 for two values at once (VALU lane swap):
+// returns x0 + x0' in lanes 0..31 and x1 + x1' in lanes 32..63.
+__device__ __forceinline__ float half_sum_pair(float x0, float x1) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(int, x0),
+                                                  __builtin_bit_cast(int, x1), false, false);
+  return __builtin_bit_cast(float, (int)r[0]) + __builtin_bit_cast(float, (int)r[1]);
+}
 
 template <int D, int G>
 __global__ __launch_bounds__(kWaves * 64)
@@ -236,7 +242,7 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
   }
-  float *pl = sm.u.p[wave];
+  float *pl = sm.p[wave];
   // Only this workgroup reads the new slot in this launch: a workgroup-scope
   // release/acquire around the barrier orders the store before its loads
   // (agent scope would write back and invalidate the whole L2).
@@ -388,23 +394,31 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
     kofs = kofs_n;
   }
 
-  // ---- wave partials: l over all lanes, acc over lanes sharing a chunk
+  // ---- wave partials: l over all lanes; acc over the lanes that share a
+  // channel chunk (lane, lane ^ NC, ..., lane ^ 32).  The last step pairs
+  // channel e with e + 4 in one lane swap, so lanes 0..31 end with channels
+  // 0..3 and lanes 32..63 with channels 4..7 of their chunk.
 #pragma unroll
   for (int h = 0; h < G; ++h) {
     l[h] = wave_sum(l[h]);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
 #pragma unroll
-      for (int off = 32; off >= NC; off >>= 1)
+      for (int off = 16; off >= NC; off >>= 1)
         acc[h][e] += __shfl_xor(acc[h][e], off);
     }
   }
-  __syncthreads();  // every wave is done with its p slice
-  if (rsub == 0) {
+  const int half = lane >> 5;
+  float red[G][4];
+#pragma unroll
+  for (int h = 0; h < G; ++h)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) red[h][e] = half_sum_pair(acc[h][e], acc[h][e + 4]);
+  if ((lane & 31) < NC) {
 #pragma unroll
     for (int h = 0; h < G; ++h)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) sm.u.acc[wave][h][c8 * 8 + e] = acc[h][e];
+      *reinterpret_cast<float4 *>(&sm.acc[wave][h][c8 * 8 + 4 * half]) =
+          make_float4(red[h][0], red[h][1], red[h][2], red[h][3]);
   }
   if (lane == 0) {
 #pragma unroll
@@ -415,24 +429,40 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
   }
   __syncthreads();
 
-  // ---- merge the waves (wave 0 of every split has at least one tile)
+  // ---- merge the waves (wave 0 of every split has at least one tile), 4
+  // channels per thread and step
   float *part = a.ws + (size_t)(it.ws_split0 + blk) * (G * (D + 2));
-  for (int idx = threadIdx.x; idx < G * D; idx += kWaves * 64) {
-    const int h = idx / D, c = idx % D;
+  for (int idx = threadIdx.x; idx < G * D / 4; idx += kWaves * 64) {
+    const int h = idx / (D / 4), c = (idx % (D / 4)) * 4;
     float M = sm.m[0][h];
 #pragma unroll
     for (int w = 1; w < kWaves; ++w) M = fmaxf(M, sm.m[w][h]);
-    float L = 0.f, A = 0.f;
+    float L = 0.f;
+    float4 A = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) {
       const float f = exp2f(sm.m[w][h] - M);
       L += sm.l[w][h] * f;
-      A += sm.u.acc[w][h][c] * f;
+      const float4 x = *reinterpret_cast<const float4 *>(&sm.acc[w][h][c]);
+      A.x += x.x * f;
+      A.y += x.y * f;
+      A.z += x.z * f;
+      A.w += x.w * f;
     }
     if (nsplit == 1) {
-      a.out[((size_t)it.q_row[item] + h) * D + c] = A / L;
+      const float inv = 1.0f / L;
+      *reinterpret_cast<float4 *>(&a.out[((size_t)it.q_row[item] + h) * D + c]) =
+          make_float4(A.x * inv, A.y * inv, A.z * inv, A.w * inv);
     } else {
-      part[2 * G + h * D + c] = A;
+      float *dst = &part[2 * G + h * D + c];
+      if constexpr ((2 * G) % 4 == 0) {     // partial records 16-byte aligned
+        *reinterpret_cast<float4 *>(dst) = A;
+      } else {
+        dst[0] = A.x;
+        dst[1] = A.y;
+        dst[2] = A.z;
+        dst[3] = A.w;
+      }
       if (c == 0) {
         part[h] = M;
         part[G + h] = L;
