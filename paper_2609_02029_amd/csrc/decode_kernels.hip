@@ -76,13 +76,13 @@ constexpr int kTilesPerWave = HWKV_DECODE_TPW;   // 64-slot tiles per wave
 constexpr int kPrefetch = HWKV_DECODE_PREFETCH;  // 16-byte loads in flight
 constexpr int kMinWavesPerEU = HWKV_DECODE_MINWAVES;  // VGPR budget
 #ifndef HWKV_COMBINE_THREADS
-#define HWKV_COMBINE_THREADS 1024
+#define HWKV_COMBINE_THREADS 512
 #endif
 #ifndef HWKV_COMBINE_CHAN
-#define HWKV_COMBINE_CHAN 64
+#define HWKV_COMBINE_CHAN 32
 #endif
 #ifndef HWKV_COMBINE_UNROLL
-#define HWKV_COMBINE_UNROLL 8
+#define HWKV_COMBINE_UNROLL 16
 #endif
 constexpr int kCombineThreads = HWKV_COMBINE_THREADS;  // per merge workgroup
 constexpr int kCombineChan = HWKV_COMBINE_CHAN;        // channels per workgroup
