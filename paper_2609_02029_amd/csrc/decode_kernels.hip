@@ -63,7 +63,7 @@ __device__ __forceinline__ void static_for(F &&f) {
 #define HWKV_DECODE_TPW 1
 #endif
 #ifndef HWKV_DECODE_PREFETCH
-#define HWKV_DECODE_PREFETCH 8
+#define HWKV_DECODE_PREFETCH 4
 #endif
 #ifndef HWKV_DECODE_AUX
 #define HWKV_DECODE_AUX 0  // cache-policy bits of the streaming loads
