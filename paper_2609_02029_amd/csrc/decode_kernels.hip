@@ -66,7 +66,7 @@ __device__ __forceinline__ void static_for(F &&f) {
 #define HWKV_DECODE_PREFETCH 4
 #endif
 #ifndef HWKV_DECODE_AUX
-#define HWKV_DECODE_AUX 0  // cache-policy bits of the streaming loads
+#define HWKV_DECODE_AUX 2  // cache-policy bits of the streaming loads (nt)
 #endif
 #ifndef HWKV_DECODE_MINWAVES
 #define HWKV_DECODE_MINWAVES 4
