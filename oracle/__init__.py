@@ -15,7 +15,13 @@ restated in ``oracle.c``):
 * the slot table after prefill materialisation and appends (canonical ring
   slot rule, a reading of an unspecified arrangement);
 * attention outputs -- Eqs. conditional-attention-weight and
-  conditional-attention, fp64, over the retained set.
+  conditional-attention, fp64, over the retained set;
+* the calibration replay -- candidate outputs o^(w) for every codebook
+  window (the same attention with window w), the stabilised cosine score
+  (Eq. stabilized-cosine), the per-head mean score (Eq.
+  conditional-similarity), the threshold selection (Eq.
+  threshold-selection) and the finite-grid budget selector (Eq.
+  budget-selector).
 """
 import ctypes
 import os
@@ -70,6 +76,8 @@ def _load():
     lib.orc_decode_layer.argtypes = [ctypes.c_int, _i64, _i64, _i64, _i64, _i64,
                                      _vp, _vp, _vp, _vp, _vp, _dbl, _vp]
     lib.orc_decode_layer.restype = ctypes.c_int
+    lib.orc_cos_eval.argtypes = [_vp, _vp, _i64]
+    lib.orc_cos_eval.restype = _dbl
     _lib = lib
     return lib
 
@@ -232,3 +240,88 @@ def decode_layer(q, k_hist, v_hist, t, n_sinks, windows, scale, n_threads=1):
     if rc != 0:
         raise ValueError("invalid decode_layer arguments")
     return out
+
+
+# --------------------------------------------------------------------------
+# calibration replay and selection
+# --------------------------------------------------------------------------
+def cos_eval(u, v):
+    """Stabilised cosine of two vectors (Eq. stabilized-cosine), fp64."""
+    u = np.ascontiguousarray(u, dtype=np.float64)
+    v = np.ascontiguousarray(v, dtype=np.float64)
+    if u.shape != v.shape or u.ndim != 1:
+        raise ValueError("u and v must be vectors of one length")
+    return float(_load().orc_cos_eval(_ptr(u), _ptr(v), u.size))
+
+
+def replay_outputs(q_rows, k_hist, v_hist, rows, n_sinks, windows, scale, n_threads=8):
+    """Candidate outputs o^(w) of every sampled row for every window of
+    ``windows`` (0 = full), Eq. conditional-attention with window w.
+    ``q_rows`` ``[R, Hq, d]``, ``k_hist``/``v_hist`` ``[N, Hkv, d]`` bf16 bits,
+    ``rows`` the query positions.  Returns fp64 ``[len(windows), R, Hq, d]``."""
+    rows = np.asarray(rows, dtype=np.int64)
+    Hkv = np.asarray(k_hist).shape[1]
+    out = []
+    for w in windows:
+        out.append(decode_layer(q_rows, [k_hist] * len(rows), [v_hist] * len(rows), rows,
+                                n_sinks, [int(w)] * Hkv, scale, n_threads=n_threads))
+    return np.stack(out)
+
+
+def replay_scores(outs):
+    """cos_eval of every finite candidate against the full one: ``outs`` is
+    ``[K + 1, R, Hq, d]`` with the full candidate last; returns ``[K, R, Hq]``."""
+    K = outs.shape[0] - 1
+    sc = np.empty((K,) + outs.shape[1:3], dtype=np.float64)
+    for k in range(K):
+        for r in range(outs.shape[1]):
+            for q in range(outs.shape[2]):
+                sc[k, r, q] = cos_eval(outs[k, r, q], outs[K, r, q])
+    return sc
+
+
+def head_means(scores, group):
+    """Eq. conditional-similarity: the mean of the scores of KV head h over
+    its index set (every sampled row and every query head q with
+    q // group == h).  ``scores`` ``[K, R, Hq]``; returns ``[K, Hkv]``."""
+    scores = np.asarray(scores, dtype=np.float64)
+    K, R, Hq = scores.shape
+    Hkv = Hq // group
+    out = np.empty((K, Hkv), dtype=np.float64)
+    for k in range(K):
+        for h in range(Hkv):
+            out[k, h] = scores[k, :, h * group:(h + 1) * group].mean()
+    return out
+
+
+def select_windows(means, windows, n_sinks, ctx, tau):
+    """Eq. threshold-selection for one layer: per KV head, the candidate of
+    lowest cost min(S + w, ctx) whose mean score is at least ``tau``; equal
+    costs go to the earlier codebook entry.  ``means`` ``[K, Hkv]`` for the
+    finite ``windows`` (in codebook order); the full candidate (score one,
+    cost ctx) is always feasible and is returned as index K."""
+    means = np.asarray(means, dtype=np.float64)
+    K, Hkv = means.shape
+    choice = []
+    for h in range(Hkv):
+        best, best_cost = None, None
+        # candidates in codebook order, full (index K, score 1, cost ctx) last
+        for k in range(K + 1):
+            score = means[k, h] if k < K else 1.0
+            cost = min(n_sinks + int(windows[k]), ctx) if k < K else ctx
+            if score >= tau and (best is None or cost < best_cost):
+                best, best_cost = k, cost
+        choice.append(best)
+    return choice
+
+
+def budget_select(rates, floors, budget):
+    """Eq. budget-selector over a recorded grid: among runs g (in grid order)
+    with rate <= budget, maximise the floor, then minimise the rate, then the
+    grid index.  Returns the 0-based grid index, or None if no run fits."""
+    feas = [g for g in range(len(rates)) if rates[g] <= budget]
+    if not feas:
+        return None
+    phi = max(floors[g] for g in feas)
+    beta = min(rates[g] for g in feas if floors[g] == phi)
+    return min(g for g in feas if floors[g] == phi and rates[g] == beta)

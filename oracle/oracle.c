@@ -373,3 +373,29 @@ int orc_decode_layer(int n_threads, int64_t batch, int64_t n_q_heads,
     free(th);
     return 0;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Calibration score (Appendix, "Calibration Score and Fixed-Prefix         */
+/* Selection", Eq. stabilized-cosine).                                       */
+/* ------------------------------------------------------------------------ */
+
+/* Stabilised cosine of u and v (length d): a vector whose Euclidean norm is
+ * at most eps = 1e-12 counts as zero; two zero vectors score 1, exactly one
+ * zero vector scores 0, otherwise the plain cosine u.v / (|u| |v|).  fp64. */
+double orc_cos_eval(const double *u, const double *v, int64_t d)
+{
+    const double eps = 1e-12;
+    double uu = 0.0, vv = 0.0, uv = 0.0;
+    for (int64_t i = 0; i < d; ++i) {
+        uu += u[i] * u[i];
+        vv += v[i] * v[i];
+        uv += u[i] * v[i];
+    }
+    const double nu = sqrt(uu), nv = sqrt(vv);
+    const int zu = nu <= eps, zv = nv <= eps;
+    if (zu && zv)
+        return 1.0;
+    if (zu || zv)
+        return 0.0;
+    return uv / (nu * nv);
+}

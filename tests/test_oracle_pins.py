@@ -389,3 +389,78 @@ def test_compacted_equals_masked_full_bitwise():
         perm = r.permutation(u.cap)
         c = oracle.attend_slots(q, ck[perm], cv[perm], u.table[perm], 0.3)
         assert np.array_equal(a, c)
+
+
+# ---------------------------------------------------------------------------
+# calibration score and selection rules
+# ---------------------------------------------------------------------------
+def test_cos_eval_special_cases():
+    r = np.random.default_rng(7)
+    u = r.standard_normal(64)
+    v = r.standard_normal(64)
+    assert oracle.cos_eval(u, u) == pytest.approx(1.0, abs=1e-15)
+    assert oracle.cos_eval(u, -u) == pytest.approx(-1.0, abs=1e-15)
+    e0, e1 = np.eye(64)[0], np.eye(64)[1]
+    assert oracle.cos_eval(e0, e1) == 0.0
+    # scale invariance for positive factors
+    assert oracle.cos_eval(3.0 * u, 0.25 * v) == pytest.approx(oracle.cos_eval(u, v), abs=1e-15)
+    # the library routine on ordinary vectors
+    for _ in range(20):
+        a, b = r.standard_normal(256), r.standard_normal(256)
+        ref = float(np.dot(a, b) / (np.linalg.norm(a) * np.linalg.norm(b)))
+        assert oracle.cos_eval(a, b) == pytest.approx(ref, abs=1e-14)
+    # stabilisation: norms <= 1e-12 count as zero
+    z = np.zeros(64)
+    tiny = e0 * 1e-13
+    small = e0 * 1e-11
+    assert oracle.cos_eval(z, z) == 1.0
+    assert oracle.cos_eval(z, u) == 0.0 and oracle.cos_eval(u, z) == 0.0
+    assert oracle.cos_eval(tiny, z) == 1.0 and oracle.cos_eval(tiny, e1 * 1e-13) == 1.0
+    assert oracle.cos_eval(tiny, u) == 0.0
+    assert oracle.cos_eval(small, e0) == pytest.approx(1.0, abs=1e-15)
+    assert oracle.cos_eval(e0 * 1e-12, e0) == 0.0          # the bound is inclusive
+
+
+def test_replay_window_covering_the_history_is_full():
+    """A window that reaches back to position 0 retains the whole history, so
+    its candidate output is the full one bit for bit and scores one."""
+    r = np.random.default_rng(8)
+    N, Hkv, G, d = 40, 2, 3, 16
+    k = W.f32_to_bf16_bits(r.standard_normal((N, Hkv, d)).astype(np.float32))
+    v = W.f32_to_bf16_bits(r.standard_normal((N, Hkv, d)).astype(np.float32))
+    rows = [5, 17, 39]
+    q = W.f32_to_bf16_bits(r.standard_normal((3, Hkv * G, d)).astype(np.float32))
+    outs = oracle.replay_outputs(q, k, v, rows, 2, [40, 37, 7, 0], 0.25)
+    assert np.array_equal(outs[0], outs[3])          # 40 >= t + 1 for every row
+    assert np.array_equal(outs[1, :2], outs[3, :2])  # 2 + 37 covers rows 5 and 17
+    assert not np.array_equal(outs[1, 2], outs[3, 2])  # ... but leaves out position 2 of row 39
+    sc = oracle.replay_scores(outs)
+    assert np.all(np.abs(sc[0] - 1.0) <= 1e-15)
+    assert np.all(np.abs(sc[2, 0] - 1.0) <= 1e-15)   # 2 + 7 >= 6 covers row 5
+    assert np.all(sc[2, 1:] < 1.0 - 1e-6)            # rows 17 and 39 lose keys
+
+
+def test_head_means_average_each_group():
+    K, R, Hq, G = 2, 3, 6, 3
+    scores = np.zeros((K, R, Hq))
+    for k in range(K):
+        for r_ in range(R):
+            for q in range(Hq):
+                scores[k, r_, q] = 100 * k + 10 * r_ + q
+    m = oracle.head_means(scores, G)
+    # head h averages q in {3h, 3h+1, 3h+2} and r in {0, 1, 2}: 100k + 10 + 3h + 1
+    for k in range(K):
+        for h in range(2):
+            assert m[k, h] == pytest.approx(100 * k + 10 + 3 * h + 1)
+
+
+def test_selection_rules_on_worked_examples(golden):
+    g = golden("calibration.json")
+    for case in g["threshold"]:
+        means = np.array(case["means"])
+        got = oracle.select_windows(means, case["windows"], case["n_sinks"], case["ctx"],
+                                    case["tau"])
+        assert got == case["choice"], case["derivation"]
+    for case in g["budget"]:
+        got = oracle.budget_select(case["rates"], case["floors"], case["budget"])
+        assert got == case["chosen"], case["derivation"]
