@@ -14,6 +14,11 @@ budget, 128 decode steps after a 114,560-token prompt.
 Prints ONE JSON line: resident-KV GB/s (``value``), microseconds per step,
 the roofline of the dominant kernel and the oracle's CPU baseline.
 
+``--workload calib128k`` times the calibration replay of one traced layer:
+a 131,072-token trace, 256 query positions from its final quarter, candidate
+windows {2048, 8192, 32768} and full; a step is one ``hwkv_calib_replay``
+(every candidate's outputs, the scores and the per-head means).
+
 ``--workload prefill128k`` instead times the long-prefill path: a step is a
 131,072-token prompt processed in 8,192-token chunks, each chunk's sink +
 window causal attention (``hwkv_prefill_attn``, bf16 MFMA) followed by its
@@ -31,6 +36,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "decode-attn µs/step + resident-KV HBM GB/s (% of peak) at 112K ctx, 1 GPU"
+CALIB_METRIC = "calibration replay TFLOP/s (128K trace, 256 rows, 3 windows + full, 1 GPU)"
 PREFILL_METRIC = "prefill-attn TFLOP/s (128K prompt in 8K chunks, sink+window causal, 1 GPU)"
 HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFS = 2500.0
@@ -42,7 +48,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=60)
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--workload", default="ctx112k",
-                    choices=["ctx112k", "ctx32k", "batch16", "pr1", "prefill128k"])
+                    choices=["ctx112k", "ctx32k", "batch16", "pr1", "prefill128k", "calib128k"])
     ap.add_argument("--unfused", action="store_true",
                     help="time hwkv_append + hwkv_decode_attn instead of the fused call")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -81,6 +87,9 @@ def main():
         del src, dst
     if args.workload == "prefill128k":
         prefill_main(args, dev)
+        return
+    if args.workload == "calib128k":
+        calib_main(args, dev)
         return
     cfg = W.CONFIGS[args.workload]
     L, B = cfg["n_layers"], cfg["batch"]
@@ -459,6 +468,113 @@ def prefill_traffic(n_chunks):
     if rec.get("kernel_source_sha256_16") != profiling.kernel_source_hash(rec["kernel"]):
         return None
     return round(rec["fetch_bytes"] + rec["write_bytes"])
+
+
+def calib_main(args, dev):
+    import numpy as np
+    import torch
+
+    import workloads as W
+    from paper_2609_02029_amd import hwkv
+
+    cfg = W.CONFIGS["calib128k"]
+    N, Hq, Hkv, D, S = cfg["prompt"][0], cfg["n_q_heads"], cfg["n_kv_heads"], cfg["head_dim"], \
+        cfg["n_sinks"]
+    G = Hq // Hkv
+    windows = [w for w in cfg["level_windows"] if w]
+    rows = W.calib_rows(cfg)
+    R = len(rows)
+    scale = 1.0 / math.sqrt(D)
+    k = W.normal_bf16_device((N, Hkv, D), cfg["seed"], 0, W.K, 0, device=dev)
+    v = W.normal_bf16_device((N, Hkv, D), cfg["seed"], 0, W.V, 0, device=dev)
+    q = W.normal_bf16_device((R, Hq, D), cfg["seed"], 0, W.Q_PROMPT, 0, device=dev)
+    K = len(windows)
+    outs = torch.empty((K + 1, R, Hq, D), dtype=torch.float32, device=dev)
+    scores = torch.empty((K, R, Hq), dtype=torch.float32, device=dev)
+    means = torch.empty((K, Hkv), dtype=torch.float32, device=dev)
+    ws = torch.zeros(hwkv.calib_workspace_bytes(Hq, D, S, k.shape[0], R), dtype=torch.uint8,
+                     device=dev)
+    # algorithmic FLOP: every candidate of every row and q head, 4d per
+    # retained key
+    pairs = 0
+    for w in windows + [0]:
+        for t in rows:
+            pairs += (t + 1) if w == 0 else min(t + 1, S + w)
+    flop = pairs * Hq * 4 * D
+    steps, warmup = min(max(1, args.steps), 10), min(max(0, args.warmup), 3)
+
+    def run():
+        hwkv.calib_replay(k, v, rows, q, windows, S, scale, outs, scores, means, ws)
+
+    for _ in range(warmup):
+        run()
+    torch.cuda.synchronize()
+    ms = []
+    for _ in range(steps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        run()
+        b.record()
+        torch.cuda.synchronize()
+        ms.append(a.elapsed_time(b))
+    ms_step = sum(ms) / len(ms)
+    tfs = flop / (ms_step * 1e-3) / 1e12
+    result = {
+        "metric": CALIB_METRIC,
+        "value": round(tfs, 1),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": round(ms_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 (fp32 accumulate)",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"calib128k: one traced layer of {N} tokens, {R} query rows from the "
+                         f"final quarter, {Hq} q / {Hkv} kv heads, head_dim {D}, {S} sinks, "
+                         f"candidates {windows} + full; outputs, scores and per-head means"),
+            "algorithmic_flop_per_step": flop,
+            "means": [[round(float(x), 5) for x in row] for row in means.cpu().numpy()],
+        },
+        "roofline": {
+            "bound": "mfma",
+            "kernel": "prefill_attn in replay mode (one launch per candidate) + scores + means",
+            "achieved": round(tfs, 1),
+            "peak": MFMA_BF16_PEAK_TFS,
+            "unit": "TFLOP/s",
+            "frac": round(tfs / MFMA_BF16_PEAK_TFS, 4),
+            "traffic": None,
+        },
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        bits = lambda t: t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+        kh, vh, qh = bits(k), bits(v), bits(q)
+        threads = max(1, min(16, os.cpu_count() or 1))
+        spent, done_pairs, done = 0.0, 0, 0
+        for i in range(R):
+            t0 = time.perf_counter()
+            oracle.replay_outputs(qh[i:i + 1], kh, vh, [rows[i]], S, windows + [0], scale,
+                                  n_threads=threads)
+            spent += time.perf_counter() - t0
+            done_pairs += sum((rows[i] + 1) if w == 0 else min(rows[i] + 1, S + w)
+                              for w in windows + [0])
+            done += 1
+            if spent >= args.cpu_seconds:
+                break
+        result["cpu_baseline"] = {
+            "value": round(done_pairs * Hq * 4 * D / spent / 1e9, 3),
+            "unit": "GFLOP/s",
+            "ms_per_step": round(spent / done_pairs * pairs * 1e3, 1),
+            "cores": threads,
+            "kind": "oracle",
+            "sample": (f"{done} of the {R} rows (all {Hq} q heads, every candidate), fp64 "
+                       f"masked-full-history oracle, {spent:.1f} s; scaled by retained pairs"),
+        }
+    print(json.dumps(result), flush=True)
 
 
 def prefill_cpu_baseline(args, cfg, q, k, v, windows, scale, step_flop, gpu_ms):

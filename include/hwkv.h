@@ -212,6 +212,74 @@ int hwkv_append_decode_attn(hwkv_cache *cache, int32_t layer,
                             const void *q, float scale, void *out, void *ws,
                             size_t ws_bytes, void *stream);
 
+/* ------------------------------------------------------------------------ */
+/* Calibration (Method, "Sequential Prefix-Conditioned Calibration";         */
+/* Appendix, "Calibration Score and Fixed-Prefix Selection" and             */
+/* "Finite-grid budget selection")                                           */
+/* ------------------------------------------------------------------------ */
+
+/* Device workspace bytes hwkv_calib_replay needs for n_rows sampled rows of
+ * an n_hist-token trace: the row positions and the split-K partials of the
+ * longest candidate (rows x n_q_heads x (head_dim + 4) fp32 per split of
+ * 4,096 keys). */
+int hwkv_calib_workspace_bytes(int32_t n_q_heads, int32_t head_dim,
+                               int32_t n_sinks, int64_t n_hist, int64_t n_rows,
+                               size_t *bytes);
+
+/* Candidate replay of one traced layer.  For every sampled query row r (at
+ * position rows[r]) and query head qh of KV head qh / G, the output over
+ * R(t + 1) restricted to [0, t] (t = rows[r], n_sinks sinks plus the last w
+ * positions) for every finite codebook window w (Eq. conditional-attention,
+ * z = scale * q.k), and for the full history; then the stabilised cosine of
+ * each candidate against the full output (Eq. stabilized-cosine) and, per
+ * KV head, its mean over the rows and the head's G query heads (Eq.
+ * conditional-similarity).
+ *   windows   host int64 [n_windows], finite (> 0), strictly increasing:
+ *             the codebook in order; the full candidate is implicit
+ *   k, v      device bf16 [n_hist][n_kv_heads][head_dim]: the layer's traced
+ *             full-history keys (post-RoPE) and values
+ *   rows      host int64 [n_rows], strictly increasing, in [0, n_hist)
+ *   q         device bf16 [n_rows][n_q_heads][head_dim]: traced queries
+ *   outs      device fp32 [n_windows + 1][n_rows][n_q_heads][head_dim]:
+ *             the candidate outputs in codebook order, the full one last
+ *   scores    device fp32 [n_windows][n_rows][n_q_heads]
+ *   means     device fp32 [n_windows][n_kv_heads]
+ *   ref_full  device fp32 [n_rows][n_q_heads][head_dim] or NULL: the traced
+ *             full-history output; if given, check[r][qh] is the stabilised
+ *             cosine of the replayed full output against it (the full-window
+ *             check; the paper's runs abort below 0.99)
+ *   check     device fp32 [n_rows][n_q_heads], required iff ref_full
+ *   ws        device workspace of ws_bytes >= hwkv_calib_workspace_bytes
+ * Same arithmetic as hwkv_prefill_attn (bf16 MFMA, fp32 accumulation);
+ * scores and means in fp32.  Waits for the stream once (the row positions
+ * are uploaded from host memory).  EINVAL on bad shapes, rows or windows. */
+int hwkv_calib_replay(int32_t n_kv_heads, int32_t n_q_heads, int32_t head_dim,
+                      int32_t n_sinks, int32_t n_windows,
+                      const int64_t *windows, int64_t n_hist, const void *k,
+                      const void *v, int64_t n_rows, const int64_t *rows,
+                      const void *q, float scale, void *outs, void *scores,
+                      void *means, const void *ref_full, void *check, void *ws,
+                      size_t ws_bytes, void *stream);
+
+/* Eq. threshold-selection for one layer (host only): for each KV head h, the
+ * codebook candidate of lowest cost min(n_sinks + w, ctx) whose mean score
+ * means[k][h] is at least tau; equal costs go to the earlier codebook entry;
+ * the full candidate (score one, cost ctx) is last in the codebook and
+ * always feasible.  choice[h] receives the window index, or n_windows for
+ * full; *floor (if non-NULL) the lowest selected mean (1 for full), whose
+ * minimum over layers is a run's floor. */
+int hwkv_calib_select(int32_t n_kv_heads, int32_t n_windows,
+                      const int64_t *windows, int32_t n_sinks, int64_t ctx,
+                      const double *means, double tau, int32_t *choice,
+                      double *floor);
+
+/* Eq. budget-selector over a recorded grid of n_records runs (host only):
+ * among runs g with rates[g] <= budget, the largest floors[g], then the
+ * smallest rate, then the smallest g.  *chosen = g, or -1 if no run meets
+ * the budget. */
+int hwkv_budget_select(int32_t n_records, const double *rates,
+                       const double *floors, double budget, int32_t *chosen);
+
 /* Kernel timing, for profiling.  While enabled (enable != 0) on a cache,
  * every hwkv_decode_attn / hwkv_append_decode_attn call records HIP events
  * on its stream before its split kernel, between the split and the merge

@@ -18,7 +18,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
 SOURCES = ["hwkv_api.hip", "decode_kernels.hip", "write_kernels.hip",
-           "prefill_attn_kernels.hip"]
+           "prefill_attn_kernels.hip", "calib_kernels.hip"]
 
 CFLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",

@@ -1,0 +1,159 @@
+// calib_kernels.hip -- scores of the calibration replay (gfx950).
+//
+// For every sampled query row and query head, the stabilised cosine of each
+// candidate window's output against the full-history output (Appendix,
+// calibration score, Eq. stabilized-cosine: a vector whose norm is at most
+// 1e-12 counts as zero; two zero vectors score 1, exactly one scores 0), and
+// per (candidate, kv head) the mean of those scores over the rows and the
+// head's G query heads (Eq. conditional-similarity).  fp32 throughout: one
+// wavefront per (row, q head) with lanes over channels and DPP/lane-read
+// reductions; one workgroup per (candidate, kv head) for the means.  The
+// replay's split-K partials are merged here too.
+#include "hwkv_internal.h"
+
+namespace hwkv {
+namespace {
+
+__device__ __forceinline__ float wave_sum64(float v) {
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+  return v;
+}
+
+__device__ __forceinline__ float cos_stab(float uv, float uu, float vv) {
+  const float eps = 1e-12f;
+  const float nu = sqrtf(uu), nv = sqrtf(vv);
+  const bool zu = nu <= eps, zv = nv <= eps;
+  if (zu && zv) return 1.0f;
+  if (zu || zv) return 0.0f;
+  return uv / (nu * nv);
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void calib_scores(const CalibArgs a) {
+  constexpr int PER = D / 64;                      // channels per lane
+  const int wave = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int rq = a.n_rows * a.n_q_heads;
+  if (wave >= rq) return;                          // uniform per wave
+  const size_t vec = (size_t)rq * D;               // one candidate's outputs
+  const float *full = a.outs + (size_t)a.n_cand * vec + (size_t)wave * D;
+  float f[PER];
+  float ff = 0.f;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    f[i] = full[lane + 64 * i];
+    ff += f[i] * f[i];
+  }
+  ff = wave_sum64(ff);
+  for (int k = 0; k < a.n_cand; ++k) {
+    const float *o = a.outs + (size_t)k * vec + (size_t)wave * D;
+    float uv = 0.f, uu = 0.f;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const float x = o[lane + 64 * i];
+      uv += x * f[i];
+      uu += x * x;
+    }
+    uv = wave_sum64(uv);
+    uu = wave_sum64(uu);
+    if (lane == 0) a.scores[(size_t)k * rq + wave] = cos_stab(uv, uu, ff);
+  }
+  if (a.ref) {
+    const float *r = a.ref + (size_t)wave * D;
+    float uv = 0.f, rr = 0.f;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const float x = r[lane + 64 * i];
+      uv += x * f[i];
+      rr += x * x;
+    }
+    uv = wave_sum64(uv);
+    rr = wave_sum64(rr);
+    if (lane == 0) a.check[wave] = cos_stab(uv, ff, rr);
+  }
+}
+
+// one workgroup per (candidate k, kv head h): mean of scores[k][r][h G + g]
+__global__ __launch_bounds__(256) void calib_means(const CalibArgs a) {
+  __shared__ float part[4];
+  const int hkv = a.n_q_heads / a.group;
+  const int k = blockIdx.x / hkv, h = blockIdx.x % hkv;
+  const int n = a.n_rows * a.group;
+  const float *sc = a.scores + (size_t)k * a.n_rows * a.n_q_heads;
+  float s = 0.f;
+  for (int i = threadIdx.x; i < n; i += 256) {
+    const int r = i / a.group, g = i - r * a.group;
+    s += sc[(size_t)r * a.n_q_heads + h * a.group + g];
+  }
+  s = wave_sum64(s);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0)
+    a.means[(size_t)k * hkv + h] = ((part[0] + part[1]) + (part[2] + part[3])) / (float)n;
+}
+
+// Replay split-K merge: one wavefront per (row, q head) column, lanes over
+// channels: out = sum_j acc_j 2^((m_j - M) c) / sum_j l_j 2^((m_j - M) c),
+// M = max over splits with l_j > 0 (m in logit units, c = scale * log2 e).
+template <int D>
+__global__ __launch_bounds__(256) void replay_merge(const ReplayMergeArgs a) {
+  constexpr int PER = D / 64;
+  const int col = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (col >= a.n_cols) return;                     // uniform per wave
+  const size_t stride = (size_t)a.n_cols * (D + 4);
+  const float *p = a.part + (size_t)col * (D + 4);
+  float M = -1e30f;
+  for (int j = 0; j < a.n_splits; ++j) {
+    const float *pj = p + (size_t)j * stride;
+    if (pj[1] > 0.0f) M = fmaxf(M, pj[0]);
+  }
+  float L = 0.f, acc[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) acc[i] = 0.f;
+  for (int j = 0; j < a.n_splits; ++j) {
+    const float *pj = p + (size_t)j * stride;
+    const float lj = pj[1];
+    if (!(lj > 0.0f)) continue;                    // uniform: empty split
+    const float f = __builtin_amdgcn_exp2f((pj[0] - M) * a.scale_log2);
+    L += lj * f;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) acc[i] += pj[4 + lane + 64 * i] * f;
+  }
+  const float inv = 1.0f / L;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) a.out[(size_t)col * D + lane + 64 * i] = acc[i] * inv;
+}
+
+}  // namespace
+
+hipError_t launch_replay_merge(int D, const ReplayMergeArgs &a, hipStream_t s) {
+  const dim3 grid((unsigned)((a.n_cols + 3) / 4)), block(256);
+  switch (D) {
+    case 64: hipLaunchKernelGGL(replay_merge<64>, grid, block, 0, s, a); break;
+    case 128: hipLaunchKernelGGL(replay_merge<128>, grid, block, 0, s, a); break;
+    case 256: hipLaunchKernelGGL(replay_merge<256>, grid, block, 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_calib_scores(int D, const CalibArgs &a, hipStream_t s) {
+  const int waves = a.n_rows * a.n_q_heads;
+  const dim3 grid((unsigned)((waves + 3) / 4)), block(256);
+  switch (D) {
+    case 64: hipLaunchKernelGGL(calib_scores<64>, grid, block, 0, s, a); break;
+    case 128: hipLaunchKernelGGL(calib_scores<128>, grid, block, 0, s, a); break;
+    case 256: hipLaunchKernelGGL(calib_scores<256>, grid, block, 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_calib_means(const CalibArgs &a, hipStream_t s) {
+  const dim3 grid((unsigned)(a.n_cand * (a.n_q_heads / a.group))), block(256);
+  hipLaunchKernelGGL(calib_means, grid, block, 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace hwkv

@@ -592,6 +592,211 @@ int hwkv_prefill_attn(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0,
              : HWKV_EDEVICE;
 }
 
+namespace {
+
+// Key tiles (32 keys) the replay kernel visits for the column block whose
+// first and last query positions are ta and tb, with window w (0 = full).
+int64_t replay_tiles(int64_t ta, int64_t tb, int64_t w, int64_t S) {
+  const int64_t lo = w == 0 ? 0 : std::max<int64_t>(0, ta + 1 - w);
+  if (lo <= S) return (tb + 1 + 31) / 32;
+  return (S + 31) / 32 + (tb + 1 - lo + 31) / 32;
+}
+
+size_t replay_rows_bytes(int64_t n_rows) { return (size_t)((n_rows * 4 + 255) / 256 * 256); }
+
+// Upper bound of the splits of any candidate: every column block visits at
+// most ceil(n_hist / 32) + ceil(S / 32) tiles.
+int64_t replay_max_splits(int64_t n_hist, int64_t S) {
+  const int64_t t = (n_hist + 31) / 32 + (S + 31) / 32;
+  return (t + hwkv::kReplayTilesPerSplit - 1) / hwkv::kReplayTilesPerSplit;
+}
+
+}  // namespace
+
+int hwkv_calib_workspace_bytes(int32_t n_q_heads, int32_t head_dim, int32_t n_sinks,
+                               int64_t n_hist, int64_t n_rows, size_t *bytes) {
+  if (!bytes) return fail(HWKV_EINVAL, "bytes is null");
+  if (n_rows < 1 || n_rows > (int64_t)(1 << 24) || n_hist < 1 ||
+      n_hist > (int64_t)(1 << 24) || n_q_heads < 1 || n_q_heads > 64 * 8 ||
+      (head_dim != 64 && head_dim != 128 && head_dim != 256) || n_sinks < 0)
+    return fail(HWKV_EINVAL, "bad replay shape");
+  const uint64_t part = (uint64_t)replay_max_splits(n_hist, n_sinks) * (uint64_t)n_rows *
+                        (uint64_t)n_q_heads * (uint64_t)(head_dim + 4) * 4u;
+  *bytes = replay_rows_bytes(n_rows) + (size_t)part;
+  return ok();
+}
+
+int hwkv_calib_replay(int32_t n_kv_heads, int32_t n_q_heads, int32_t head_dim,
+                      int32_t n_sinks, int32_t n_windows,
+                      const int64_t *windows, int64_t n_hist, const void *k,
+                      const void *v, int64_t n_rows, const int64_t *rows,
+                      const void *q, float scale, void *outs, void *scores,
+                      void *means, const void *ref_full, void *check, void *ws,
+                      size_t ws_bytes, void *stream) {
+  if (n_kv_heads < 1 || n_kv_heads > hwkv::kMaxItems || n_q_heads < 1 ||
+      n_q_heads % n_kv_heads != 0 || !valid_group(n_q_heads / n_kv_heads))
+    return fail(HWKV_EINVAL, "n_kv_heads in [1, 64] and n_q_heads = G * n_kv_heads "
+                             "with G in {1, 2, 4, 6, 8}");
+  if (head_dim != 64 && head_dim != 128 && head_dim != 256)
+    return fail(HWKV_EINVAL, "head_dim must be 64, 128 or 256");
+  if (n_sinks < 0) return fail(HWKV_EINVAL, "n_sinks must be >= 0");
+  if (n_windows < 0 || n_windows > 64 || (n_windows > 0 && !windows))
+    return fail(HWKV_EINVAL, "n_windows in [0, 64] with a window array");
+  for (int32_t i = 0; i < n_windows; ++i)
+    if (windows[i] < 1 || (i > 0 && windows[i] <= windows[i - 1]))
+      return fail(HWKV_EINVAL, "windows must be finite (> 0) and strictly increasing");
+  if (n_hist < 1 || n_hist > (int64_t)(1 << 24))
+    return fail(HWKV_EINVAL, "n_hist must be in [1, 2^24]");
+  if (n_rows < 1 || n_rows > (int64_t)(1 << 24) || !rows)
+    return fail(HWKV_EINVAL, "n_rows must be in [1, 2^24] with a row array");
+  for (int64_t i = 0; i < n_rows; ++i)
+    if (rows[i] < 0 || rows[i] >= n_hist || (i > 0 && rows[i] <= rows[i - 1]))
+      return fail(HWKV_EINVAL, "rows must be strictly increasing positions in [0, n_hist)");
+  if (!std::isfinite(scale) || !(scale > 0.0f))
+    return fail(HWKV_EINVAL, "scale must be finite and > 0");
+  if (!k || !v || !q || !outs || !ws || (n_windows > 0 && (!scores || !means)))
+    return fail(HWKV_EINVAL, "k, v, q, outs, ws (and scores, means) must be non-null");
+  if ((ref_full == nullptr) != (check == nullptr))
+    return fail(HWKV_EINVAL, "check is required exactly when ref_full is given");
+  size_t need = 0;
+  if (hwkv_calib_workspace_bytes(n_q_heads, head_dim, n_sinks, n_hist, n_rows, &need) !=
+      HWKV_OK)
+    return HWKV_EINVAL;
+  if (ws_bytes < need) return fail(HWKV_EINVAL, "workspace too small");
+  const int32_t G = n_q_heads / n_kv_heads;
+  const int64_t per = hwkv::prefill_attn_columns_per_block();
+  const int64_t nb = (n_rows * G + per - 1) / per;
+  if (nb * n_kv_heads > (int64_t)INT32_MAX)
+    return fail(HWKV_EINVAL, "n_rows too large for one launch");
+  hipStream_t st = (hipStream_t)stream;
+
+  // row positions to the device; the wait keeps the host buffer alive
+  std::vector<int32_t> r32(rows, rows + n_rows);
+  int rc = check_device(hipMemcpyAsync(ws, r32.data(), r32.size() * sizeof(int32_t),
+                                       hipMemcpyHostToDevice, st),
+                        "hipMemcpyAsync (rows)");
+  if (rc != HWKV_OK) return rc;
+  rc = check_device(hipStreamSynchronize(st), "hipStreamSynchronize");
+  if (rc != HWKV_OK) return rc;
+
+  const size_t vec = (size_t)n_rows * n_q_heads * head_dim;
+  float *part = reinterpret_cast<float *>(static_cast<uint8_t *>(ws) +
+                                          replay_rows_bytes(n_rows));
+  for (int32_t c = 0; c <= n_windows; ++c) {
+    hwkv::PrefillAttnArgs a;
+    std::memset(&a, 0, sizeof a);
+    // a window reaching back past the history is the full candidate
+    const int64_t w0 = c < n_windows ? windows[c] : 0;
+    const int64_t w = (w0 >= n_hist) ? 0 : w0;
+    // splits: the most tiles any column block of this candidate visits
+    int64_t max_tiles = 1;
+    for (int64_t b = 0; b < nb; ++b) {
+      const int64_t c0 = b * per, c1 = std::min(c0 + per, n_rows * G) - 1;
+      max_tiles = std::max(max_tiles, replay_tiles(rows[c0 / G], rows[c1 / G], w, n_sinks));
+    }
+    const int64_t n_splits =
+        (max_tiles + hwkv::kReplayTilesPerSplit - 1) / hwkv::kReplayTilesPerSplit;
+    for (int32_t h = 0; h < n_kv_heads; ++h) {
+      a.head[h].window = (int32_t)w;
+      a.head_order[h] = h;
+    }
+    a.q = static_cast<const uint16_t *>(q);
+    a.k = static_cast<const uint16_t *>(k);
+    a.v = static_cast<const uint16_t *>(v);
+    a.out = static_cast<float *>(outs) + (size_t)c * vec;
+    a.rows = static_cast<const int32_t *>(ws);
+    a.p0 = 0;
+    a.n_tokens = (int32_t)n_rows;
+    a.n_kv_heads = n_kv_heads;
+    a.group = G;
+    a.n_sinks = n_sinks;
+    a.n_col_blocks = (int32_t)nb;
+    a.scale_log2 = scale * 1.4426950408889634f;
+    if (n_splits > 1) {
+      a.part = part;
+      a.tiles_per_split = hwkv::kReplayTilesPerSplit;
+    }
+    rc = check_device(hwkv::launch_prefill_attn(head_dim, a, st, (int)n_splits),
+                      "calib replay launch");
+    if (rc != HWKV_OK) return rc;
+    if (n_splits > 1) {
+      hwkv::ReplayMergeArgs ma;
+      ma.part = part;
+      ma.out = a.out;
+      ma.n_splits = (int32_t)n_splits;
+      ma.n_cols = (int32_t)(n_rows * n_q_heads);
+      ma.scale_log2 = a.scale_log2;
+      rc = check_device(hwkv::launch_replay_merge(head_dim, ma, st), "calib merge launch");
+      if (rc != HWKV_OK) return rc;
+    }
+  }
+  hwkv::CalibArgs ca;
+  ca.outs = static_cast<const float *>(outs);
+  ca.ref = static_cast<const float *>(ref_full);
+  ca.scores = static_cast<float *>(scores);
+  ca.check = static_cast<float *>(check);
+  ca.means = static_cast<float *>(means);
+  ca.n_cand = n_windows;
+  ca.n_rows = (int32_t)n_rows;
+  ca.n_q_heads = n_q_heads;
+  ca.group = G;
+  if (n_windows > 0 || ref_full) {
+    rc = check_device(hwkv::launch_calib_scores(head_dim, ca, st), "calib scores launch");
+    if (rc != HWKV_OK) return rc;
+  }
+  if (n_windows > 0) {
+    rc = check_device(hwkv::launch_calib_means(ca, st), "calib means launch");
+    if (rc != HWKV_OK) return rc;
+  }
+  return ok();
+}
+
+int hwkv_calib_select(int32_t n_kv_heads, int32_t n_windows,
+                      const int64_t *windows, int32_t n_sinks, int64_t ctx,
+                      const double *means, double tau, int32_t *choice,
+                      double *floor) {
+  if (n_kv_heads < 1 || n_windows < 0 || (n_windows > 0 && (!windows || !means)) ||
+      !choice || n_sinks < 0 || ctx < 1 || !(tau > 0.0 && tau <= 1.0))
+    return fail(HWKV_EINVAL, "bad selection arguments (tau must lie in (0, 1])");
+  for (int32_t i = 0; i < n_windows; ++i)
+    if (windows[i] < 1) return fail(HWKV_EINVAL, "windows must be finite (> 0)");
+  double lowest = 1.0;
+  for (int32_t h = 0; h < n_kv_heads; ++h) {
+    int32_t best = -1;
+    int64_t best_cost = 0;
+    double best_score = 1.0;
+    // candidates in codebook order; the full one (score 1, cost ctx) last
+    for (int32_t c = 0; c <= n_windows; ++c) {
+      const double score = c < n_windows ? means[(size_t)c * n_kv_heads + h] : 1.0;
+      const int64_t cost = c < n_windows ? std::min((int64_t)n_sinks + windows[c], ctx) : ctx;
+      if (score >= tau && (best < 0 || cost < best_cost)) {
+        best = c;
+        best_cost = cost;
+        best_score = score;
+      }
+    }
+    choice[h] = best;
+    lowest = std::min(lowest, best_score);
+  }
+  if (floor) *floor = lowest;
+  return ok();
+}
+
+int hwkv_budget_select(int32_t n_records, const double *rates,
+                       const double *floors, double budget, int32_t *chosen) {
+  if (n_records < 1 || !rates || !floors || !chosen)
+    return fail(HWKV_EINVAL, "need at least one record and non-null arrays");
+  int32_t g_best = -1;
+  for (int32_t g = 0; g < n_records; ++g) {
+    if (!(rates[g] <= budget)) continue;
+    if (g_best < 0 || floors[g] > floors[g_best] ||
+        (floors[g] == floors[g_best] && rates[g] < rates[g_best]))
+      g_best = g;                                  // earlier g wins full ties
+  }
+  *chosen = g_best;
+  return ok();
+}
+
 int hwkv_append(hwkv_cache *c, int32_t layer, const void *k_new,
                 const void *v_new, void *stream) {
   if (!c) return fail(HWKV_EINVAL, "cache is null");

@@ -97,6 +97,11 @@ struct PrefillAttnArgs {
   const uint16_t *k;             // [n_tokens][Hkv][D]
   const uint16_t *v;
   float *out;                    // [n_tokens][Hq][D]
+  const int32_t *rows;           // calibration replay: position of each query
+                                 // row (ascending); null for prefill (p0 + row)
+  float *part;                   // split-K partials (replay) or null: per split
+                                 // and column [m, l, -, -, acc[D]]
+  int32_t tiles_per_split;       // key tiles per split when part is set
   int32_t p0;
   int32_t n_tokens;
   int32_t n_kv_heads;
@@ -123,7 +128,32 @@ hipError_t launch_prefill_write(int D, const WriteArgs &a, int max_tiles,
                                 hipStream_t s);
 hipError_t launch_append(int D, const AppendArgs &a, hipStream_t s);
 int prefill_attn_columns_per_block();   // (token, q head) columns
-hipError_t launch_prefill_attn(int D, const PrefillAttnArgs &a, hipStream_t s);
+hipError_t launch_prefill_attn(int D, const PrefillAttnArgs &a, hipStream_t s,
+                              int n_splits = 1);
+
+// Calibration scores: for every (row, q head), the stabilised cosine of each
+// candidate output against the full one (and of the full one against a
+// reference); then per (candidate, kv head) the mean score.
+struct CalibArgs {
+  const float *outs;             // [n_cand + 1][n_rows][Hq][D], full last
+  const float *ref;              // [n_rows][Hq][D] or null
+  float *scores;                 // [n_cand][n_rows][Hq]
+  float *check;                  // [n_rows][Hq] (if ref)
+  float *means;                  // [n_cand][Hkv]
+  int32_t n_cand, n_rows, n_q_heads, group;
+};
+hipError_t launch_calib_scores(int D, const CalibArgs &a, hipStream_t s);
+
+// Merge of the replay's split-K partials into normalised outputs.
+struct ReplayMergeArgs {
+  const float *part;             // [n_splits][n_cols][D + 4]
+  float *out;                    // [n_cols][D]
+  int32_t n_splits, n_cols;
+  float scale_log2;
+};
+hipError_t launch_replay_merge(int D, const ReplayMergeArgs &a, hipStream_t s);
+constexpr int kReplayTilesPerSplit = 128;   // 32-key tiles per split
+hipError_t launch_calib_means(const CalibArgs &a, hipStream_t s);
 
 }  // namespace hwkv
 

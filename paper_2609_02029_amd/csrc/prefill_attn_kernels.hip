@@ -10,6 +10,10 @@
 // whose residency at length p0 covers every s >= p0 + 1 - w); keys in
 // [p0, t] come from the chunk's own K/V.
 //
+// Calibration replay runs the same kernel with a list of query positions
+// (ascending, one per query row), p0 = 0 and the layer's whole traced K/V as
+// the "chunk", once per candidate window.
+//
 // Formulation.  A workgroup owns one KV head and 32 * NW consecutive
 // (token, q-head) columns of that head (column c = token * G + g), one
 // 32-column block per wavefront.  Per key tile of 32 positions it computes
@@ -126,11 +130,14 @@ void prefill_attn(const PrefillAttnArgs a) {
   const int ncols = a.n_tokens * G;
   const int c_first = cb * 32 * NW;
   const int c_last = min(c_first + 32 * NW, ncols) - 1;
-  // positions and slots fit in 32 bits (max_ctx < 2^24)
+  // positions and slots fit in 32 bits (max_ctx < 2^24).  Query row r sits
+  // at position p0 + r, or rows[r] in calibration replay (ascending).
   const int p0 = a.p0;
+  const int32_t *rows = a.rows;
+  auto pos = [&](int r) -> int { return rows ? rows[r] : p0 + r; };
   const int S = a.n_sinks;
   const int W = hd.window;                          // 0 = full
-  const int ta = p0 + c_first / G, tb = p0 + c_last / G;
+  const int ta = pos(c_first / G), tb = pos(c_last / G);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -143,12 +150,12 @@ void prefill_attn(const PrefillAttnArgs a) {
   const int wc0 = c_first + 32 * wave;
   const bool wave_live = wc0 <= c_last;
   const int wc_last = min(wc0 + 31, c_last);
-  const int t_lo = p0 + min(wc0, c_last) / G, t_hi = p0 + wc_last / G;
+  const int t_lo = pos(min(wc0, c_last) / G), t_hi = pos(wc_last / G);
   const int c = wc0 + cl;
   const bool col_ok = c <= c_last;
   const int cc = min(c, c_last);
   const int tl = cc / G, g = cc - tl * G;
-  const int t = p0 + tl;
+  const int t = pos(tl);
   const size_t q_row = ((size_t)tl * Hq + (size_t)h * G + g) * D;
 
   u32x4_t qv[KS];
@@ -168,6 +175,22 @@ void prefill_attn(const PrefillAttnArgs a) {
   }
   const int na = (ra1 + kKeys - 1) / kKeys;
   const int ntiles = na + (rb1 - rb0 + kKeys - 1) / kKeys;
+  // split-K (calibration replay): this workgroup's share of the tiles
+  int i_begin = 0, i_end = ntiles;
+  if (a.part) {
+    i_begin = blockIdx.y * a.tiles_per_split;
+    i_end = min(ntiles, i_begin + a.tiles_per_split);
+  }
+  const size_t col_id = q_row / D;                  // row * Hq + h * G + g
+  float *pp = a.part ? a.part + ((size_t)blockIdx.y * (a.n_tokens * Hq) + col_id) * (D + 4)
+                     : nullptr;
+  if (i_begin >= i_end) {                           // uniform: an empty split
+    if (pp && col_ok && half == 0) {
+      pp[0] = -1e30f;
+      pp[1] = 0.0f;
+    }
+    return;
+  }
 
   const uint16_t *kc = a.cache + hd.k_off;
   const uint16_t *vc = a.cache + hd.v_off;
@@ -264,12 +287,12 @@ void prefill_attn(const PrefillAttnArgs a) {
   const int vkey0 = 4 * (gq >> 1) + (mq >> 2);
   const int vlane = (gq & 1) * P::VPAIR + vpar * 512 + (vkey0 ^ (4 * vpar)) * 16 + (mq & 1) * 8;
 
-  if (ntiles > 0) issue_loads(0, 0);
+  issue_loads(i_begin, i_begin & 1);
 
-  for (int i = 0; i < ntiles; ++i) {
+  for (int i = i_begin; i < i_end; ++i) {
     wait_loads();
     __syncthreads();
-    if (i + 1 < ntiles) issue_loads(i + 1, (i + 1) & 1);
+    if (i + 1 < i_end) issue_loads(i + 1, (i + 1) & 1);
     int s0, se;
     tile_range(i, &s0, &se);
     const int slast = min(s0 + kKeys, se) - 1;
@@ -354,6 +377,20 @@ void prefill_attn(const PrefillAttnArgs a) {
   halves(l, &l_lo, &l_hi);
   if (!col_ok) return;
   const float lt = l_lo + l_hi;
+  if (pp) {                                         // split-K partial, unnormalised
+    if (half == 0) {
+      pp[0] = m;
+      pp[1] = lt;
+    }
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq)
+        *reinterpret_cast<float4 *>(pp + 4 + 32 * db + 8 * rq + 4 * half) =
+            make_float4(o[db][4 * rq + 0], o[db][4 * rq + 1], o[db][4 * rq + 2],
+                        o[db][4 * rq + 3]);
+    return;
+  }
   const float inv = 1.0f / lt;
   // the output row, recomputed here rather than kept live through the loop
   int c_out = c;
@@ -377,8 +414,9 @@ void prefill_attn(const PrefillAttnArgs a) {
 
 int prefill_attn_columns_per_block() { return 32 * kPrefillWaves; }
 
-hipError_t launch_prefill_attn(int D, const PrefillAttnArgs &a, hipStream_t s) {
-  const dim3 grid((unsigned)(a.n_col_blocks * a.n_kv_heads));
+hipError_t launch_prefill_attn(int D, const PrefillAttnArgs &a, hipStream_t s,
+                              int n_splits) {
+  const dim3 grid((unsigned)(a.n_col_blocks * a.n_kv_heads), (unsigned)n_splits);
   const dim3 block(kPrefillWaves * 64);
   switch (D) {
     case 64: hipLaunchKernelGGL((prefill_attn<64, kPrefillWaves>), grid, block, 0, s, a); break;

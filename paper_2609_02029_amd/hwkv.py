@@ -53,6 +53,11 @@ SYMBOLS = {
     "hwkv_cache_read_unit": ([_vp, _i32, _i32, _i32, _vp, _vp, _P(_i64)], ctypes.c_int),
     "hwkv_decode_timing": ([_vp, _i32], ctypes.c_int),
     "hwkv_decode_timing_read": ([_vp, _P(_dbl), _P(_dbl), _P(_i64)], ctypes.c_int),
+    "hwkv_calib_workspace_bytes": ([_i32, _i32, _i32, _i64, _i64, _P(_sz)], ctypes.c_int),
+    "hwkv_calib_replay": ([_i32, _i32, _i32, _i32, _i32, _vp, _i64, _vp, _vp, _i64, _vp, _vp,
+                           _flt, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp], ctypes.c_int),
+    "hwkv_calib_select": ([_i32, _i32, _vp, _i32, _i64, _vp, _dbl, _vp, _P(_dbl)], ctypes.c_int),
+    "hwkv_budget_select": ([_i32, _vp, _vp, _dbl, _P(_i32)], ctypes.c_int),
 }
 for _name, (_args, _res) in SYMBOLS.items():
     _f = getattr(_lib, _name)
@@ -295,3 +300,70 @@ def decode_timing_read(cache):
     _check(_lib.hwkv_decode_timing_read(cache.handle, ctypes.byref(sp), ctypes.byref(mg),
                                         ctypes.byref(n)))
     return sp.value, mg.value, n.value
+
+
+def calib_workspace_bytes(n_q_heads, head_dim, n_sinks, n_hist, n_rows):
+    n = _sz()
+    _check(_lib.hwkv_calib_workspace_bytes(int(n_q_heads), int(head_dim), int(n_sinks),
+                                           int(n_hist), int(n_rows), ctypes.byref(n)))
+    return n.value
+
+
+def _i64_array(x):
+    import numpy as np
+    return np.ascontiguousarray(x, dtype=np.int64)
+
+
+def calib_replay(k, v, rows, q, windows, n_sinks, scale, outs, scores, means, ws,
+                 ref_full=None, check=None, stream=None):
+    """Candidate replay of one traced layer (see ``hwkv_calib_replay``).
+
+    ``k``, ``v``: bf16 [n_hist, Hkv, D]; ``q``: bf16 [R, Hq, D]; ``rows``:
+    R increasing positions (host); ``windows``: the finite codebook in
+    order; ``outs``: fp32 [K + 1, R, Hq, D]; ``scores``: fp32 [K, R, Hq];
+    ``means``: fp32 [K, Hkv]; ``ws``: device workspace tensor."""
+    n_hist, hkv, d = k.shape
+    R, hq, _ = q.shape
+    w = _i64_array(windows)
+    r = _i64_array(rows)
+    if r.shape != (R,):
+        raise ValueError("rows must hold one position per query row")
+    K = w.size
+    if tuple(outs.shape) != (K + 1, R, hq, d):
+        raise ValueError("outs must be [n_windows + 1, n_rows, n_q_heads, head_dim]")
+    if K and (tuple(scores.shape) != (K, R, hq) or tuple(means.shape) != (K, hkv)):
+        raise ValueError("scores must be [n_windows, n_rows, n_q_heads], means [n_windows, n_kv_heads]")
+    _check(_lib.hwkv_calib_replay(
+        hkv, hq, d, int(n_sinks), K, w.ctypes.data if K else None, n_hist,
+        _dev(k, "bfloat16", "k"), _dev(v, "bfloat16", "v"), R, r.ctypes.data,
+        _dev(q, "bfloat16", "q"), float(scale), _dev(outs, "float32", "outs"),
+        _dev(scores, "float32", "scores") if K else None,
+        _dev(means, "float32", "means") if K else None,
+        _dev(ref_full, "float32", "ref_full"), _dev(check, "float32", "check"),
+        _dev(ws, "uint8", "ws"), ws.numel(), _stream(stream)))
+
+
+def calib_select(means, windows, n_sinks, ctx, tau):
+    """Eq. threshold-selection on host ``means`` [K, Hkv]; returns
+    (choice per KV head with K = full, floor)."""
+    import numpy as np
+    m = np.ascontiguousarray(means, dtype=np.float64)
+    w = _i64_array(windows)
+    K, hkv = m.shape
+    choice = np.zeros(hkv, dtype=np.int32)
+    fl = _dbl()
+    _check(_lib.hwkv_calib_select(hkv, K, w.ctypes.data if K else None, int(n_sinks), int(ctx),
+                                  m.ctypes.data if K else None, float(tau), choice.ctypes.data,
+                                  ctypes.byref(fl)))
+    return [int(x) for x in choice], fl.value
+
+
+def budget_select(rates, floors, budget):
+    """Eq. budget-selector; returns the grid index or None."""
+    import numpy as np
+    r = np.ascontiguousarray(rates, dtype=np.float64)
+    f = np.ascontiguousarray(floors, dtype=np.float64)
+    g = _i32()
+    _check(_lib.hwkv_budget_select(r.size, r.ctypes.data, f.ctypes.data, float(budget),
+                                   ctypes.byref(g)))
+    return None if g.value < 0 else g.value

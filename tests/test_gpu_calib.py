@@ -1,0 +1,221 @@
+"""GPU parity of the calibration replay (hwkv_calib_replay) and the
+selection rules against the fp64 oracle.
+
+* candidate outputs o^(w): the windowed attention of every sampled row, per
+  channel within the bf16 weight-rounding bound (2^-8 + 2e-5) max |v| over
+  the retained keys, as for prefill attention (same kernel);
+* scores: the score kernel must return the stabilised cosine of the outputs
+  it was given, to fp32 dot-product accuracy ((2 D + 8) 2^-24); against the
+  oracle's own scores, within the bound the measured output deviations
+  imply, 2 (|du| / |u| + |dv| / |v|) plus that accuracy;
+* means: the group averages of the GPU scores within n 2^-24 (n = rows x G);
+* selection: on the same means, the library's choice equals the oracle's.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+from hwkv_harness import log, up
+from paper_2609_02029_amd import hwkv
+
+pytestmark = pytest.mark.gpu
+
+P_ROUND = 2.0 ** -8 + 2e-5
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.set_device(0)
+
+
+def replay(k, v, q, rows, windows, S, scale, ref_full=None, dev="cuda:0"):
+    """Runs hwkv_calib_replay on device tensors; returns host arrays."""
+    R, Hq, D = q.shape
+    Hkv = k.shape[1]
+    K = len(windows)
+    outs = torch.full((K + 1, R, Hq, D), float("nan"), dtype=torch.float32, device=dev)
+    scores = torch.full((max(K, 1), R, Hq), float("nan"), dtype=torch.float32, device=dev)[:K]
+    means = torch.full((max(K, 1), Hkv), float("nan"), dtype=torch.float32, device=dev)[:K]
+    ws = torch.zeros(hwkv.calib_workspace_bytes(Hq, D, S, k.shape[0], R), dtype=torch.uint8,
+                     device=dev)
+    check = None
+    if ref_full is not None:
+        check = torch.full((R, Hq), float("nan"), dtype=torch.float32, device=dev)
+    hwkv.calib_replay(k, v, rows, q, windows, S, scale, outs, scores.contiguous(),
+                      means.contiguous(), ws, ref_full=ref_full, check=check)
+    torch.cuda.synchronize()
+    res = dict(outs=outs.cpu().numpy().astype(np.float64),
+               scores=scores.cpu().numpy().astype(np.float64),
+               means=means.cpu().numpy().astype(np.float64))
+    if check is not None:
+        res["check"] = check.cpu().numpy().astype(np.float64)
+    return res
+
+
+def vmax_retained(vh, rows, windows, S):
+    """[K + 1, R, Hkv, D]: max |v| per channel over each row's retained keys."""
+    av = np.abs(W.bf16_bits_to_f32(vh)).astype(np.float64)
+    pos = np.arange(av.shape[0])
+    out = np.empty((len(windows) + 1, len(rows), av.shape[1], av.shape[2]))
+    for ki, w in enumerate(list(windows) + [0]):
+        for i, t in enumerate(rows):
+            keep = pos <= t
+            if w:
+                keep &= (pos < S) | (pos >= t + 1 - w)
+            out[ki, i] = av[keep].max(axis=0)
+    return out
+
+
+def check_all(res, ref_outs, kh, vh, rows, windows, S, G, what, vmax=None):
+    K = len(windows)
+    outs = res["outs"]
+    assert np.all(np.isfinite(outs)), f"{what}: non-finite output"
+    # candidate outputs
+    if vmax is None:
+        vmax = vmax_retained(vh, rows, windows, S)
+    vb = np.repeat(vmax, G, axis=2)
+    ratio = float((np.abs(outs - ref_outs) / (P_ROUND * vb)).max())
+    assert ratio <= 1.0, f"{what}: outputs {ratio:.3f} x the rounding bound"
+    D = outs.shape[-1]
+    tol = (2 * D + 8) * 2.0 ** -24
+    # scores: the cosine of the given outputs
+    for k in range(K):
+        for r in range(outs.shape[1]):
+            for q in range(outs.shape[2]):
+                c = oracle.cos_eval(outs[k, r, q], outs[K, r, q])
+                assert abs(res["scores"][k, r, q] - c) <= tol, (what, k, r, q)
+    # scores against the oracle's, within the deviation-implied bound
+    ref_sc = oracle.replay_scores(ref_outs)
+    du = np.linalg.norm(outs - ref_outs, axis=-1) / np.maximum(
+        np.linalg.norm(ref_outs, axis=-1), 1e-30)
+    bound = 2.0 * (du[:K] + du[K][None]) + tol
+    err = np.abs(res["scores"] - ref_sc)
+    assert np.all(err <= bound), f"{what}: score error {float(err.max())}"
+    # means of the GPU scores
+    n = outs.shape[1] * G
+    m_ref = oracle.head_means(res["scores"], G)
+    assert np.all(np.abs(res["means"] - m_ref) <= n * 2.0 ** -24), what
+    # selection on identical means
+    for tau in (0.9, 0.99, 0.995, 0.999):
+        got, _ = hwkv.calib_select(res["means"], windows, S, int(kh.shape[0]), tau)
+        assert got == oracle.select_windows(res["means"], windows, S, int(kh.shape[0]), tau)
+    return ratio, float(err.max())
+
+
+def small_case(seed, N, Hkv, G, D, windows, S, extra_rows=32):
+    r = np.random.default_rng(seed)
+    kh = W.normal_bf16((N, Hkv, D), seed, 0, W.K, 0)
+    vh = W.normal_bf16((N, Hkv, D), seed, 0, W.V, 0)
+    edge = {0, 1, S - 1, S, N - 1}
+    for w in windows:
+        edge |= {S + w - 1, S + w, S + w + 1, w - 1, w}
+    edge = {x for x in edge if 0 <= x < N}
+    rest = np.setdiff1d(np.arange(N), sorted(edge))
+    rows = sorted(edge | {int(x) for x in r.choice(rest, size=extra_rows, replace=False)})
+    qh = W.normal_bf16((len(rows), Hkv * G, D), seed, 0, W.Q_PROMPT, 7)
+    return kh, vh, qh, rows
+
+
+@pytest.mark.parametrize("D,G", [(64, 4), (128, 1), (128, 8), (256, 6)])
+def test_replay_small(D, G):
+    S, windows = 4, [16, 64, 200]
+    kh, vh, qh, rows = small_case(31, 600, 2, G, D, windows, S)
+    scale = 1.0 / math.sqrt(D)
+    res = replay(up(kh, "cuda:0"), up(vh, "cuda:0"), up(qh, "cuda:0"), rows, windows, S, scale)
+    ref = oracle.replay_outputs(qh, kh, vh, rows, S, list(windows) + [0], scale)
+    ratio, serr = check_all(res, ref, kh, vh, rows, windows, S, G, f"D={D} G={G}")
+    log(f"replay D={D} G={G}: {len(rows)} rows, outputs {ratio:.3f} of the bound, "
+        f"max score error {serr:.2e}")
+
+
+@pytest.mark.parametrize("D,G", [(128, 4), (256, 6)])
+def test_replay_split_keys(D, G):
+    """Histories long enough that the full and the 5000 candidates are split
+    over several workgroups (4,096 keys each) and merged."""
+    S, windows = 4, [100, 5000]
+    kh, vh, qh, rows = small_case(34, 9000, 2, G, D, windows, S, extra_rows=24)
+    scale = 1.0 / math.sqrt(D)
+    res = replay(up(kh, "cuda:0"), up(vh, "cuda:0"), up(qh, "cuda:0"), rows, windows, S, scale)
+    ref = oracle.replay_outputs(qh, kh, vh, rows, S, list(windows) + [0], scale, n_threads=16)
+    ratio, serr = check_all(res, ref, kh, vh, rows, windows, S, G, f"split D={D} G={G}")
+    log(f"replay split D={D} G={G}: outputs {ratio:.3f} of the bound, score error {serr:.2e}")
+
+
+def test_replay_edges_and_full_check():
+    """Sinks 0 and 3, a window of 1, windows beyond the history, a row at
+    position 0; the full-window check against the oracle's full output."""
+    for S, windows in ((0, [1, 33, 5000]), (3, [2, 31, 32, 100])):
+        kh, vh, qh, rows = small_case(32, 300, 2, 4, 128, windows, S, extra_rows=16)
+        rows = sorted(set(rows) | {0})
+        qh = W.normal_bf16((len(rows), 8, 128), 32, 0, W.Q_PROMPT, 8)
+        scale = 1.0 / math.sqrt(128)
+        ref = oracle.replay_outputs(qh, kh, vh, rows, S, list(windows) + [0], scale)
+        ref_full = torch.from_numpy(ref[-1].astype(np.float32)).to("cuda:0")
+        res = replay(up(kh, "cuda:0"), up(vh, "cuda:0"), up(qh, "cuda:0"), rows, windows, S,
+                     scale, ref_full=ref_full)
+        check_all(res, ref, kh, vh, rows, windows, S, 4, f"S={S}")
+        assert np.all(res["check"] >= 0.99)
+        # the row at position 0 sees one key under every candidate: score one
+        assert np.all(np.abs(res["scores"][:, 0] - 1.0) <= 1e-6)
+        # windows reaching back past the history equal the full candidate
+        for k, w in enumerate(windows):
+            covered = [i for i, t in enumerate(rows) if S + w >= t + 1]
+            assert np.array_equal(res["outs"][k, covered], res["outs"][-1, covered])
+
+
+def test_replay_zero_values_score_one():
+    """V = 0 makes every output the zero vector: stabilised cosine 1."""
+    kh = W.normal_bf16((100, 1, 64), 33, 0, W.K, 0)
+    vh = np.zeros((100, 1, 64), dtype=np.uint16)
+    qh = W.normal_bf16((5, 2, 64), 33, 0, W.Q_PROMPT, 0)
+    res = replay(up(kh, "cuda:0"), up(vh, "cuda:0"), up(qh, "cuda:0"), [3, 10, 50, 60, 99],
+                 [8, 32], 2, 0.125)
+    assert np.all(res["outs"] == 0.0)
+    assert np.all(res["scores"] == 1.0) and np.all(res["means"] == 1.0)
+
+
+def test_calib128k_workload():
+    """The calibration workload in full: a 128K trace, 256 rows from the final
+    quarter; outputs checked on 24 of the rows, scores, means and selection
+    on all of them."""
+    cfg = W.CONFIGS["calib128k"]
+    N, Hq, Hkv, D, S = cfg["prompt"][0], cfg["n_q_heads"], cfg["n_kv_heads"], cfg["head_dim"], \
+        cfg["n_sinks"]
+    G = Hq // Hkv
+    windows = [w for w in cfg["level_windows"] if w]
+    rows = W.calib_rows(cfg)
+    dev = "cuda:0"
+    k = W.normal_bf16_device((N, Hkv, D), cfg["seed"], 0, W.K, 0, device=dev)
+    v = W.normal_bf16_device((N, Hkv, D), cfg["seed"], 0, W.V, 0, device=dev)
+    q = W.normal_bf16_device((len(rows), Hq, D), cfg["seed"], 0, W.Q_PROMPT, 0, device=dev)
+    scale = 1.0 / math.sqrt(D)
+    res = replay(k, v, q, rows, windows, S, scale)
+    bits = lambda t: t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    kh, vh, qh = bits(k), bits(v), bits(q)
+    pick = list(range(0, len(rows), len(rows) // 24))[:24]
+    sub_rows = [rows[i] for i in pick]
+    ref = oracle.replay_outputs(qh[pick], kh, vh, sub_rows, S, list(windows) + [0], scale,
+                                n_threads=16)
+    outs = res["outs"][:, pick]
+    vmax = np.abs(W.bf16_bits_to_f32(vh)).max(axis=0)[None, None].astype(np.float64)
+    vb = np.repeat(np.broadcast_to(vmax, (len(windows) + 1, len(pick), Hkv, D)), G, axis=2)
+    ratio = float((np.abs(outs - ref) / (P_ROUND * vb)).max())
+    assert ratio <= 1.0
+    tol = (2 * D + 8) * 2.0 ** -24
+    for kk in range(len(windows)):
+        for r in range(0, len(rows), 7):
+            for qq in range(Hq):
+                c = oracle.cos_eval(res["outs"][kk, r, qq], res["outs"][-1, r, qq])
+                assert abs(res["scores"][kk, r, qq] - c) <= tol
+    m_ref = oracle.head_means(res["scores"], G)
+    assert np.all(np.abs(res["means"] - m_ref) <= len(rows) * G * 2.0 ** -24)
+    for tau in (0.99, 0.995, 0.999):
+        got, _ = hwkv.calib_select(res["means"], windows, S, N, tau)
+        assert got == oracle.select_windows(res["means"], windows, S, N, tau)
+    log(f"calib128k: outputs {ratio:.3f} of the (global-max) bound; means {res['means'].round(4)}")

@@ -252,3 +252,68 @@ def test_decode_timing_without_calls(hw):
     assert (sp.value, mg.value, n.value) == (0.0, 0.0, 0)
     assert L.hwkv_decode_timing(None, 1) == hw.EINVAL
     L.hwkv_cache_free(h)
+
+
+def test_calib_selection_matches_golden_and_oracle(hw, golden):
+    g = golden("calibration.json")
+    for case in g["threshold"]:
+        got, fl = hw.calib_select(np.array(case["means"]), case["windows"], case["n_sinks"],
+                                  case["ctx"], case["tau"])
+        assert got == case["choice"], case["derivation"]
+        sel = [case["means"][c][h] if c < len(case["windows"]) else 1.0
+               for h, c in enumerate(got)]
+        assert fl == min(sel)
+    for case in g["budget"]:
+        assert hw.budget_select(case["rates"], case["floors"], case["budget"]) == case["chosen"]
+    r = np.random.default_rng(3)
+    for _ in range(300):
+        K, H = int(r.integers(0, 5)), int(r.integers(1, 9))
+        wins = sorted(set(int(x) for x in r.integers(1, 400, size=K)))
+        K = len(wins)
+        means = r.choice([0.9, 0.99, 0.995, 0.999, 1.0], size=(K, H))
+        S, ctx, tau = int(r.integers(0, 5)), int(r.integers(50, 500)), float(r.choice([0.99, 0.995]))
+        got, _ = hw.calib_select(means, wins, S, ctx, tau)
+        assert got == oracle.select_windows(means, wins, S, ctx, tau)
+        n = int(r.integers(1, 8))
+        rates = r.choice([0.3, 0.45, 0.5, 0.7], size=n).tolist()
+        floors = r.choice([0.99, 0.995, 0.999], size=n).tolist()
+        assert hw.budget_select(rates, floors, 0.5) == oracle.budget_select(rates, floors, 0.5)
+
+
+def test_calib_host_errors(hw):
+    L = hw._lib
+    sc = ctypes.c_float(0.125)
+    wins = np.array([16, 64], dtype=np.int64)
+    rows = np.array([3, 9, 40], dtype=np.int64)
+    ws_ok = hw.calib_workspace_bytes(8, 64, 4, 50, 3)
+
+    def call(hkv=2, hq=8, d=64, S=4, K=2, w=wins, n_hist=50, nr=3, r=rows, scale=sc,
+             ws=FAKE, wsb=ws_ok, ref=None, chk=None, scores=FAKE):
+        return L.hwkv_calib_replay(hkv, hq, d, S, K, w.ctypes.data, n_hist, FAKE, FAKE, nr,
+                                   r.ctypes.data, FAKE, scale, FAKE, scores, FAKE, ref, chk,
+                                   ws, wsb, None)
+    assert call(d=96) == hw.EINVAL
+    assert call(hq=6) == hw.EINVAL                  # G = 3
+    assert call(S=-1) == hw.EINVAL
+    assert call(w=np.array([64, 16], dtype=np.int64)) == hw.EINVAL
+    assert call(w=np.array([0, 16], dtype=np.int64)) == hw.EINVAL
+    assert call(r=np.array([9, 3, 40], dtype=np.int64)) == hw.EINVAL
+    assert call(r=np.array([3, 3, 40], dtype=np.int64)) == hw.EINVAL
+    assert call(r=np.array([3, 9, 50], dtype=np.int64)) == hw.EINVAL   # >= n_hist
+    assert call(scale=ctypes.c_float(float("nan"))) == hw.EINVAL
+    assert call(ws=None) == hw.EINVAL
+    assert call(wsb=ws_ok - 1) == hw.EINVAL
+    assert call(ref=FAKE) == hw.EINVAL               # check missing
+    assert call(scores=None) == hw.EINVAL
+    assert call(n_hist=0) == hw.EINVAL
+    n = ctypes.c_size_t()
+    assert L.hwkv_calib_workspace_bytes(8, 64, 4, 50, 0, ctypes.byref(n)) == hw.EINVAL
+    assert L.hwkv_calib_workspace_bytes(8, 96, 4, 50, 3, ctypes.byref(n)) == hw.EINVAL
+    ch = np.zeros(2, dtype=np.int32)
+    assert L.hwkv_calib_select(2, 2, wins.ctypes.data, 4, 100, None, ctypes.c_double(0.99),
+                               ch.ctypes.data, None) == hw.EINVAL
+    m = np.ones((2, 2))
+    assert L.hwkv_calib_select(2, 2, wins.ctypes.data, 4, 100, m.ctypes.data,
+                               ctypes.c_double(1.5), ch.ctypes.data, None) == hw.EINVAL
+    g = ctypes.c_int32()
+    assert L.hwkv_budget_select(0, None, None, ctypes.c_double(0.5), ctypes.byref(g)) == hw.EINVAL

@@ -52,6 +52,12 @@ CONFIGS = {
                     level_windows=[1024, 4096, 16384, FULL], levels=None,
                     prompt=None, prompt_range=(16384, 65536), steps=64,
                     max_ctx=65536 + 64, budget=(0.20, 0.25), rate_ctx=65536),
+    # calibration replay of one traced layer: a 128K-token trace, 256 query
+    # positions sampled from its final quarter, candidates {2K, 8K, 32K, full}.
+    "calib128k": dict(name="calib128k", seed=6, n_layers=1, batch=1, n_q_heads=24,
+                      n_kv_heads=4, head_dim=256, n_sinks=4,
+                      level_windows=[2048, 8192, 32768, FULL], levels=[[3, 3, 3, 3]],
+                      prompt=[131072], n_rows=256, steps=0, max_ctx=131072),
     # long prefill: 128K prompt in 8K chunks; kv head h gets level h.
     "prefill128k": dict(name="prefill128k", seed=5, n_layers=1, batch=1,
                         n_q_heads=24, n_kv_heads=4, head_dim=256, n_sinks=4,
@@ -172,6 +178,16 @@ def prefill_sample_rows(cfg, n_rows=512):
     r = rng(cfg["seed"], 0, SAMPLE, 0)
     extra = r.choice(rest, size=max(0, n_rows - len(edge)), replace=False)
     return sorted(edge + [int(x) for x in extra])
+
+
+def calib_rows(cfg):
+    """The calibration workload's query positions: ``n_rows`` distinct
+    positions drawn uniformly from the final quarter of the trace, ascending
+    (the paper samples 256 unique positions from the final quarter)."""
+    N = cfg["prompt"][0]
+    r = rng(cfg["seed"], 0, SAMPLE, 1)
+    return sorted(int(x) for x in r.choice(np.arange(N - N // 4, N), size=cfg["n_rows"],
+                                           replace=False))
 
 
 def windows_of(cfg, lv=None):
