@@ -91,6 +91,13 @@ int hwkv_policy_set(hwkv_policy **out, int32_t n_layers, int32_t n_kv_heads,
 
 int hwkv_policy_free(hwkv_policy *policy);
 
+/* Shape of a policy: layers, KV heads, query heads, head_dim, sink count and
+ * codebook size (any output pointer may be NULL). */
+int hwkv_policy_shape(const hwkv_policy *policy, int32_t *n_layers,
+                      int32_t *n_kv_heads, int32_t *n_q_heads, int32_t *head_dim,
+                      int32_t *n_sinks, int32_t *n_levels);
+
+
 /* Nominal K/V bytes of the policy at context ctx (Eq. nominal-storage with
  * bf16 K and V: r_C(w) * head_dim * (2 + 2) per unit and sequence, where
  * r_C(w) = min(S + w, ctx) for a finite window and ctx for full). */
@@ -279,6 +286,33 @@ int hwkv_calib_select(int32_t n_kv_heads, int32_t n_windows,
  * the budget. */
 int hwkv_budget_select(int32_t n_records, const double *rates,
                        const double *floors, double budget, int32_t *chosen);
+
+/* Calibration artifact (Appendix, experimental protocol: each run stores its
+ * artifact identifier, seed and final policy matrix; Appendix, finite-grid
+ * budget selection: run g is recorded as (g, tau_g, policy, rate, floor)).
+ * Text (JSON) of one object with the keys "format" ("hwkv-policy/1"),
+ * "artifact", "seed", "grid_index", "tau", "rate", "floor", "n_layers",
+ * "n_kv_heads", "n_q_heads", "head_dim", "n_sinks", "level_window" and
+ * "level_of_unit" ([n_layers][n_kv_heads]); doubles carry 17 significant
+ * digits, so they read back bit for bit.  Host only.
+ *
+ * Serialise: artifact_id is printable ASCII without '"' or '\\' (EINVAL
+ * otherwise).  *len receives the text length (without the terminating NUL);
+ * buf == NULL queries it; a buf of cap < *len + 1 bytes gets ENOMEM. */
+int hwkv_policy_serialize(const hwkv_policy *policy, const char *artifact_id,
+                          uint64_t seed, int32_t grid_index, double tau,
+                          double rate, double floor, char *buf, size_t cap,
+                          size_t *len);
+
+/* Parse an artifact written by hwkv_policy_serialize: a new policy in *out
+ * (validated as by hwkv_policy_set) and the recorded fields (each output
+ * pointer may be NULL; artifact_id receives at most id_cap - 1 characters
+ * and a NUL).  EINVAL on any other text: unknown, missing or repeated keys,
+ * malformed values, trailing characters. */
+int hwkv_policy_deserialize(const char *buf, size_t len, hwkv_policy **out,
+                            char *artifact_id, size_t id_cap, uint64_t *seed,
+                            int32_t *grid_index, double *tau, double *rate,
+                            double *floor);
 
 /* Kernel timing, for profiling.  While enabled (enable != 0) on a cache,
  * every hwkv_decode_attn / hwkv_append_decode_attn call records HIP events

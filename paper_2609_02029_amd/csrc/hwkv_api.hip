@@ -6,8 +6,13 @@
 #include "hwkv.h"
 
 #include <algorithm>
+#include <cerrno>
+#include <cinttypes>
 #include <cmath>
+#include <cstdio>
+#include <cstdlib>
 #include <cstring>
+#include <map>
 #include <new>
 #include <string>
 #include <vector>
@@ -311,6 +316,19 @@ int hwkv_policy_set(hwkv_policy **out, int32_t n_layers, int32_t n_kv_heads,
 
 int hwkv_policy_free(hwkv_policy *policy) {
   delete policy;
+  return ok();
+}
+
+int hwkv_policy_shape(const hwkv_policy *p, int32_t *n_layers, int32_t *n_kv_heads,
+                      int32_t *n_q_heads, int32_t *head_dim, int32_t *n_sinks,
+                      int32_t *n_levels) {
+  if (!p) return fail(HWKV_EINVAL, "policy is null");
+  if (n_layers) *n_layers = p->n_layers;
+  if (n_kv_heads) *n_kv_heads = p->n_kv_heads;
+  if (n_q_heads) *n_q_heads = p->n_q_heads;
+  if (head_dim) *head_dim = p->head_dim;
+  if (n_sinks) *n_sinks = p->n_sinks;
+  if (n_levels) *n_levels = p->n_levels;
   return ok();
 }
 
@@ -794,6 +812,226 @@ int hwkv_budget_select(int32_t n_records, const double *rates,
       g_best = g;                                  // earlier g wins full ties
   }
   *chosen = g_best;
+  return ok();
+}
+
+namespace {
+
+const char kArtifactFormat[] = "hwkv-policy/1";
+
+std::string fmt_double(double x) {
+  char b[64];
+  std::snprintf(b, sizeof b, "%.17g", x);
+  return b;
+}
+
+// A strict reader for the artifact's JSON subset: one object whose values
+// are strings without escapes, numbers, arrays of integers or arrays of
+// arrays of integers.
+struct ArtifactReader {
+  const char *p, *end;
+  bool ok = true;
+  void ws() {
+    while (p < end && (*p == ' ' || *p == '\n' || *p == '\t' || *p == '\r')) ++p;
+  }
+  bool eat(char c) {
+    ws();
+    if (p < end && *p == c) {
+      ++p;
+      return true;
+    }
+    return false;
+  }
+  bool string(std::string *out) {
+    ws();
+    if (p >= end || *p != '"') return false;
+    const char *q = ++p;
+    while (p < end && *p != '"') {
+      if (*p == '\\' || (unsigned char)*p < 0x20) return false;
+      ++p;
+    }
+    if (p >= end) return false;
+    out->assign(q, p);
+    ++p;
+    return true;
+  }
+  // the characters of a JSON number, then strtod / strtoll over them
+  bool number_text(std::string *t) {
+    ws();
+    const char *q = p;
+    while (p < end && (std::strchr("+-0123456789.eE", *p) != nullptr)) ++p;
+    if (p == q) return false;
+    t->assign(q, p);
+    return true;
+  }
+  bool dbl(double *x) {
+    std::string t;
+    if (!number_text(&t)) return false;
+    char *e = nullptr;
+    *x = std::strtod(t.c_str(), &e);
+    return e && *e == '\0';
+  }
+  bool i64(int64_t *x) {
+    std::string t;
+    if (!number_text(&t)) return false;
+    if (t.find_first_of(".eE") != std::string::npos) return false;
+    char *e = nullptr;
+    errno = 0;
+    const long long v = std::strtoll(t.c_str(), &e, 10);
+    if (!e || *e != '\0' || errno) return false;
+    *x = v;
+    return true;
+  }
+  bool u64(uint64_t *x) {
+    std::string t;
+    if (!number_text(&t)) return false;
+    if (t.find_first_not_of("0123456789") != std::string::npos) return false;
+    char *e = nullptr;
+    errno = 0;
+    const unsigned long long v = std::strtoull(t.c_str(), &e, 10);
+    if (!e || *e != '\0' || errno) return false;
+    *x = v;
+    return true;
+  }
+  bool int_array(std::vector<int64_t> *v) {
+    if (!eat('[')) return false;
+    v->clear();
+    if (eat(']')) return true;
+    do {
+      int64_t x;
+      if (!i64(&x)) return false;
+      v->push_back(x);
+    } while (eat(','));
+    return eat(']');
+  }
+};
+
+}  // namespace
+
+int hwkv_policy_serialize(const hwkv_policy *p, const char *artifact_id, uint64_t seed,
+                          int32_t grid_index, double tau, double rate, double floor,
+                          char *buf, size_t cap, size_t *len) {
+  if (!p || !artifact_id || !len) return fail(HWKV_EINVAL, "policy, artifact_id and len required");
+  for (const char *c = artifact_id; *c; ++c)
+    if ((unsigned char)*c < 0x20 || (unsigned char)*c > 0x7e || *c == '"' || *c == '\\')
+      return fail(HWKV_EINVAL, "artifact_id must be printable ASCII without quote or backslash");
+  if (!std::isfinite(tau) || !std::isfinite(rate) || !std::isfinite(floor))
+    return fail(HWKV_EINVAL, "tau, rate and floor must be finite");
+  std::string t = "{\n";
+  t += "  \"format\": \"" + std::string(kArtifactFormat) + "\",\n";
+  t += "  \"artifact\": \"" + std::string(artifact_id) + "\",\n";
+  t += "  \"seed\": " + std::to_string(seed) + ",\n";
+  t += "  \"grid_index\": " + std::to_string(grid_index) + ",\n";
+  t += "  \"tau\": " + fmt_double(tau) + ",\n";
+  t += "  \"rate\": " + fmt_double(rate) + ",\n";
+  t += "  \"floor\": " + fmt_double(floor) + ",\n";
+  t += "  \"n_layers\": " + std::to_string(p->n_layers) + ",\n";
+  t += "  \"n_kv_heads\": " + std::to_string(p->n_kv_heads) + ",\n";
+  t += "  \"n_q_heads\": " + std::to_string(p->n_q_heads) + ",\n";
+  t += "  \"head_dim\": " + std::to_string(p->head_dim) + ",\n";
+  t += "  \"n_sinks\": " + std::to_string(p->n_sinks) + ",\n";
+  t += "  \"level_window\": [";
+  for (int32_t k = 0; k < p->n_levels; ++k)
+    t += (k ? ", " : "") + std::to_string(p->level_window[k]);
+  t += "],\n  \"level_of_unit\": [";
+  for (int32_t l = 0; l < p->n_layers; ++l) {
+    t += l ? ",\n    [" : "\n    [";
+    for (int32_t h = 0; h < p->n_kv_heads; ++h)
+      t += (h ? ", " : "") + std::to_string(p->level_of_unit[(size_t)l * p->n_kv_heads + h]);
+    t += "]";
+  }
+  t += "\n  ]\n}\n";
+  *len = t.size();
+  if (!buf) return ok();
+  if (cap < t.size() + 1) return fail(HWKV_ENOMEM, "buffer too small for the artifact");
+  std::memcpy(buf, t.c_str(), t.size() + 1);
+  return ok();
+}
+
+int hwkv_policy_deserialize(const char *buf, size_t len, hwkv_policy **out,
+                            char *artifact_id, size_t id_cap, uint64_t *seed,
+                            int32_t *grid_index, double *tau, double *rate,
+                            double *floor) {
+  if (!buf || !out) return fail(HWKV_EINVAL, "buf and out required");
+  ArtifactReader r{buf, buf + len};
+  std::map<std::string, int> seen;
+  std::string fmt, id;
+  uint64_t sd = 0;
+  int64_t gi = 0, L = 0, H = 0, Q = 0, D = 0, S = 0;
+  double ta = 0, ra = 0, fl = 0;
+  std::vector<int64_t> lw, lou;
+  int64_t rows_read = 0;
+  if (!r.eat('{')) return fail(HWKV_EINVAL, "artifact: expected an object");
+  do {
+    std::string key;
+    if (!r.string(&key) || !r.eat(':')) return fail(HWKV_EINVAL, "artifact: expected a key");
+    if (seen[key]++) return fail(HWKV_EINVAL, "artifact: repeated key " + key);
+    bool good;
+    if (key == "format") good = r.string(&fmt);
+    else if (key == "artifact") good = r.string(&id);
+    else if (key == "seed") good = r.u64(&sd);
+    else if (key == "grid_index") good = r.i64(&gi);
+    else if (key == "tau") good = r.dbl(&ta);
+    else if (key == "rate") good = r.dbl(&ra);
+    else if (key == "floor") good = r.dbl(&fl);
+    else if (key == "n_layers") good = r.i64(&L);
+    else if (key == "n_kv_heads") good = r.i64(&H);
+    else if (key == "n_q_heads") good = r.i64(&Q);
+    else if (key == "head_dim") good = r.i64(&D);
+    else if (key == "n_sinks") good = r.i64(&S);
+    else if (key == "level_window") good = r.int_array(&lw);
+    else if (key == "level_of_unit") {
+      good = r.eat('[');
+      lou.clear();
+      rows_read = 0;
+      if (good && !r.eat(']')) {
+        do {
+          std::vector<int64_t> row;
+          good = r.int_array(&row);
+          if (!good) break;
+          if (rows_read > 0 && (int64_t)row.size() * rows_read != (int64_t)lou.size()) {
+            good = false;
+            break;
+          }
+          lou.insert(lou.end(), row.begin(), row.end());
+          ++rows_read;
+        } while (r.eat(','));
+        good = good && r.eat(']');
+      }
+    } else {
+      return fail(HWKV_EINVAL, "artifact: unknown key " + key);
+    }
+    if (!good) return fail(HWKV_EINVAL, "artifact: malformed value of " + key);
+  } while (r.eat(','));
+  if (!r.eat('}')) return fail(HWKV_EINVAL, "artifact: expected '}'");
+  r.ws();
+  if (r.p != r.end) return fail(HWKV_EINVAL, "artifact: trailing characters");
+  if (seen.size() != 14) return fail(HWKV_EINVAL, "artifact: missing keys");
+  if (fmt != kArtifactFormat) return fail(HWKV_EINVAL, "artifact: unknown format " + fmt);
+  if (L < 1 || L > INT32_MAX || H < 1 || H > INT32_MAX || Q > INT32_MAX || D > INT32_MAX ||
+      S < 0 || S > INT32_MAX || gi < INT32_MIN || gi > INT32_MAX || lw.size() > INT32_MAX ||
+      rows_read != L || (int64_t)lou.size() != L * H)
+    return fail(HWKV_EINVAL, "artifact: inconsistent shape");
+  std::vector<int32_t> lev(lou.size());
+  for (size_t i = 0; i < lou.size(); ++i) {
+    if (lou[i] < INT32_MIN || lou[i] > INT32_MAX) return fail(HWKV_EINVAL, "artifact: level");
+    lev[i] = (int32_t)lou[i];
+  }
+  hwkv_policy *p = nullptr;
+  const int rc = hwkv_policy_set(&p, (int32_t)L, (int32_t)H, (int32_t)Q, (int32_t)D, (int32_t)S,
+                                 (int32_t)lw.size(), lw.data(), lev.data());
+  if (rc != HWKV_OK) return rc;
+  *out = p;
+  if (artifact_id && id_cap > 0) {
+    const size_t n = std::min(id.size(), id_cap - 1);
+    std::memcpy(artifact_id, id.data(), n);
+    artifact_id[n] = '\0';
+  }
+  if (seed) *seed = sd;
+  if (grid_index) *grid_index = (int32_t)gi;
+  if (tau) *tau = ta;
+  if (rate) *rate = ra;
+  if (floor) *floor = fl;
   return ok();
 }
 

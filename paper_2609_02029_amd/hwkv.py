@@ -58,6 +58,13 @@ SYMBOLS = {
                            _flt, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp], ctypes.c_int),
     "hwkv_calib_select": ([_i32, _i32, _vp, _i32, _i64, _vp, _dbl, _vp, _P(_dbl)], ctypes.c_int),
     "hwkv_budget_select": ([_i32, _vp, _vp, _dbl, _P(_i32)], ctypes.c_int),
+    "hwkv_policy_shape": ([_vp, _P(_i32), _P(_i32), _P(_i32), _P(_i32), _P(_i32), _P(_i32)],
+                          ctypes.c_int),
+    "hwkv_policy_serialize": ([_vp, ctypes.c_char_p, ctypes.c_uint64, _i32, _dbl, _dbl, _dbl,
+                               _vp, _sz, _P(_sz)], ctypes.c_int),
+    "hwkv_policy_deserialize": ([ctypes.c_char_p, _sz, _P(_vp), _vp, _sz,
+                                 _P(ctypes.c_uint64), _P(_i32), _P(_dbl), _P(_dbl), _P(_dbl)],
+                                ctypes.c_int),
 }
 for _name, (_args, _res) in SYMBOLS.items():
     _f = getattr(_lib, _name)
@@ -367,3 +374,36 @@ def budget_select(rates, floors, budget):
     _check(_lib.hwkv_budget_select(r.size, r.ctypes.data, f.ctypes.data, float(budget),
                                    ctypes.byref(g)))
     return None if g.value < 0 else g.value
+
+
+def policy_serialize(policy, artifact, seed, grid_index, tau, rate, floor):
+    """The calibration artifact of ``policy`` as text (the keyword names match
+    the record ``policy_deserialize`` returns)."""
+    n = _sz()
+    aid = artifact.encode("ascii")
+    _check(_lib.hwkv_policy_serialize(policy.handle, aid, int(seed), int(grid_index), float(tau),
+                                      float(rate), float(floor), None, 0, ctypes.byref(n)))
+    buf = ctypes.create_string_buffer(n.value + 1)
+    _check(_lib.hwkv_policy_serialize(policy.handle, aid, int(seed), int(grid_index), float(tau),
+                                      float(rate), float(floor), buf, n.value + 1,
+                                      ctypes.byref(n)))
+    return buf.value.decode("ascii")
+
+
+def policy_deserialize(text):
+    """Parses an artifact: returns (Policy, dict of the recorded fields)."""
+    raw = text.encode("ascii") if isinstance(text, str) else bytes(text)
+    h = _vp()
+    aid = ctypes.create_string_buffer(256)
+    seed, gi = ctypes.c_uint64(), _i32()
+    tau, rate, fl = _dbl(), _dbl(), _dbl()
+    _check(_lib.hwkv_policy_deserialize(raw, len(raw), ctypes.byref(h), aid, 256,
+                                        ctypes.byref(seed), ctypes.byref(gi), ctypes.byref(tau),
+                                        ctypes.byref(rate), ctypes.byref(fl)))
+    p = Policy(h.value)
+    L, H, Q, D = _i32(), _i32(), _i32(), _i32()
+    _check(_lib.hwkv_policy_shape(p.handle, ctypes.byref(L), ctypes.byref(H), ctypes.byref(Q),
+                                  ctypes.byref(D), None, None))
+    p.n_layers, p.n_kv_heads, p.n_q_heads, p.head_dim = L.value, H.value, Q.value, D.value
+    return p, dict(artifact=aid.value.decode("ascii"), seed=seed.value, grid_index=gi.value,
+                   tau=tau.value, rate=rate.value, floor=fl.value)

@@ -317,3 +317,72 @@ def test_calib_host_errors(hw):
                                ctypes.c_double(1.5), ch.ctypes.data, None) == hw.EINVAL
     g = ctypes.c_int32()
     assert L.hwkv_budget_select(0, None, None, ctypes.c_double(0.5), ctypes.byref(g)) == hw.EINVAL
+
+
+def test_policy_artifact_format(hw, golden):
+    g = golden("policy_artifact.json")
+    a = g["inputs"]
+    p = hw.policy_set(a["n_layers"], a["n_kv_heads"], a["n_q_heads"], a["head_dim"],
+                      a["n_sinks"], a["level_window"], a["level_of_unit"])
+    text = hw.policy_serialize(p, a["artifact"], a["seed"], a["grid_index"], a["tau"], a["rate"],
+                               a["floor"])
+    assert text == g["text"]
+    q, meta = hw.policy_deserialize(g["text"])
+    assert meta == {k: a[k] for k in ("artifact", "seed", "grid_index", "tau", "rate", "floor")}
+    assert (q.n_layers, q.n_kv_heads, q.n_q_heads, q.head_dim) == (2, 2, 8, 64)
+
+
+def test_policy_artifact_round_trip(hw):
+    r = np.random.default_rng(9)
+    for _ in range(100):
+        L, H = int(r.integers(1, 6)), int(r.choice([1, 2, 4]))
+        lw = [int(x) for x in r.integers(1, 100000, size=int(r.integers(1, 5)))] + [0]
+        lv = r.integers(0, len(lw), size=(L, H)).tolist()
+        S = int(r.integers(0, 9))
+        p = hw.policy_set(L, H, H * int(r.choice([1, 2, 4, 6, 8])), int(r.choice([64, 128, 256])),
+                          S, lw, lv)
+        meta = dict(artifact=f"r{int(r.integers(1 << 30))}", seed=int(r.integers(0, 1 << 63)),
+                    grid_index=int(r.integers(0, 50)), tau=float(r.random()),
+                    rate=float(r.random()), floor=float(r.random()))
+        text = hw.policy_serialize(p, **meta)
+        q, back = hw.policy_deserialize(text)
+        assert back == meta                                   # doubles bit for bit
+        assert hw.policy_serialize(q, **meta) == text
+        for ctx in (1, 1000, 123457):
+            assert hw.policy_rate(q, ctx) == hw.policy_rate(p, ctx)
+            assert hw.policy_bytes(q, ctx) == hw.policy_bytes(p, ctx)
+
+
+def test_policy_artifact_rejects_malformed_text(hw, golden):
+    good = golden("policy_artifact.json")["text"]
+    bad = [
+        good.replace('"format": "hwkv-policy/1"', '"format": "hwkv-policy/2"'),
+        good.replace('  "seed": 42,\n', ''),                             # missing key
+        good.replace('"seed": 42,', '"seed": 42,\n  "seed": 43,'),        # repeated key
+        good.replace('"seed": 42,', '"seed": 42,\n  "colour": 1,'),       # unknown key
+        good + "x",                                                       # trailing text
+        good[:-10],                                                       # truncated
+        good.replace('[1, 1]\n', '[1, 1.5]\n'),                           # non-integer level
+        good.replace('[1, 1]\n', '[1]\n'),                                # ragged rows
+        good.replace('[1, 1]\n', '[1, 2]\n'),                             # level out of range
+        good.replace('"n_layers": 2', '"n_layers": 3'),                   # shape mismatch
+        good.replace('"seed": 42', '"seed": -42'),
+        good.replace('"tau": 0.5', '"tau": "0.5"'),
+        good.replace('"run-1"', '"run\\"1"'),
+    ]
+    for text in bad:
+        with pytest.raises(hw.HwkvError) as e:
+            hw.policy_deserialize(text)
+        assert e.value.code == hw.EINVAL, text
+    p = hw.policy_set(1, 1, 1, 64, 0, [0], [[0]])
+    for aid in ('a"b', "a\\b", "tab\there", "é"):
+        with pytest.raises((hw.HwkvError, UnicodeEncodeError)):
+            hw.policy_serialize(p, aid, 1, 0, 0.5, 0.5, 1.0)
+    n = ctypes.c_size_t()
+    assert hw._lib.hwkv_policy_serialize(p.handle, b"x", 1, 0, ctypes.c_double(0.5),
+                                         ctypes.c_double(0.5), ctypes.c_double(1.0), None, 0,
+                                         ctypes.byref(n)) == hw.OK
+    small = ctypes.create_string_buffer(n.value)                          # no room for the NUL
+    assert hw._lib.hwkv_policy_serialize(p.handle, b"x", 1, 0, ctypes.c_double(0.5),
+                                         ctypes.c_double(0.5), ctypes.c_double(1.0), small,
+                                         n.value, ctypes.byref(n)) == hw.ENOMEM
