@@ -256,7 +256,7 @@ def measured_traffic(args):
             rec = json.load(f)
     except (OSError, ValueError):
         return None, None
-    if rec.get("kernel_source_sha256_16") != profiling.kernel_source_hash():
+    if rec.get("kernel_source_sha256_16") != profiling.kernel_source_hash(rec["kernel"]):
         return None, "counter record is stale: decode kernel source changed"
     total = rec["fetch_bytes"] + rec["write_bytes"]
     return round(total), {"fetch_bytes": round(rec["fetch_bytes"]),

@@ -58,6 +58,25 @@ extern "C" {
 #define HWKV_ESTATE 4    /* call does not match the cache state */
 #define HWKV_EDEVICE 5   /* HIP runtime or launch error */
 
+/* Cache formats p_KV of the stored keys and values (Method, Eq.
+ * nominal-storage: the format enters the storage through the effective bytes
+ * per element b^K, b^V; a format that changes numerical execution is used by
+ * every reader of the cache).  Inputs are always bf16; the cache stores:
+ *   HWKV_KV_BF16      the bf16 input as is (2 bytes per element);
+ *   HWKV_KV_F16       IEEE binary16 of the input, round to nearest even,
+ *                     overflow to infinity (2 bytes);
+ *   HWKV_KV_FP8_E4M3  OCP FP8 E4M3 ("E4M3FN": bias 7, subnormals m * 2^-9,
+ *                     largest finite 448, no infinities, S.1111.111 = NaN) of
+ *                     x / s, where s is the fp32 scale of the element's
+ *                     (layer, KV head) and tensor (K or V): the quotient is the
+ *                     correctly rounded fp32 division, rounded to nearest even
+ *                     and saturated to +-448, NaN kept (1 byte).
+ * The value an element contributes to attention is its stored value (times s
+ * for fp8). */
+#define HWKV_KV_BF16 0
+#define HWKV_KV_F16 1
+#define HWKV_KV_FP8_E4M3 2
+
 typedef struct hwkv_policy hwkv_policy;
 typedef struct hwkv_cache hwkv_cache;
 
@@ -103,6 +122,11 @@ int hwkv_policy_shape(const hwkv_policy *policy, int32_t *n_layers,
  * r_C(w) = min(S + w, ctx) for a finite window and ctx for full). */
 int hwkv_policy_bytes(const hwkv_policy *policy, int64_t ctx, double *bytes);
 
+/* Eq. nominal-storage under cache format kv_format: r_C(w) * head_dim *
+ * (b^K + b^V) per unit and sequence, with b = 2 (bf16, f16) or 1 (fp8). */
+int hwkv_policy_bytes_format(const hwkv_policy *policy, int64_t ctx,
+                             int32_t kv_format, double *bytes);
+
 /* Normalized rate R_C (Eq. normalized-rate): nominal bytes divided by the
  * all-full policy's nominal bytes at the same ctx.  Host only. */
 int hwkv_policy_rate(const hwkv_policy *policy, int64_t ctx, double *rate);
@@ -124,6 +148,12 @@ int hwkv_policy_rate(const hwkv_policy *policy, int64_t ctx, double *rate);
 int hwkv_cache_bytes(const hwkv_policy *policy, int32_t batch, int64_t max_ctx,
                      size_t *bytes);
 
+/* hwkv_cache_bytes for a cache of format kv_format: element size b (2 or 1)
+ * in place of 2, and the limit max_ctx (rounded up to 64) * head_dim * b <
+ * 2^31.  EINVAL on an unknown format. */
+int hwkv_cache_bytes_format(const hwkv_policy *policy, int32_t batch,
+                            int64_t max_ctx, int32_t kv_format, size_t *bytes);
+
 /* Allocate a cache.  dev_buf == NULL: the library allocates (hipMalloc on the
  * current device), zero-fills, and owns the memory.  Otherwise the caller's
  * device buffer of buf_bytes is adopted as is (ENOMEM if smaller than
@@ -132,6 +162,22 @@ int hwkv_cache_bytes(const hwkv_policy *policy, int32_t batch, int64_t max_ctx,
 int hwkv_cache_alloc(hwkv_cache **out, const hwkv_policy *policy,
                      int32_t batch, int64_t max_ctx, void *dev_buf,
                      size_t buf_bytes);
+
+/* hwkv_cache_alloc for a cache of format kv_format (hwkv_cache_alloc is the
+ * bf16 case).  k_scale, v_scale: host fp32 [n_layers][n_kv_heads], the fp8
+ * scales s of K and V per unit (copied; NULL = all 1.0); each must be
+ * positive, finite and normal.  For the 16-bit formats they must be NULL.
+ * Buffer size rules as for hwkv_cache_alloc with hwkv_cache_bytes_format.
+ * EINVAL on an unknown format or a bad scale. */
+int hwkv_cache_alloc_format(hwkv_cache **out, const hwkv_policy *policy,
+                            int32_t batch, int64_t max_ctx, int32_t kv_format,
+                            const float *k_scale, const float *v_scale,
+                            void *dev_buf, size_t buf_bytes);
+
+/* Format of a cache and, if the pointers are non-NULL, its scales (host fp32
+ * [n_layers][n_kv_heads] each; all 1.0 for the 16-bit formats). */
+int hwkv_cache_format(const hwkv_cache *cache, int32_t *kv_format,
+                      float *k_scale, float *v_scale);
 
 /* Release the cache; frees device memory only if the library allocated it.
  * The caller must make sure no enqueued work still uses the cache. */
@@ -156,7 +202,8 @@ int hwkv_cache_unit_info(const hwkv_cache *cache, int32_t layer,
  * length pos0 + n_tokens are written, each into its slot; no full-length
  * cache is ever formed (Method, physical residency; Intro: storage shrinks
  * before the cache is built).  Then n(layer, seq) = pos0 + n_tokens.
- *   k, v   device bf16 [n_tokens][n_kv_heads][head_dim], post-RoPE keys.
+ *   k, v   device bf16 [n_tokens][n_kv_heads][head_dim], post-RoPE keys,
+ *          stored in the cache's format.
  * ESTATE if pos0 != n(layer, seq); ECAPACITY if a full unit would pass
  * max_ctx; n_tokens == 0 is a no-op. */
 int hwkv_prefill_write(hwkv_cache *cache, int32_t layer, int32_t seq,
@@ -177,8 +224,8 @@ int hwkv_prefill_write(hwkv_cache *cache, int32_t layer, int32_t seq,
  * bf16 MFMA products with fp32 accumulation; the softmax weights enter the
  * value product rounded to bf16.  ESTATE if pos0 != n(layer, seq);
  * ECAPACITY if pos0 + n_tokens > max_ctx; EINVAL on bad indices, null
- * pointers or a non-finite or non-positive scale; n_tokens == 0 is a
- * no-op. */
+ * pointers, a non-finite or non-positive scale, or a cache whose format is
+ * not bf16; n_tokens == 0 is a no-op. */
 int hwkv_prefill_attn(hwkv_cache *cache, int32_t layer, int32_t seq,
                       int64_t pos0, int64_t n_tokens, const void *q,
                       const void *k, const void *v, float scale, void *out,
@@ -187,7 +234,8 @@ int hwkv_prefill_attn(hwkv_cache *cache, int32_t layer, int32_t seq,
 /* Append one token to every sequence of `layer`: token n_b of sequence b
  * goes to slot(n_b) of each unit (once n_b >= S + w this overwrites token
  * n_b - w, the one leaving the window), then n_b += 1.
- *   k_new, v_new   device bf16 [batch][n_kv_heads][head_dim].
+ *   k_new, v_new   device bf16 [batch][n_kv_heads][head_dim], stored in
+ *                  the cache's format.
  * ECAPACITY if a full unit of the layer already holds max_ctx tokens. */
 int hwkv_append(hwkv_cache *cache, int32_t layer, const void *k_new,
                 const void *v_new, void *stream);
@@ -206,7 +254,10 @@ int hwkv_decode_workspace_bytes(const hwkv_cache *cache, size_t *bytes);
  *         concatenated)
  *   ws    device workspace of ws_bytes >= hwkv_decode_workspace_bytes
  * EINVAL if a sequence is empty or the workspace is short.  Does not change
- * state.  Fp32 accumulation; the result does not depend on the slot order. */
+ * state.  Fp32 accumulation; the result does not depend on the slot order.
+ * Keys and values enter with their stored values: for fp8, q.k is taken over
+ * the decoded codes and multiplied by the K scale, and the output by the V
+ * scale. */
 int hwkv_decode_attn(hwkv_cache *cache, int32_t layer, const void *q,
                      float scale, void *out, void *ws, size_t ws_bytes,
                      void *stream);
@@ -330,8 +381,10 @@ int hwkv_decode_timing_read(hwkv_cache *cache, double *split_ms,
 
 /* Test hook: synchronously copy unit (layer, kv_head) of sequence `seq` to
  * the host after all device work completes.  host_k, host_v receive
- * [capacity][head_dim] bf16 in slot order; *n_valid = min(n, capacity), the
- * number of occupied slots.  Slots >= n_valid hold unspecified values. */
+ * [capacity][head_dim] stored elements in slot order (bf16 or binary16 bit
+ * patterns, 2 bytes each, or E4M3 codes, 1 byte each); *n_valid =
+ * min(n, capacity), the number of occupied slots.  Slots >= n_valid hold
+ * unspecified values. */
 int hwkv_cache_read_unit(const hwkv_cache *cache, int32_t layer,
                          int32_t kv_head, int32_t seq, void *host_k,
                          void *host_v, int64_t *n_valid);

@@ -17,7 +17,8 @@ LIB = os.path.join(LIBDIR, "libhwkv.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["hwkv_api.hip", "decode_kernels.hip", "write_kernels.hip",
+SOURCES = ["hwkv_api.hip", "decode_kernels.hip", "decode_split_bf16.hip",
+           "decode_split_f16.hip", "decode_split_fp8.hip", "write_kernels.hip",
            "prefill_attn_kernels.hip", "calib_kernels.hip"]
 
 CFLAGS = [

@@ -1,0 +1,8 @@
+// decode_split_fp8.hip -- decode split kernels for fp8-e4m3 caches (all head
+// dims and group sizes).
+#include "decode_split.h"
+
+namespace hwkv {
+template hipError_t launch_decode_split_fmt<HWKV_KV_FP8_E4M3>(int, int, const DecodeArgs &,
+                                                   int, hipStream_t);
+}  // namespace hwkv

@@ -37,7 +37,11 @@ struct hwkv_cache {
   std::vector<int64_t> k_off;    // element offset of (u, seq 0); seq stride
   std::vector<int64_t> v_off;    //   is cap_pad * head_dim
   std::vector<int64_t> n;        // [layer * batch + b] sequence lengths
-  uint16_t *base = nullptr;
+  int32_t fmt = HWKV_KV_BF16;    // cache format (HWKV_KV_*)
+  int32_t elem = 2;              // bytes per stored element
+  std::vector<float> k_scale;    // per unit (fp8 scales; 1 otherwise)
+  std::vector<float> v_scale;
+  uint8_t *base = nullptr;
   size_t bytes = 0;
   bool owned = false;
   size_t ws_bytes = 0;
@@ -69,6 +73,16 @@ int64_t round_tile(int64_t x) {
   return (x + hwkv::kTile - 1) / hwkv::kTile * hwkv::kTile;
 }
 
+// Bytes per stored element of a cache format, or 0 if unknown.
+int format_bytes(int32_t fmt) {
+  switch (fmt) {
+    case HWKV_KV_BF16: return 2;
+    case HWKV_KV_F16: return 2;
+    case HWKV_KV_FP8_E4M3: return 1;
+    default: return 0;
+  }
+}
+
 // Canonical window and capacity of a finite or full unit at max_ctx.
 void unit_shape(const hwkv_policy &p, int32_t u, int64_t max_ctx,
                 int64_t *window, int64_t *cap) {
@@ -82,16 +96,18 @@ void unit_shape(const hwkv_policy &p, int32_t u, int64_t max_ctx,
   }
 }
 
-// Lays out the grouped pools; fills per-unit vectors when `c` is non-null.
-int layout(const hwkv_policy &p, int32_t batch, int64_t max_ctx, size_t *bytes,
-           hwkv_cache *c) {
+// Lays out the grouped pools for elements of `elem` bytes; fills per-unit
+// vectors when `c` is non-null.
+int layout(const hwkv_policy &p, int32_t batch, int64_t max_ctx, int elem,
+           size_t *bytes, hwkv_cache *c) {
   if (batch < 1) return fail(HWKV_EINVAL, "batch must be >= 1");
   // the decode kernels address one (unit, sequence) region with 32-bit byte
-  // offsets: round_tile(max_ctx) * head_dim * 2 must stay below 2^31
+  // offsets: round_tile(max_ctx) * head_dim * elem must stay below 2^31
   if (max_ctx < 1 ||
-      round_tile(max_ctx) * (int64_t)p.head_dim * 2 > (int64_t)INT32_MAX)
-    return fail(HWKV_EINVAL, "max_ctx must be >= 1 and max_ctx * head_dim * 2 "
-                             "below 2^31 (bytes of one unit's K or V)");
+      round_tile(max_ctx) * (int64_t)p.head_dim * elem > (int64_t)INT32_MAX)
+    return fail(HWKV_EINVAL, "max_ctx must be >= 1 and max_ctx * head_dim * "
+                             "element bytes below 2^31 (bytes of one unit's K "
+                             "or V)");
   const int32_t U = p.n_layers * p.n_kv_heads;
   const uint64_t D = (uint64_t)p.head_dim;
   std::vector<int64_t> win(U), cap(U), capp(U), koff(U), voff(U);
@@ -117,7 +133,7 @@ int layout(const hwkv_policy &p, int32_t batch, int64_t max_ctx, size_t *bytes,
       }
     }
   }
-  *bytes = (size_t)(off * 2);
+  *bytes = (size_t)(off * (uint64_t)elem);
   if (c) {
     c->window = win;
     c->cap = cap;
@@ -230,6 +246,8 @@ int decode_impl(hwkv_cache *c, int32_t layer, const void *k_new,
       a.it.new_slot[j] = nslot[i];
       a.it.q_row[j] = b * p.n_q_heads + h * G;
       a.it.kv_row[j] = b * H + h;
+      a.it.k_scale[j] = c->k_scale[u];
+      a.it.v_scale[j] = c->v_scale[u];
       a.it.split_begin[j] = splits;
       splits += ns[i];
     }
@@ -247,8 +265,9 @@ int decode_impl(hwkv_cache *c, int32_t layer, const void *k_new,
         cnt * hwkv::decode_combine_blocks_per_item(p.head_dim, G);
     int rc;
     if (c->timing && (rc = record_event(c, s)) != HWKV_OK) return rc;
-    rc = check_device(hwkv::launch_decode_split(p.head_dim, G, a, splits, s),
-                      "decode split launch");
+    rc = check_device(
+        hwkv::launch_decode_split(c->fmt, p.head_dim, G, a, splits, s),
+        "decode split launch");
     if (rc != HWKV_OK) return rc;  // earlier launches of this call may run
     if (c->timing && (rc = record_event(c, s)) != HWKV_OK) return rc;
     rc = check_device(
@@ -333,10 +352,17 @@ int hwkv_policy_shape(const hwkv_policy *p, int32_t *n_layers, int32_t *n_kv_hea
 }
 
 int hwkv_policy_bytes(const hwkv_policy *p, int64_t ctx, double *bytes) {
+  return hwkv_policy_bytes_format(p, ctx, HWKV_KV_BF16, bytes);
+}
+
+int hwkv_policy_bytes_format(const hwkv_policy *p, int64_t ctx,
+                             int32_t kv_format, double *bytes) {
   if (!p || !bytes) return fail(HWKV_EINVAL, "null argument");
   if (ctx < 1) return fail(HWKV_EINVAL, "ctx must be >= 1");
+  const int b = format_bytes(kv_format);
+  if (b == 0) return fail(HWKV_EINVAL, "unknown cache format");
   double tot = 0.0;
-  const double row = (double)p->head_dim * (2.0 + 2.0);
+  const double row = (double)p->head_dim * (double)(b + b);  // d^K b^K + d^V b^V
   for (int32_t lv : p->level_of_unit) {
     const int64_t w = p->level_window[lv];
     const int64_t r = (w == 0) ? ctx : std::min<int64_t>(p->n_sinks + w, ctx);
@@ -359,23 +385,55 @@ int hwkv_policy_rate(const hwkv_policy *p, int64_t ctx, double *rate) {
 
 int hwkv_cache_bytes(const hwkv_policy *p, int32_t batch, int64_t max_ctx,
                      size_t *bytes) {
+  return hwkv_cache_bytes_format(p, batch, max_ctx, HWKV_KV_BF16, bytes);
+}
+
+int hwkv_cache_bytes_format(const hwkv_policy *p, int32_t batch,
+                            int64_t max_ctx, int32_t kv_format, size_t *bytes) {
   if (!p || !bytes) return fail(HWKV_EINVAL, "null argument");
-  const int rc = layout(*p, batch, max_ctx, bytes, nullptr);
+  const int elem = format_bytes(kv_format);
+  if (elem == 0) return fail(HWKV_EINVAL, "unknown cache format");
+  const int rc = layout(*p, batch, max_ctx, elem, bytes, nullptr);
   return rc == HWKV_OK ? ok() : rc;
 }
 
 int hwkv_cache_alloc(hwkv_cache **out, const hwkv_policy *p, int32_t batch,
                      int64_t max_ctx, void *dev_buf, size_t buf_bytes) {
+  return hwkv_cache_alloc_format(out, p, batch, max_ctx, HWKV_KV_BF16, nullptr,
+                                 nullptr, dev_buf, buf_bytes);
+}
+
+int hwkv_cache_alloc_format(hwkv_cache **out, const hwkv_policy *p,
+                            int32_t batch, int64_t max_ctx, int32_t kv_format,
+                            const float *k_scale, const float *v_scale,
+                            void *dev_buf, size_t buf_bytes) {
   if (!out || !p) return fail(HWKV_EINVAL, "null argument");
   *out = nullptr;
+  const int elem = format_bytes(kv_format);
+  if (elem == 0) return fail(HWKV_EINVAL, "unknown cache format");
+  const size_t n_units = (size_t)p->n_layers * p->n_kv_heads;
+  if (kv_format != HWKV_KV_FP8_E4M3 && (k_scale || v_scale))
+    return fail(HWKV_EINVAL, "scales are for fp8 caches only");
+  for (const float *sc : {k_scale, v_scale}) {
+    if (!sc) continue;
+    for (size_t u = 0; u < n_units; ++u)
+      if (!(std::isnormal(sc[u]) && sc[u] > 0.f))
+        return fail(HWKV_EINVAL, "fp8 scales must be positive, finite and normal");
+  }
   hwkv_cache *c = nullptr;
   try {
     c = new hwkv_cache;
     c->pol = *p;
     c->batch = batch;
     c->max_ctx = max_ctx;
+    c->fmt = kv_format;
+    c->elem = elem;
+    c->k_scale.assign(n_units, 1.0f);
+    c->v_scale.assign(n_units, 1.0f);
+    if (k_scale) c->k_scale.assign(k_scale, k_scale + n_units);
+    if (v_scale) c->v_scale.assign(v_scale, v_scale + n_units);
     size_t bytes = 0;
-    int rc = layout(*p, batch, max_ctx, &bytes, c);
+    int rc = layout(*p, batch, max_ctx, elem, &bytes, c);
     if (rc != HWKV_OK) {
       delete c;
       return rc;
@@ -397,7 +455,7 @@ int hwkv_cache_alloc(hwkv_cache **out, const hwkv_policy *p, int32_t batch,
         return fail(HWKV_ENOMEM, "device buffer smaller than cache bytes (" +
                                      std::to_string(bytes) + ")");
       }
-      c->base = static_cast<uint16_t *>(dev_buf);
+      c->base = static_cast<uint8_t *>(dev_buf);
       c->owned = false;
     } else {
       void *ptr = nullptr;
@@ -414,7 +472,7 @@ int hwkv_cache_alloc(hwkv_cache **out, const hwkv_policy *p, int32_t batch,
         delete c;
         return fail(HWKV_EDEVICE, std::string("hipMemset: ") + hipGetErrorString(e));
       }
-      c->base = static_cast<uint16_t *>(ptr);
+      c->base = static_cast<uint8_t *>(ptr);
       c->owned = true;
     }
   } catch (const std::bad_alloc &) {
@@ -435,6 +493,15 @@ int hwkv_cache_free(hwkv_cache *c) {
   }
   delete c;
   return rc == HWKV_OK ? ok() : rc;
+}
+
+int hwkv_cache_format(const hwkv_cache *c, int32_t *kv_format, float *k_scale,
+                      float *v_scale) {
+  if (!c || !kv_format) return fail(HWKV_EINVAL, "null argument");
+  *kv_format = c->fmt;
+  if (k_scale) std::copy(c->k_scale.begin(), c->k_scale.end(), k_scale);
+  if (v_scale) std::copy(c->v_scale.begin(), c->v_scale.end(), v_scale);
+  return ok();
 }
 
 int hwkv_cache_seq_len(const hwkv_cache *c, int32_t layer, int32_t seq,
@@ -491,6 +558,8 @@ int hwkv_prefill_write(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0,
     wh.k_off = c->k_off[u] + seq_off;
     wh.v_off = c->v_off[u] + seq_off;
     wh.window = w;
+    wh.k_scale = c->k_scale[u];
+    wh.v_scale = c->v_scale[u];
     // slot ranges [lo, hi) written by this chunk
     std::vector<std::pair<int64_t, int64_t>> sr;
     if (w == 0) {
@@ -538,7 +607,8 @@ int hwkv_prefill_write(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0,
   a.n_sinks = p.n_sinks;
   if (max_tiles > 0) {
     const int rc = check_device(
-        hwkv::launch_prefill_write(p.head_dim, a, max_tiles, (hipStream_t)stream),
+        hwkv::launch_prefill_write(c->fmt, p.head_dim, a, max_tiles,
+                                   (hipStream_t)stream),
         "prefill_write launch");
     if (rc != HWKV_OK) return rc;
   }
@@ -550,6 +620,8 @@ int hwkv_prefill_attn(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0,
                       int64_t n_tokens, const void *q, const void *k,
                       const void *v, float scale, void *out, void *stream) {
   if (!c) return fail(HWKV_EINVAL, "cache is null");
+  if (c->fmt != HWKV_KV_BF16)
+    return fail(HWKV_EINVAL, "prefill attention needs a bf16 cache");
   const hwkv_policy &p = c->pol;
   if (layer < 0 || layer >= p.n_layers || seq < 0 || seq >= c->batch)
     return fail(HWKV_EINVAL, "layer or seq out of range");
@@ -591,7 +663,7 @@ int hwkv_prefill_attn(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0,
   const int64_t nb = (cols + per - 1) / per;
   if (nb * H > (int64_t)INT32_MAX)
     return fail(HWKV_EINVAL, "n_tokens too large for one launch");
-  a.cache = c->base;
+  a.cache = reinterpret_cast<const uint16_t *>(c->base);
   a.q = static_cast<const uint16_t *>(q);
   a.k = static_cast<const uint16_t *>(k);
   a.v = static_cast<const uint16_t *>(v);
@@ -1063,13 +1135,16 @@ int hwkv_append(hwkv_cache *c, int32_t layer, const void *k_new,
       a.v_off[j] = c->v_off[u] + seq_off;
       a.slot[j] = (int32_t)slot_of(c, u, seq_len(c, layer, b));
       a.kv_row[j] = b * H + h;
+      a.k_scale[j] = c->k_scale[u];
+      a.v_scale[j] = c->v_scale[u];
     }
     a.n_items = cnt;
     a.cache = c->base;
     a.k_new = static_cast<const uint16_t *>(k_new);
     a.v_new = static_cast<const uint16_t *>(v_new);
     const int rc = check_device(
-        hwkv::launch_append(p.head_dim, a, (hipStream_t)stream), "append launch");
+        hwkv::launch_append(c->fmt, p.head_dim, a, (hipStream_t)stream),
+        "append launch");
     if (rc != HWKV_OK) return rc;
   }
   for (int32_t b = 0; b < B; ++b) seq_len(c, layer, b) += 1;
@@ -1144,31 +1219,32 @@ int hwkv_cache_read_unit(const hwkv_cache *c, int32_t layer, int32_t kv_head,
     return fail(HWKV_EINVAL, "layer, kv_head or seq out of range");
   const int32_t u = layer * p.n_kv_heads + kv_head;
   const int64_t D = p.head_dim, cap = c->cap[u], capp = c->cap_pad[u];
+  const int64_t E = c->elem;                 // bytes per element
   const int64_t seq_off = (int64_t)seq * capp * D;
-  std::vector<uint16_t> tiles;
+  std::vector<uint8_t> tiles;
   try {
-    tiles.resize((size_t)(capp * D));
+    tiles.resize((size_t)(capp * D * E));
   } catch (const std::bad_alloc &) {
     return fail(HWKV_ENOMEM, "host allocation failed");
   }
   int rc = check_device(hipDeviceSynchronize(), "synchronize");
   if (rc != HWKV_OK) return rc;
-  rc = check_device(hipMemcpy(tiles.data(), c->base + c->k_off[u] + seq_off,
-                              (size_t)(capp * D) * 2, hipMemcpyDeviceToHost),
+  rc = check_device(hipMemcpy(tiles.data(), c->base + (c->k_off[u] + seq_off) * E,
+                              (size_t)(capp * D * E), hipMemcpyDeviceToHost),
                     "copy K");
   if (rc != HWKV_OK) return rc;
-  rc = check_device(hipMemcpy(host_v, c->base + c->v_off[u] + seq_off,
-                              (size_t)(cap * D) * 2, hipMemcpyDeviceToHost),
+  rc = check_device(hipMemcpy(host_v, c->base + (c->v_off[u] + seq_off) * E,
+                              (size_t)(cap * D * E), hipMemcpyDeviceToHost),
                     "copy V");
   if (rc != HWKV_OK) return rc;
-  // untile K: [tile][D/8][64][8] -> [slot][D]
-  uint16_t *hk = static_cast<uint16_t *>(host_k);
-  const int64_t NC = D / 8;
+  // untile K: [tile][D/8][64][8 elements] -> [slot][D]
+  uint8_t *hk = static_cast<uint8_t *>(host_k);
+  const int64_t NC = D / 8, LB = 8 * E;
   for (int64_t j = 0; j < cap; ++j) {
     const int64_t t = j / hwkv::kTile, sl = j % hwkv::kTile;
     for (int64_t g = 0; g < NC; ++g)
-      std::memcpy(hk + j * D + g * 8,
-                  tiles.data() + ((t * NC + g) * hwkv::kTile + sl) * 8, 16);
+      std::memcpy(hk + (j * D + g * 8) * E,
+                  tiles.data() + ((t * NC + g) * hwkv::kTile + sl) * LB, (size_t)LB);
   }
   *n_valid = std::min(c->n[(size_t)layer * c->batch + seq], cap);
   return ok();

@@ -1,15 +1,18 @@
 // hwkv_internal.h -- types shared by the host API and the gfx950 kernels.
 //
-// Device layout of one (unit, sequence) region, element type bf16:
+// Device layout of one (unit, sequence) region; elements are those of the
+// cache format (kv_format.h: 2 bytes for bf16 and f16, 1 byte for fp8), and
+// a chunk is 8 elements (16 or 8 bytes):
 //   K: cap_pad / 64 tiles; tile t holds slots 64t .. 64t+63 as
-//      [head_dim / 8][64 slots][8 channels]   (16-byte chunks, slot-minor)
-//      so that a wavefront with one lane per slot reads 1 KiB contiguous per
-//      channel chunk (lane-per-token q.k without LDS staging or reductions).
+//      [head_dim / 8][64 slots][8 channels]   (chunks, slot-minor)
+//      so that a wavefront with one lane per slot reads 64 chunks contiguous
+//      per channel chunk (lane-per-token q.k without LDS staging or
+//      reductions).
 //   V: [cap_pad][head_dim] row-major, so that lanes owning channel slices
 //      read whole rows contiguously for the p * v accumulation.
 // cap_pad = cap rounded up to a multiple of 64.  Regions are grouped by
 // window level: for each level, the K regions of its units ([unit][seq]),
-// then their V regions.
+// then their V regions.  Offsets below count elements.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -31,6 +34,8 @@ struct DecodeItems {
   int32_t new_slot[kMaxItems];   // slot taking the appended token, or -1
   int32_t q_row[kMaxItems];      // b * n_q_heads + h * G (first q head)
   int32_t kv_row[kMaxItems];     // b * n_kv_heads + h (row of k_new/v_new)
+  float k_scale[kMaxItems];      // fp8 scales of the item's unit (else 1)
+  float v_scale[kMaxItems];
   int32_t split_begin[kMaxItems + 1];
   int32_t n_items;
   int32_t ws_split0;             // first partial slot of this launch in ws
@@ -38,7 +43,7 @@ struct DecodeItems {
 
 struct DecodeArgs {
   DecodeItems it;
-  uint16_t *cache;               // cache base (bf16)
+  void *cache;                   // cache base
   const uint16_t *q;             // [B][Hq][D]
   const uint16_t *k_new;         // [B][Hkv][D] or null
   const uint16_t *v_new;
@@ -55,11 +60,12 @@ struct WriteHead {
   int64_t window;                // 0 = full
   int32_t tile0[3];
   int32_t n_tiles[3];
+  float k_scale, v_scale;        // fp8 scales of the unit (else 1)
 };
 
 struct WriteArgs {
   WriteHead head[kMaxItems];     // one per kv head of the layer
-  uint16_t *cache;
+  void *cache;
   const uint16_t *k;             // [n_tokens][Hkv][D]
   const uint16_t *v;
   int64_t p0, p1;                // chunk [p0, p1)
@@ -72,8 +78,10 @@ struct AppendArgs {
   int64_t v_off[kMaxItems];
   int32_t slot[kMaxItems];
   int32_t kv_row[kMaxItems];
+  float k_scale[kMaxItems];
+  float v_scale[kMaxItems];
   int32_t n_items;
-  uint16_t *cache;
+  void *cache;
   const uint16_t *k_new;
   const uint16_t *v_new;
 };
@@ -92,7 +100,7 @@ struct PrefillAttnHead {
 struct PrefillAttnArgs {
   PrefillAttnHead head[kMaxItems];
   int32_t head_order[kMaxItems];
-  const uint16_t *cache;
+  const uint16_t *cache;         // bf16 caches only
   const uint16_t *q;             // [n_tokens][Hq][D]
   const uint16_t *k;             // [n_tokens][Hkv][D]
   const uint16_t *v;
@@ -117,16 +125,19 @@ struct PrefillAttnArgs {
 constexpr int kPrefillWaves = HWKV_PREFILL_WAVES;
 
 // Launchers (return the launch status).  D in {64, 128, 256}; G in
-// {1, 2, 4, 6, 8}.
-hipError_t launch_decode_split(int D, int G, const DecodeArgs &a, int n_splits,
-                               hipStream_t s);
+// {1, 2, 4, 6, 8}; fmt one of the HWKV_KV_* formats.
+hipError_t launch_decode_split(int fmt, int D, int G, const DecodeArgs &a,
+                               int n_splits, hipStream_t s);
+template <int F>
+hipError_t launch_decode_split_fmt(int D, int G, const DecodeArgs &a,
+                                   int n_splits, hipStream_t s);
 hipError_t launch_decode_combine(int D, int G, const DecodeArgs &a,
                                  int n_combine_blocks, hipStream_t s);
 int decode_split_tokens();       // tokens per split (a multiple of 64)
 int decode_combine_blocks_per_item(int D, int G);  // merge workgroups
-hipError_t launch_prefill_write(int D, const WriteArgs &a, int max_tiles,
-                                hipStream_t s);
-hipError_t launch_append(int D, const AppendArgs &a, hipStream_t s);
+hipError_t launch_prefill_write(int fmt, int D, const WriteArgs &a,
+                                int max_tiles, hipStream_t s);
+hipError_t launch_append(int fmt, int D, const AppendArgs &a, hipStream_t s);
 int prefill_attn_columns_per_block();   // (token, q head) columns
 hipError_t launch_prefill_attn(int D, const PrefillAttnArgs &a, hipStream_t s,
                               int n_splits = 1);

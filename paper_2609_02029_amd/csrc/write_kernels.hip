@@ -1,6 +1,7 @@
 // write_kernels.hip -- prefill materialisation and ring-buffer append into
-// the per-head grouped cache (gfx950).  Pure 16-byte copies; the only
-// arithmetic is the slot <-> position map.
+// the per-head grouped cache (gfx950).  Chunk copies of 8 elements, stored in
+// the cache format (kv_format.h); the only other arithmetic is the
+// slot <-> position map.
 //
 // Retained set of a finite unit at length n: {p < S} U {p >= n - w} (the
 // paper's J_t(w) window plus an additive sink prefix); slot(p) = p for full
@@ -9,17 +10,20 @@
 // p in [p1 - w, p1) with p = j (mod w), namely p = b + ((j - b) mod w) with
 // b = p1 - w, provided p >= S; the chunk writes slot j iff that p lies in
 // [p0, p1).  Iterating over destination slots makes every K tile write a
-// full, coalesced 16-byte-per-lane store and never touches slots the chunk
+// full, coalesced chunk-per-lane store and never touches slots the chunk
 // does not own, so prefill never forms a full-length cache.
 #include "hwkv_internal.h"
+#include "kv_format.h"
 
 namespace hwkv {
 namespace {
 
 // One workgroup per (destination tile, kv head): 64 slots x D channels.
-template <int D>
+template <int D, int F>
 __global__ __launch_bounds__(256) void prefill_write(WriteArgs a) {
   constexpr int NC = D / 8;
+  constexpr int EB = KvFormat<F>::kBytes;
+  constexpr int LB = 8 * EB;
   __shared__ int64_t src_row[kTile];  // source row of each slot, or -1
   const int h = blockIdx.y;
   const WriteHead &wh = a.head[h];
@@ -53,8 +57,9 @@ __global__ __launch_bounds__(256) void prefill_write(WriteArgs a) {
   }
   __syncthreads();
 
-  uint16_t *kt = a.cache + wh.k_off + (size_t)tile * kTile * D;
-  uint16_t *vt = a.cache + wh.v_off + (size_t)tile * kTile * D;
+  uint8_t *const cache = static_cast<uint8_t *>(a.cache);
+  uint8_t *kt = cache + (wh.k_off + (size_t)tile * kTile * D) * EB;
+  uint8_t *vt = cache + (wh.v_off + (size_t)tile * kTile * D) * EB;
   const size_t row_stride = (size_t)a.n_kv_heads * D;
   // K: thread -> (chunk g, slot), slot fastest: coalesced tile stores
   for (int e = threadIdx.x; e < kTile * NC; e += 256) {
@@ -63,7 +68,7 @@ __global__ __launch_bounds__(256) void prefill_write(WriteArgs a) {
     if (r < 0) continue;
     const uint4 val =
         *reinterpret_cast<const uint4 *>(a.k + r * row_stride + h * D + g * 8);
-    *reinterpret_cast<uint4 *>(kt + ((size_t)g * kTile + sl) * 8) = val;
+    store_chunk<F>(kt + ((size_t)g * kTile + sl) * LB, encode8<F>(val, wh.k_scale));
   }
   // V: thread -> (slot, chunk g), chunk fastest: row-contiguous both sides
   for (int e = threadIdx.x; e < kTile * NC; e += 256) {
@@ -72,54 +77,80 @@ __global__ __launch_bounds__(256) void prefill_write(WriteArgs a) {
     if (r < 0) continue;
     const uint4 val =
         *reinterpret_cast<const uint4 *>(a.v + r * row_stride + h * D + g * 8);
-    *reinterpret_cast<uint4 *>(vt + (size_t)sl * D + g * 8) = val;
+    store_chunk<F>(vt + (size_t)sl * D * EB + g * LB, encode8<F>(val, wh.v_scale));
   }
 }
 
 // One workgroup of 64 lanes per (sequence, kv head): lanes [0, NC) copy K
 // chunks into the tile layout, lanes [NC, 2 NC) copy the V row.
-template <int D>
+template <int D, int F>
 __global__ __launch_bounds__(64) void append_token(AppendArgs a) {
   constexpr int NC = D / 8;
+  constexpr int EB = KvFormat<F>::kBytes;
+  constexpr int LB = 8 * EB;
   const int i = blockIdx.x;
   const int t = threadIdx.x;
   const int slot = a.slot[i];
   const size_t src = (size_t)a.kv_row[i] * D;
+  uint8_t *const cache = static_cast<uint8_t *>(a.cache);
   if (t < NC) {
-    uint16_t *kt = a.cache + a.k_off[i] + (size_t)(slot / kTile) * kTile * D;
+    uint8_t *kt = cache + (a.k_off[i] + (size_t)(slot / kTile) * kTile * D) * EB;
     const uint4 val = *reinterpret_cast<const uint4 *>(a.k_new + src + t * 8);
-    *reinterpret_cast<uint4 *>(kt + ((size_t)t * kTile + slot % kTile) * 8) =
-        val;
+    store_chunk<F>(kt + ((size_t)t * kTile + slot % kTile) * LB,
+                   encode8<F>(val, a.k_scale[i]));
   } else if (t < 2 * NC) {
     const int g = t - NC;
     const uint4 val = *reinterpret_cast<const uint4 *>(a.v_new + src + g * 8);
-    *reinterpret_cast<uint4 *>(a.cache + a.v_off[i] + (size_t)slot * D +
-                               g * 8) = val;
+    store_chunk<F>(cache + (a.v_off[i] + (size_t)slot * D) * EB + g * LB,
+                   encode8<F>(val, a.v_scale[i]));
   }
 }
+
+// Calls L<D, F>::run(args...) for the runtime (D, format).
+template <template <int, int> class L, typename... Args>
+hipError_t dispatch_df(int fmt, int D, Args &&...args) {
+#define HWKV_F(DD)                                                        \
+  switch (fmt) {                                                          \
+    case HWKV_KV_BF16: return L<DD, HWKV_KV_BF16>::run(args...);          \
+    case HWKV_KV_F16: return L<DD, HWKV_KV_F16>::run(args...);            \
+    case HWKV_KV_FP8_E4M3: return L<DD, HWKV_KV_FP8_E4M3>::run(args...);  \
+    default: return hipErrorInvalidValue;                                 \
+  }
+  switch (D) {
+    case 64: HWKV_F(64)
+    case 128: HWKV_F(128)
+    case 256: HWKV_F(256)
+    default: return hipErrorInvalidValue;
+  }
+#undef HWKV_F
+}
+
+template <int D, int F>
+struct WriteLaunch {
+  static hipError_t run(const WriteArgs &a, int max_tiles, hipStream_t s) {
+    hipLaunchKernelGGL((prefill_write<D, F>), dim3(max_tiles, a.n_kv_heads),
+                       dim3(256), 0, s, a);
+    return hipGetLastError();
+  }
+};
+
+template <int D, int F>
+struct AppendLaunch {
+  static hipError_t run(const AppendArgs &a, hipStream_t s) {
+    hipLaunchKernelGGL((append_token<D, F>), dim3(a.n_items), dim3(64), 0, s, a);
+    return hipGetLastError();
+  }
+};
 
 }  // namespace
 
-hipError_t launch_prefill_write(int D, const WriteArgs &a, int max_tiles,
-                                hipStream_t s) {
-  const dim3 grid(max_tiles, a.n_kv_heads);
-  switch (D) {
-    case 64: hipLaunchKernelGGL(prefill_write<64>, grid, dim3(256), 0, s, a); break;
-    case 128: hipLaunchKernelGGL(prefill_write<128>, grid, dim3(256), 0, s, a); break;
-    case 256: hipLaunchKernelGGL(prefill_write<256>, grid, dim3(256), 0, s, a); break;
-    default: return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
+hipError_t launch_prefill_write(int fmt, int D, const WriteArgs &a,
+                                int max_tiles, hipStream_t s) {
+  return dispatch_df<WriteLaunch>(fmt, D, a, max_tiles, s);
 }
 
-hipError_t launch_append(int D, const AppendArgs &a, hipStream_t s) {
-  switch (D) {
-    case 64: hipLaunchKernelGGL(append_token<64>, dim3(a.n_items), dim3(64), 0, s, a); break;
-    case 128: hipLaunchKernelGGL(append_token<128>, dim3(a.n_items), dim3(64), 0, s, a); break;
-    case 256: hipLaunchKernelGGL(append_token<256>, dim3(a.n_items), dim3(64), 0, s, a); break;
-    default: return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
+hipError_t launch_append(int fmt, int D, const AppendArgs &a, hipStream_t s) {
+  return dispatch_df<AppendLaunch>(fmt, D, a, s);
 }
 
 }  // namespace hwkv

@@ -13,6 +13,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "_lib", "libhwkv.so")
 
 OK, EINVAL, ENOMEM, ECAPACITY, ESTATE, EDEVICE = 0, 1, 2, 3, 4, 5
+# cache formats (HWKV_KV_*): name -> (code, bytes per element)
+KV_FORMATS = {"bf16": (0, 2), "f16": (1, 2), "fp8": (2, 1)}
 _NAMES = {EINVAL: "EINVAL", ENOMEM: "ENOMEM", ECAPACITY: "ECAPACITY",
           ESTATE: "ESTATE", EDEVICE: "EDEVICE"}
 
@@ -38,6 +40,11 @@ SYMBOLS = {
     "hwkv_policy_free": ([_vp], ctypes.c_int),
     "hwkv_policy_bytes": ([_vp, _i64, _P(_dbl)], ctypes.c_int),
     "hwkv_policy_rate": ([_vp, _i64, _P(_dbl)], ctypes.c_int),
+    "hwkv_policy_bytes_format": ([_vp, _i64, _i32, _P(_dbl)], ctypes.c_int),
+    "hwkv_cache_bytes_format": ([_vp, _i32, _i64, _i32, _P(_sz)], ctypes.c_int),
+    "hwkv_cache_alloc_format": ([_P(_vp), _vp, _i32, _i64, _i32, _vp, _vp, _vp, _sz],
+                                ctypes.c_int),
+    "hwkv_cache_format": ([_vp, _P(_i32), _vp, _vp], ctypes.c_int),
     "hwkv_cache_bytes": ([_vp, _i32, _i64, _P(_sz)], ctypes.c_int),
     "hwkv_cache_alloc": ([_P(_vp), _vp, _i32, _i64, _vp, _sz], ctypes.c_int),
     "hwkv_cache_free": ([_vp], ctypes.c_int),
@@ -165,9 +172,16 @@ def policy_free(policy):
         policy.handle = None
 
 
-def policy_bytes(policy, ctx):
+def _fmt_code(kv_format):
+    if kv_format not in KV_FORMATS:
+        raise ValueError(f"kv_format must be one of {sorted(KV_FORMATS)}")
+    return KV_FORMATS[kv_format][0]
+
+
+def policy_bytes(policy, ctx, kv_format="bf16"):
     r = _dbl()
-    _check(_lib.hwkv_policy_bytes(policy.handle, ctx, ctypes.byref(r)))
+    _check(_lib.hwkv_policy_bytes_format(policy.handle, ctx, _fmt_code(kv_format),
+                                         ctypes.byref(r)))
     return r.value
 
 
@@ -180,24 +194,57 @@ def policy_rate(policy, ctx):
 # ---------------------------------------------------------------------------
 # cache
 # ---------------------------------------------------------------------------
-def cache_bytes(policy, batch, max_ctx):
+def cache_bytes(policy, batch, max_ctx, kv_format="bf16"):
     r = _sz()
-    _check(_lib.hwkv_cache_bytes(policy.handle, batch, max_ctx, ctypes.byref(r)))
+    _check(_lib.hwkv_cache_bytes_format(policy.handle, batch, max_ctx, _fmt_code(kv_format),
+                                        ctypes.byref(r)))
     return r.value
 
 
-def cache_alloc(policy, batch, max_ctx, dev_buf=None):
-    """``dev_buf``: optional uint8 device tensor to adopt (kept alive)."""
+def _scales(policy, x):
+    """Host fp32 [n_layers][n_kv_heads] scales (array-like or scalar) or None."""
+    if x is None:
+        return None
+    import numpy as np
+    a = np.ascontiguousarray(np.broadcast_to(np.asarray(x, dtype=np.float32),
+                                             (policy.n_layers, policy.n_kv_heads)))
+    return a
+
+
+def cache_alloc(policy, batch, max_ctx, dev_buf=None, kv_format="bf16", k_scale=None,
+                v_scale=None):
+    """``dev_buf``: optional uint8 device tensor to adopt (kept alive).
+    ``kv_format``: "bf16", "f16" or "fp8"; ``k_scale``/``v_scale``: fp8 scales,
+    a scalar or ``[n_layers, n_kv_heads]`` (None = 1.0)."""
     h = _vp()
     ptr = None
     nbytes = 0
     if dev_buf is not None:
         ptr = _dev(dev_buf, "uint8", "dev_buf")
         nbytes = dev_buf.numel()
-    _check(_lib.hwkv_cache_alloc(ctypes.byref(h), policy.handle, batch, max_ctx, ptr, nbytes))
+    ks = _scales(policy, k_scale)
+    vs = _scales(policy, v_scale)
+    _check(_lib.hwkv_cache_alloc_format(
+        ctypes.byref(h), policy.handle, batch, max_ctx, _fmt_code(kv_format),
+        None if ks is None else ks.ctypes.data_as(_vp),
+        None if vs is None else vs.ctypes.data_as(_vp), ptr, nbytes))
     c = Cache(h, policy.n_layers, policy.n_kv_heads, policy.n_q_heads, policy.head_dim, batch)
     c.dev_buf = dev_buf
+    c.kv_format = kv_format
     return c
+
+
+def cache_format(cache):
+    """Returns (kv_format name, k_scale, v_scale): scales as numpy fp32
+    ``[n_layers, n_kv_heads]``."""
+    import numpy as np
+    code = _i32()
+    ks = np.empty((cache.n_layers, cache.n_kv_heads), dtype=np.float32)
+    vs = np.empty_like(ks)
+    _check(_lib.hwkv_cache_format(cache.handle, ctypes.byref(code), ks.ctypes.data_as(_vp),
+                                  vs.ctypes.data_as(_vp)))
+    name = [k for k, (c, _) in KV_FORMATS.items() if c == code.value][0]
+    return name, ks, vs
 
 
 def cache_free(cache):
@@ -218,11 +265,13 @@ def cache_unit_info(cache, layer, kv_head):
 
 
 def cache_read_unit(cache, layer, kv_head, seq):
-    """Returns (k, v, n_valid): numpy uint16 [capacity, head_dim] bf16 bits."""
+    """Returns (k, v, n_valid): numpy [capacity, head_dim] stored elements --
+    uint16 bit patterns (bf16, f16) or uint8 E4M3 codes (fp8)."""
     import numpy as np
     cap, _ = cache_unit_info(cache, layer, kv_head)
-    k = np.empty((cap, cache.head_dim), dtype=np.uint16)
-    v = np.empty((cap, cache.head_dim), dtype=np.uint16)
+    dt = np.uint8 if getattr(cache, "kv_format", "bf16") == "fp8" else np.uint16
+    k = np.empty((cap, cache.head_dim), dtype=dt)
+    v = np.empty((cap, cache.head_dim), dtype=dt)
     nv = _i64()
     _check(_lib.hwkv_cache_read_unit(cache.handle, layer, kv_head, seq,
                                      k.ctypes.data_as(_vp), v.ctypes.data_as(_vp),

@@ -121,20 +121,25 @@ def traffic(db_fetch, db_write, mib):
     return scale_f, scale_w, per
 
 
-SOURCES = {"decode_split<": "decode_kernels.hip",
-           "prefill_attn<": "prefill_attn_kernels.hip"}
+# source files of each profiled kernel (the split kernel's template and the
+# format helpers it inlines)
+SOURCES = {"decode_split<": ["decode_split.h", "kv_format.h"],
+           "prefill_attn<": ["prefill_attn_kernels.hip"]}
 
 
-def kernel_source_hash(kernel="decode_split<256, 6>"):
-    """Hash of a kernel's source file: a traffic record is current only while
+def kernel_source_hash(kernel="decode_split<256, 6, 0>"):
+    """Hash of a kernel's source files: a traffic record is current only while
     the kernel it was measured on is unchanged."""
-    src = next(f for k, f in SOURCES.items() if kernel.startswith(k))
-    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc", src)
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    files = next(f for k, f in SOURCES.items() if kernel.startswith(k))
+    h = hashlib.sha256()
+    for src in files:
+        path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc", src)
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
-def traffic_record(db_fetch, db_write, mib, kernel="decode_split<256, 6>"):
+def traffic_record(db_fetch, db_write, mib, kernel="decode_split<256, 6, 0>"):
     sf, sw, per = traffic(db_fetch, db_write, mib)
     fv, fn = per["fetch"][kernel]
     wv, _ = per["write"].get(kernel, (0.0, 0))

@@ -15,6 +15,7 @@ import torch
 
 import oracle
 import workloads as W
+from oracle import kvformat as KF
 from paper_2609_02029_amd import hwkv
 
 REL_TOL = 1e-2     # the bar: max over rows of |o - ref|_inf / |ref|_inf
@@ -51,8 +52,9 @@ class Run:
     (large workloads) instead of on the host."""
 
     def __init__(self, cfg, dev="cuda:0", fused=True, track=None, device_gen=False,
-                 levels=None, prompts=None):
+                 levels=None, prompts=None, kv_format="bf16", k_scale=None, v_scale=None):
         self.cfg = cfg
+        self.kv_format = kv_format
         self.dev = torch.device(dev)
         self.fused = fused
         self.device_gen = device_gen
@@ -70,7 +72,10 @@ class Run:
         self.track = set(range(self.L)) if track is None else set(track)
         self.pol = hwkv.policy_set(self.L, self.Hkv, self.Hq, self.D, self.S,
                                    c["level_windows"], self.levels)
-        self.cache = hwkv.cache_alloc(self.pol, self.B, self.max_ctx)
+        self.cache = hwkv.cache_alloc(self.pol, self.B, self.max_ctx, kv_format=kv_format,
+                                      k_scale=k_scale, v_scale=v_scale)
+        # per-unit fp8 scales as the library holds them (1.0 otherwise)
+        _, self.k_scale, self.v_scale = hwkv.cache_format(self.cache)
         self.ws = torch.zeros(hwkv.decode_workspace_bytes(self.cache), dtype=torch.uint8,
                               device=self.dev)
         # host histories [layer][b] -> uint16 [max_ctx, Hkv, D]
@@ -216,8 +221,34 @@ class Run:
                                        scale_channels=sc, scale=s)[b]
         return hk, hv
 
+    def stored(self, layer, hk, hv):
+        """Stored elements (the oracle's encoding) of host histories [n, Hkv, D]
+        in the cache format, with each KV head's scales."""
+        if self.kv_format == "bf16":
+            return hk, hv
+        sk = np.stack([KF.store(hk[:, h], self.kv_format, self.k_scale[layer, h])
+                       for h in range(self.Hkv)], axis=1)
+        sv = np.stack([KF.store(hv[:, h], self.kv_format, self.v_scale[layer, h])
+                       for h in range(self.Hkv)], axis=1)
+        return sk, sv
+
+    def stored_values(self, layer, hk, hv):
+        """fp64 values of the stored elements of host histories."""
+        sk, sv = self.stored(layer, hk, hv)
+        kv = np.stack([KF.values(sk[:, h], self.kv_format, self.k_scale[layer, h])
+                       for h in range(self.Hkv)], axis=1)
+        vv = np.stack([KF.values(sv[:, h], self.kv_format, self.v_scale[layer, h])
+                       for h in range(self.Hkv)], axis=1)
+        return kv, vv
+
     def oracle_out(self, layer, qa, n_threads=8):
         t = self.n[layer] - 1
+        if self.kv_format != "bf16":
+            kvs = [self.stored_values(layer, self.kh[layer][b][: t[b] + 1],
+                                      self.vh[layer][b][: t[b] + 1]) for b in range(self.B)]
+            return KF.attend_values(KF.bf16_values(qa), [x[0] for x in kvs],
+                                    [x[1] for x in kvs], t, self.S, self.windows[layer],
+                                    self.scale)
         return oracle.decode_layer(qa, [self.kh[layer][b][: t[b] + 1] for b in range(self.B)],
                                    [self.vh[layer][b][: t[b] + 1] for b in range(self.B)], t,
                                    self.S, self.windows[layer], self.scale, n_threads=n_threads)
@@ -243,8 +274,9 @@ class Run:
         occ = tab.table[:nv]
         assert np.all(occ >= 0)
         hk, hv = (self.kh[layer][b], self.vh[layer][b]) if hist is None else hist
-        assert np.array_equal(k[:nv], hk[occ, h]), f"K residency differs: layer {layer} head {h} seq {b}"
-        assert np.array_equal(v[:nv], hv[occ, h]), f"V residency differs: layer {layer} head {h} seq {b}"
+        ek, ev = self.stored(layer, hk[occ], hv[occ])
+        assert np.array_equal(k[:nv], ek[:, h]), f"K residency differs: layer {layer} head {h} seq {b}"
+        assert np.array_equal(v[:nv], ev[:, h]), f"V residency differs: layer {layer} head {h} seq {b}"
 
     def check_layer(self, layer, hist=None):
         for b in range(self.B):

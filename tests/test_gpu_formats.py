@@ -1,0 +1,178 @@
+"""GPU parity of the cache formats p_KV (binary16 and fp8-E4M3 storage).
+
+The write paths (prefill materialisation, the standalone append and the
+fused append) must store exactly the oracle's encoding of every input
+element: bit-exact, including rounding ties, subnormals, saturation and NaN.
+Decode attention must match the fp64 oracle evaluated over the stored values
+(the format changes numerical execution, so the reference uses it too) within
+max relative error 1e-2 per output row, and within 2e-4 (fp32 accumulation).
+"""
+import numpy as np
+import pytest
+import torch
+
+from hwkv_harness import Run, log, up
+from oracle import kvformat as KF
+from paper_2609_02029_amd import hwkv
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.set_device(0)
+
+
+def mini(**kw):
+    c = dict(name="mini", seed=31, n_layers=1, batch=1, n_q_heads=8, n_kv_heads=2,
+             head_dim=64, n_sinks=4, level_windows=[256, 0], levels=[[0, 1]],
+             prompt=[300], steps=4, max_ctx=400)
+    c.update(kw)
+    return c
+
+
+# fp8 scales per (layer, kv head): distinct, not powers of two, sized so that
+# the synthetic keys and values (unit normal, outlier channels up to ~8x) use
+# the whole E4M3 range and the outliers saturate
+def fp8_scales(L, H, base):
+    return (base * (1.0 + 0.37 * np.arange(L * H))).reshape(L, H).astype(np.float32)
+
+
+FORMATS = [("f16", None, None), ("fp8", 0.013, 0.009), ("fp8", 1.0, 1.0)]
+
+
+def fmt_args(fmt, ks, vs, L, H):
+    if fmt != "fp8":
+        return dict(kv_format=fmt)
+    return dict(kv_format=fmt, k_scale=fp8_scales(L, H, ks), v_scale=fp8_scales(L, H, vs))
+
+
+def _stored_equal(fmt, got, inputs_bf16, scale):
+    exp = KF.store(inputs_bf16, fmt, scale)
+    if fmt == "f16":
+        # NaN inputs: any binary16 NaN (payloads are not part of the format)
+        nan_in = np.isnan(KF.bf16_values(inputs_bf16))
+        nan_out = ((got & 0x7C00) == 0x7C00) & ((got & 0x03FF) != 0)
+        assert np.all(nan_out[nan_in]), "NaN input not stored as NaN"
+        return np.array_equal(got[~nan_in], exp[~nan_in])
+    return np.array_equal(got, exp)
+
+
+# ---------------------------------------------------------------------------
+# every bf16 bit pattern through prefill materialisation
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("fmt,scale", [("f16", 1.0), ("fp8", 1.0), ("fp8", 0.0123),
+                                       ("fp8", 1.7e-3), ("fp8", 300.0)])
+def test_every_bf16_pattern_is_stored_exactly(fmt, scale):
+    log(f"exhaustive {fmt} scale={scale}")
+    D, P = 256, 256
+    pol = hwkv.policy_set(1, 1, 1, D, 0, [0], [[0]])
+    kw = dict(kv_format=fmt)
+    if fmt == "fp8":
+        kw.update(k_scale=scale, v_scale=scale * 0.5)
+    cache = hwkv.cache_alloc(pol, 1, 512, **kw)
+    allb = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    kin = allb.reshape(P, 1, D)
+    vin = allb[::-1].copy().reshape(P, 1, D)
+    dev = torch.device("cuda:0")
+    for p0, p1 in ((0, 100), (100, 101), (101, 256)):       # three chunks, ragged tiles
+        hwkv.prefill_write(cache, 0, 0, p0, up(kin[p0:p1], dev), up(vin[p0:p1], dev))
+    k, v, nv = hwkv.cache_read_unit(cache, 0, 0, 0)
+    assert nv == P
+    ks = scale
+    vs = np.float32(scale * 0.5) if fmt == "fp8" else 1.0
+    assert _stored_equal(fmt, k[:P].ravel(), kin.ravel(), ks), "K codes differ"
+    assert _stored_equal(fmt, v[:P].ravel(), vin.ravel(), vs), "V codes differ"
+    cache.free()
+
+
+# ---------------------------------------------------------------------------
+# workloads: residency after prefill and after every append (standalone and
+# fused), every output of every step
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("fmt,ks,vs", FORMATS)
+def test_format_workload(fmt, ks, vs):
+    cfg = mini(n_layers=2, levels=[[0, 1], [1, 0]], prompt=[700], max_ctx=800)
+    log(f"workload {fmt} {ks} {vs}")
+    r = Run(cfg, **fmt_args(fmt, ks, vs, 2, 2))
+    worst = 0.0
+    for l in range(2):
+        r.prefill(l, 0, chunks=[63, 300])
+        r.check_layer(l)
+    for st in range(6):
+        for l in range(2):
+            qa, out = r.step(l, fused=bool((st + l) % 2))
+            worst = max(worst, r.check_out(l, qa, out, f"{fmt} layer {l} step {st}"))
+            r.check_layer(l)
+    log(f"{fmt}: max rel err {worst:.3e}")
+    r.free()
+
+
+EDGES = [(0, 1, 1), (3, 5, 7), (3, 5, 9), (4, 60, 64), (4, 60, 65), (4, 508, 513),
+         (2, 1, 700), (0, 600, 1025)]
+
+
+@pytest.mark.parametrize("fmt,ks,vs", FORMATS[:2])
+@pytest.mark.parametrize("S,w,P", EDGES)
+def test_format_edge_lengths(fmt, ks, vs, S, w, P):
+    log(f"edge {fmt} S={S} w={w} P={P}")
+    cfg = mini(n_sinks=S, level_windows=[w, 0], prompt=[P], max_ctx=P + 8)
+    r = Run(cfg, **fmt_args(fmt, ks, vs, 1, 2))
+    r.prefill(0, 0)
+    r.check_layer(0)
+    for st in range(4):
+        qa, out = r.step(0, fused=bool(st % 2))
+        r.check_out(0, qa, out, f"{fmt} S={S} w={w} P={P} step {st}")
+        r.check_layer(0)
+    r.free()
+
+
+@pytest.mark.parametrize("fmt,ks,vs", FORMATS[:2])
+@pytest.mark.parametrize("D,G", [(64, 1), (64, 8), (128, 2), (128, 4), (256, 6), (256, 8)])
+def test_format_head_dims_and_groups(fmt, ks, vs, D, G):
+    log(f"dims {fmt} D={D} G={G}")
+    cfg = mini(head_dim=D, n_kv_heads=2, n_q_heads=2 * G, level_windows=[700, 0],
+               prompt=[1500], max_ctx=1600, seed=32)
+    r = Run(cfg, **fmt_args(fmt, ks, vs, 1, 2))
+    r.prefill(0, 0)
+    for st in range(2):
+        qa, out = r.step(0, fused=bool(st))
+        r.check_out(0, qa, out, f"{fmt} D={D} G={G} step {st}")
+    r.check_layer(0)
+    r.free()
+
+
+@pytest.mark.parametrize("fmt,ks,vs", FORMATS[:2])
+def test_format_batched_ragged(fmt, ks, vs):
+    cfg = mini(batch=5, head_dim=256, n_kv_heads=4, n_q_heads=24,
+               level_windows=[100, 600, 2000, 0], levels=[[0, 1, 2, 3], [3, 2, 0, 0]],
+               n_layers=2, prompt=[1, 63, 700, 1500, 2049], max_ctx=2100, seed=33)
+    log(f"ragged {fmt}")
+    r = Run(cfg, **fmt_args(fmt, ks, vs, 2, 4))
+    for l in range(2):
+        for b in range(5):
+            r.prefill(l, b)
+        r.check_layer(l)
+    for st in range(3):
+        for l in range(2):
+            qa, out = r.step(l, fused=bool((st + l) % 2))
+            r.check_out(l, qa, out, f"{fmt} layer {l} step {st}")
+    for l in range(2):
+        r.check_layer(l)
+    r.free()
+
+
+def test_fp8_cache_rejects_prefill_attention():
+    pol = hwkv.policy_set(1, 2, 8, 64, 4, [256, 0], [[0, 1]])
+    cache = hwkv.cache_alloc(pol, 1, 400, kv_format="fp8")
+    dev = torch.device("cuda:0")
+    q = torch.zeros((4, 8, 64), dtype=torch.bfloat16, device=dev)
+    kv = torch.zeros((4, 2, 64), dtype=torch.bfloat16, device=dev)
+    out = torch.zeros((4, 8, 64), dtype=torch.float32, device=dev)
+    with pytest.raises(hwkv.HwkvError) as e:
+        hwkv.prefill_attn(cache, 0, 0, 0, q, kv, kv, 0.125, out)
+    assert e.value.code == hwkv.EINVAL
+    assert hwkv.cache_seq_len(cache, 0, 0) == 0
+    cache.free()

@@ -386,3 +386,90 @@ def test_policy_artifact_rejects_malformed_text(hw, golden):
     assert hw._lib.hwkv_policy_serialize(p.handle, b"x", 1, 0, ctypes.c_double(0.5),
                                          ctypes.c_double(0.5), ctypes.c_double(1.0), small,
                                          n.value, ctypes.byref(n)) == hw.ENOMEM
+
+
+# --------------------------------------------------------------------------
+# cache formats
+# --------------------------------------------------------------------------
+def test_format_accounting_matches_oracle(hw):
+    r = np.random.default_rng(3)
+    for _ in range(30):
+        L, H, D = int(r.integers(1, 4)), int(r.choice([1, 2, 4])), int(r.choice([64, 128, 256]))
+        lw = [int(x) for x in r.integers(1, 3000, size=3)] + [0]
+        lv = r.integers(0, 4, size=(L, H))
+        S = int(r.integers(0, 8))
+        ctx = int(r.integers(1, 5000))
+        B = int(r.integers(1, 4))
+        p = hw.policy_set(L, H, H, D, S, lw, lv.tolist())
+        wins = np.array(lw)[lv].ravel()
+        for fmt, b in (("bf16", 2.0), ("f16", 2.0), ("fp8", 1.0)):
+            assert hw.policy_bytes(p, ctx, fmt) == pytest.approx(
+                oracle.policy_bytes(ctx, S, wins, D, D, b, b), rel=1e-14)
+        # fp8 elements are one byte: exactly half the 16-bit layouts
+        b16 = hw.cache_bytes(p, B, ctx)
+        assert hw.cache_bytes(p, B, ctx, "f16") == b16
+        assert 2 * hw.cache_bytes(p, B, ctx, "fp8") == b16
+
+
+def test_format_context_limit(hw):
+    # one unit's K or V must stay below 2^31 bytes: twice the tokens at 1 byte
+    p = _pol(hw)
+    n = (1 << 24) + 1                     # head_dim 64: over the limit at 2 bytes
+    with pytest.raises(hw.HwkvError):
+        hw.cache_bytes(p, 1, n, "bf16")
+    assert hw.cache_bytes(p, 1, n, "fp8") > 0
+    with pytest.raises(hw.HwkvError):
+        hw.cache_bytes(p, 1, (1 << 25) + 1, "fp8")
+
+
+def _alloc_fmt(hw, p, fmt, ks=None, vs=None, B=1, max_ctx=300):
+    h = ctypes.c_void_p()
+    nbytes = hw.cache_bytes(p, B, max_ctx, "bf16")
+    arr = lambda x: None if x is None else np.ascontiguousarray(x, dtype=np.float32)
+    ka, va = arr(ks), arr(vs)
+    rc = hw._lib.hwkv_cache_alloc_format(
+        ctypes.byref(h), p.handle, B, max_ctx, fmt,
+        None if ka is None else ka.ctypes.data_as(ctypes.c_void_p),
+        None if va is None else va.ctypes.data_as(ctypes.c_void_p), FAKE, nbytes)
+    return rc, h
+
+
+def test_format_alloc_validation(hw):
+    p = _pol(hw)                          # 2 layers x 2 kv heads
+    good = np.full((2, 2), 0.05)
+    # unknown formats
+    for fmt in (-1, 3, 99):
+        rc, h = _alloc_fmt(hw, p, fmt)
+        assert rc == hw.EINVAL and not h.value
+        b = ctypes.c_size_t()
+        assert hw._lib.hwkv_cache_bytes_format(p.handle, 1, 300, fmt, ctypes.byref(b)) == hw.EINVAL
+        d = ctypes.c_double()
+        assert hw._lib.hwkv_policy_bytes_format(p.handle, 300, fmt, ctypes.byref(d)) == hw.EINVAL
+    with pytest.raises(ValueError):       # the binding names the formats
+        hw.cache_bytes(p, 1, 300, "fp4")
+    # scales belong to fp8 only
+    for fmt in (0, 1):
+        rc, h = _alloc_fmt(hw, p, fmt, ks=good)
+        assert rc == hw.EINVAL and not h.value
+    # each scale positive, finite, normal
+    for bad in (0.0, -1.0, float("inf"), float("nan"), 1e-40):
+        ks = good.copy()
+        ks[1, 0] = bad
+        rc, h = _alloc_fmt(hw, p, 2, ks=ks)
+        assert rc == hw.EINVAL and not h.value, bad
+        rc, h = _alloc_fmt(hw, p, 2, vs=ks)
+        assert rc == hw.EINVAL and not h.value, bad
+    # accepted, and reported back
+    ks = np.arange(1, 5, dtype=np.float32).reshape(2, 2) / 8
+    rc, h = _alloc_fmt(hw, p, 2, ks=ks)
+    assert rc == hw.OK, hw.last_error()
+    code = ctypes.c_int32()
+    k_out = np.zeros((2, 2), dtype=np.float32)
+    v_out = np.zeros((2, 2), dtype=np.float32)
+    assert hw._lib.hwkv_cache_format(h, ctypes.byref(code), k_out.ctypes.data_as(ctypes.c_void_p),
+                                     v_out.ctypes.data_as(ctypes.c_void_p)) == hw.OK
+    assert code.value == 2 and np.array_equal(k_out, ks) and np.all(v_out == 1.0)
+    # prefill attention reads bf16 caches only: rejected before any device work
+    rc = hw._lib.hwkv_prefill_attn(h, 0, 0, 0, 4, FAKE, FAKE, FAKE, 0.1, FAKE, None)
+    assert rc == hw.EINVAL and "bf16" in hw.last_error()
+    hw._lib.hwkv_cache_free(h)

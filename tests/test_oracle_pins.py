@@ -464,3 +464,135 @@ def test_selection_rules_on_worked_examples(golden):
     for case in g["budget"]:
         got = oracle.budget_select(case["rates"], case["floors"], case["budget"])
         assert got == case["chosen"], case["derivation"]
+
+
+# --------------------------------------------------------------------------
+# cache formats p_KV (Eq. nominal-storage carries b^K, b^V; the stored value
+# of an element is what attention sees)
+# --------------------------------------------------------------------------
+from oracle import kvformat as KF  # noqa: E402
+
+
+def test_e4m3_table_follows_the_format_definition():
+    T = KF.E4M3_TABLE
+    assert T[0x00] == 0.0 and T[0x80] == 0.0 and np.signbit(T[0x80])
+    assert T[0x01] == 2.0 ** -9             # smallest subnormal
+    assert T[0x07] == 7 * 2.0 ** -9         # largest subnormal
+    assert T[0x08] == 2.0 ** -6             # smallest normal
+    assert T[0x38] == 1.0 and T[0x39] == 1.125 and T[0x40] == 2.0
+    assert T[0x7D] == 416.0 and T[0x7E] == 448.0 and T[0xFE] == -448.0
+    assert np.isnan(T[0x7F]) and np.isnan(T[0xFF])
+    assert np.all(np.diff(T[:0x7F]) > 0)    # magnitudes strictly increase
+    assert np.array_equal(T[0x80:0xFF], -T[0x00:0x7F])
+    # an independent decoder: torch's float8_e4m3fn, all 256 codes
+    t = torch.arange(256, dtype=torch.uint8).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    nan = np.isnan(T)
+    assert np.array_equal(np.isnan(t), nan)
+    assert np.array_equal(t[~nan], T[~nan])
+
+
+@pytest.mark.parametrize("x,s,code", [
+    (1.0, 1.0, 0x38),
+    (1.0625, 1.0, 0x38),          # tie 1.0 / 1.125: even code
+    (1.1875, 1.0, 0x3A),          # tie 1.125 / 1.25: even code
+    (2.0 ** -10, 1.0, 0x00),      # tie 0 / 2^-9: even code (zero)
+    (3 * 2.0 ** -10, 1.0, 0x02),  # tie 2^-9 / 2^-8: even code
+    (5 * 2.0 ** -10, 1.0, 0x02),  # tie 2 / 3 x 2^-9
+    (2.0 ** -6 * (1 - 2.0 ** -20), 1.0, 0x08),   # rounds up to the smallest normal
+    (240.0, 1.0, 0x77),
+    (432.0, 1.0, 0x7E),           # tie 416 (odd) / 448 (even)
+    (448.0, 1.0, 0x7E),
+    (460.0, 1.0, 0x7E),           # saturates
+    (1e30, 1.0, 0x7E),
+    (float("inf"), 1.0, 0x7E),
+    (float("-inf"), 1.0, 0xFE),
+    (float("nan"), 1.0, 0x7F),
+    (0.0, 1.0, 0x00),
+    (-0.0, 1.0, 0x80),
+    (-1e-30, 1.0, 0x80),          # rounds to zero, keeps the sign
+    (1.0, 0.5, 0x40),             # 1 / 0.5 = 2
+    (1.0, 3.0, 0x2B),             # fp32(1/3) = 1.333 x 2^-2 -> m = 3 (0.375 nearer than 0.25)
+    (-300.0, 0.25, 0xFE),         # -1200 saturates
+])
+def test_e4m3_encode_worked_cases(x, s, code):
+    assert int(KF.e4m3_encode(np.array([x]), s)[0]) == code
+
+
+@pytest.mark.parametrize("s", [1.0, 0.0123, 3.7e-3, 17.5])
+def test_e4m3_encode_matches_torch_on_every_bf16(s):
+    """Below the overflow threshold the encoder is the IEEE-style conversion
+    torch implements (round to nearest even); above it, it saturates."""
+    bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    x = KF.bf16_values(bits)
+    got = KF.e4m3_encode(x, s)
+    with np.errstate(all="ignore"):
+        y = (x.astype(np.float32) / np.float32(s)).astype(np.float32)
+    sel = np.isfinite(y) & (np.abs(y) < 464)
+    t = torch.from_numpy(y[sel]).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    assert np.array_equal(got[sel], t)
+    big = np.isfinite(y) & (np.abs(y) >= 464) | np.isinf(y)
+    assert np.all((got[big] & 0x7F) == 0x7E)
+    assert np.all((got[np.isnan(y)] & 0x7F) == 0x7F)
+    # and every code decodes to within half a step of its input
+    fin = np.isfinite(y) & (np.abs(y) <= 448)
+    v = KF.e4m3_values(got[fin])
+    a = np.abs(y[fin].astype(np.float64))
+    step = np.where(a < 2.0 ** -6, 2.0 ** -9, 2.0 ** (np.floor(np.log2(np.maximum(a, 2.0 ** -6))) - 3))
+    assert np.all(np.abs(v - y[fin]) <= step / 2)
+
+
+@pytest.mark.parametrize("x,bits", [
+    (1.0, 0x3C00), (1.0078125, 0x3C08), (65504.0, 0x7BFF), (65519.0, 0x7BFF),
+    (65520.0, 0x7C00),            # tie 65504 (odd) / overflow: to infinity
+    (2.0 ** -24, 0x0001), (2.0 ** -25, 0x0000), (3 * 2.0 ** -25, 0x0002),
+    (-(2.0 ** -25), 0x8000), (2.0 ** -14, 0x0400),
+])
+def test_f16_encode_worked_cases(x, bits):
+    assert int(KF.f16_encode(np.array([x]))[0]) == bits
+
+
+def test_f16_is_exact_on_bf16_values_in_its_normal_range():
+    bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    x = KF.bf16_values(bits)
+    sel = np.isfinite(x) & (np.abs(x) >= 2.0 ** -14) & (np.abs(x) <= 65504)
+    assert np.array_equal(KF.values(KF.store(bits[sel], "f16"), "f16"), x[sel])
+
+
+def test_attend_values_matches_the_c_oracle_on_bf16_values():
+    r = np.random.default_rng(21)
+    B, Hq, Hkv, d = 2, 6, 2, 32
+    n = 90
+    q = bf16(r.standard_normal((B, Hq, d)))
+    k = [bf16(r.standard_normal((n, Hkv, d))) for _ in range(B)]
+    v = [bf16(r.standard_normal((n, Hkv, d))) for _ in range(B)]
+    t = np.array([89, 40])
+    for S, wins in ((0, [0, 0]), (3, [7, 0]), (2, [1, 50])):
+        ref = oracle.decode_layer(q, k, v, t, S, wins, 0.3)
+        got = KF.attend_values(f64(q), [f64(x) for x in k], [f64(x) for x in v], t, S, wins, 0.3)
+        assert np.max(np.abs(got - ref)) <= 1e-13 * np.max(np.abs(ref))
+
+
+def test_attend_values_closed_forms():
+    r = np.random.default_rng(22)
+    d, n = 16, 40
+    q = r.standard_normal((1, 2, d))
+    kk = np.tile(r.standard_normal(d), (n, 1, 1))          # identical keys
+    vv = r.standard_normal((n, 1, d))
+    out = KF.attend_values(q, [kk], [vv], [n - 1], 3, [10], 0.7)
+    pos = list(range(3)) + list(range(n - 10, n))
+    assert np.allclose(out[0, 0], vv[pos, 0].mean(axis=0), rtol=0, atol=1e-14)
+    assert np.allclose(out[0, 1], vv[pos, 0].mean(axis=0), rtol=0, atol=1e-14)
+    one = KF.attend_values(q, [kk], [vv], [0], 0, [5], 0.7)  # a single retained token
+    assert np.array_equal(one[0, 0], vv[0, 0])
+
+
+def test_storage_accounting_per_format():
+    """Eq. nominal-storage with b^K = b^V = 1 (fp8) is exactly half of the
+    16-bit formats, unit by unit."""
+    wins = np.array([2048, 0, 512])
+    for ctx in (100, 4096, 131072):
+        b16 = oracle.policy_bytes(ctx, 4, wins, 256, 256, 2.0, 2.0)
+        b8 = oracle.policy_bytes(ctx, 4, wins, 256, 256, 1.0, 1.0)
+        assert b8 * 2 == b16
+        exp = sum(min(4 + w, ctx) if w else ctx for w in wins) * 256 * 2
+        assert b8 == exp
