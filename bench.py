@@ -49,6 +49,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--workload", default="ctx112k",
                     choices=["ctx112k", "ctx32k", "batch16", "pr1", "prefill128k", "calib128k"])
+    ap.add_argument("--kv-format", default="bf16", choices=["bf16", "f16", "fp8"],
+                    help="cache format of the decode workloads (fp8: E4M3 with the "
+                         "workload's per-unit scales)")
     ap.add_argument("--unfused", action="store_true",
                     help="time hwkv_append + hwkv_decode_attn instead of the fused call")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -107,7 +110,10 @@ def main():
     scale = 1.0 / math.sqrt(D)
 
     pol = hwkv.policy_set(L, Hkv, Hq, D, S, cfg["level_windows"], levels)
-    cache = hwkv.cache_alloc(pol, B, max_ctx)
+    fmt = args.kv_format
+    eb = hwkv.KV_FORMATS[fmt][1]                  # bytes per stored element
+    scales = W.fp8_scales(cfg) if fmt == "fp8" else None
+    cache = hwkv.cache_alloc(pol, B, max_ctx, kv_format=fmt, k_scale=scales, v_scale=scales)
     ws = torch.zeros(hwkv.decode_workspace_bytes(cache), dtype=torch.uint8, device=dev)
     caps = [[hwkv.cache_unit_info(cache, l, h)[0] for h in range(Hkv)] for l in range(L)]
     outl = W.outlier_channels(cfg)
@@ -146,7 +152,7 @@ def main():
             for b in range(B):
                 n = prompts[b] + step_idx + 1
                 for h in range(Hkv):
-                    tot += min(n, caps[l][h]) * D * 2 * 2
+                    tot += min(n, caps[l][h]) * D * 2 * eb
             per_layer.append(tot)
         return per_layer
 
@@ -208,9 +214,12 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16 (fp32 accumulate)",
+        "dtype": {"bf16": "bf16 (fp32 accumulate)",
+                  "f16": "f16 K/V, bf16 q (fp32 accumulate)",
+                  "fp8": "fp8-e4m3 K/V, bf16 q (fp32 accumulate)"}[fmt],
         "data": "synthetic",
         "config": {
+            "kv_format": fmt,
             "workload": (f"{cfg['name']}: {L} residual global layers, batch {B}, "
                          f"{Hq} q / {Hkv} kv heads, head_dim {D}, {S} sinks, levels "
                          f"{cfg['level_windows']} (0 = full), R={rate:.4f} at {max_ctx} tokens, "
@@ -238,7 +247,7 @@ def main():
 
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(args, cfg, prompts, windows, caps, scale, outl, osc,
-                                              dev, ms_per_step, bytes_per_step)
+                                              dev, ms_per_step, bytes_per_step, eb, scales)
     cache.free()
     print(json.dumps(result), flush=True)
 
@@ -250,7 +259,9 @@ def measured_traffic(args):
     if args.workload != "ctx112k" or args.unfused:
         return None, None
     from paper_2609_02029_amd import profiling
-    path = os.path.join(ROOT, "profiles", "decode_split_ctx112k_traffic.json")
+    name = ("decode_split_ctx112k_traffic.json" if args.kv_format == "bf16"
+            else f"decode_split_ctx112k_{args.kv_format}_traffic.json")
+    path = os.path.join(ROOT, "profiles", name)
     try:
         with open(path) as f:
             rec = json.load(f)
@@ -258,23 +269,31 @@ def measured_traffic(args):
         return None, None
     if rec.get("kernel_source_sha256_16") != profiling.kernel_source_hash(rec["kernel"]):
         return None, "counter record is stale: decode kernel source changed"
+    from paper_2609_02029_amd import hwkv
+    code = hwkv.KV_FORMATS[args.kv_format][0]
+    if not rec.get("kernel", "").endswith(f", {code}>"):
+        return None, "counter record is for another cache format"
     total = rec["fetch_bytes"] + rec["write_bytes"]
     return round(total), {"fetch_bytes": round(rec["fetch_bytes"]),
                           "write_bytes": round(rec["write_bytes"]),
-                          "source": "profiles/decode_split_ctx112k_traffic.json"}
+                          "source": "profiles/" + name}
 
 
-def cpu_baseline(args, cfg, prompts, windows, caps, scale, outl, osc, dev, gpu_ms, step_bytes):
+def cpu_baseline(args, cfg, prompts, windows, caps, scale, outl, osc, dev, gpu_ms, step_bytes,
+                 eb=2, scales=None):
     """The fp64 oracle timed on the host cores on a bounded sample of the same
     step: whole layers of decode step 0 (every sequence and query head),
     regenerated from the same seeds, until about ``--cpu-seconds`` of oracle
     time; scaled to a full step by the sampled layers' share of the step's
-    resident bytes."""
+    resident bytes.  For the f16 and fp8 formats the oracle attends over the
+    stored values (encoded before the timed call)."""
     import numpy as np
     import torch
 
     import oracle
     import workloads as W
+    from oracle import kvformat as KF
+    fmt = args.kv_format
 
     L, B = cfg["n_layers"], cfg["batch"]
     Hq, Hkv, D = cfg["n_q_heads"], cfg["n_kv_heads"], cfg["head_dim"]
@@ -303,13 +322,24 @@ def cpu_baseline(args, cfg, prompts, windows, caps, scale, outl, osc, dev, gpu_m
             vh.append(hv)
             t.append(P + step)
         q = W.normal_bf16((B, Hq, D), cfg["seed"], l, W.Q, step)
-        t0 = time.perf_counter()
-        oracle.decode_layer(q, kh, vh, t, cfg["n_sinks"], windows[l], scale, n_threads=threads)
+        if fmt == "bf16":
+            t0 = time.perf_counter()
+            oracle.decode_layer(q, kh, vh, t, cfg["n_sinks"], windows[l], scale,
+                                n_threads=threads)
+        else:
+            sc = scales[l] if scales is not None else np.ones(Hkv, dtype=np.float32)
+            kv = [np.stack([KF.values(KF.store(x[:, h], fmt, sc[h]), fmt, sc[h])
+                            for h in range(Hkv)], axis=1) for x in kh]
+            vv = [np.stack([KF.values(KF.store(x[:, h], fmt, sc[h]), fmt, sc[h])
+                            for h in range(Hkv)], axis=1) for x in vh]
+            t0 = time.perf_counter()
+            KF.attend_values(KF.bf16_values(q), kv, vv, t, cfg["n_sinks"], windows[l], scale)
+            del kv, vv
         spent += time.perf_counter() - t0
         layers += 1
         for b in range(B):
             for h in range(Hkv):
-                done_bytes += min(prompts[b] + step + 1, caps[l][h]) * D * 4
+                done_bytes += min(prompts[b] + step + 1, caps[l][h]) * D * 2 * eb
         del kh, vh
         if spent >= args.cpu_seconds:
             break
@@ -331,7 +361,8 @@ def cpu_baseline(args, cfg, prompts, windows, caps, scale, outl, osc, dev, gpu_m
         "cpu": model,
         "kind": "oracle",
         "sample": (f"decode step {step} (first timed step), layers 0..{layers - 1} of {L}, every "
-                   f"sequence and query head; fp64 masked-full-history oracle, "
+                   f"sequence and query head; fp64 masked-full-history oracle"
+                   f"{'' if fmt == 'bf16' else ' over the stored ' + fmt + ' values'}, "
                    f"{spent:.1f} s of CPU time; scaled to the whole step by resident bytes"),
         "gpu_speedup": round(us_per_step / (gpu_ms * 1e3), 1),
     }

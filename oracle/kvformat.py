@@ -14,10 +14,10 @@ an element is stored:
   correctly rounded fp32 division; the code is the finite E4M3 value nearest
   to it, ties to the code with an even last bit, magnitudes beyond 448
   (infinity included) giving 448, NaN giving S.1111.111, and the sign bit
-  copied from the quotient.  Encoding is done by brute force over the table
-  of all codes, built from the definition of the format (sign, 4 exponent
-  bits of bias 7, 3 mantissa bits; exponent field 0 holds the subnormals
-  m * 2^-9).
+  copied from the quotient.  Encoding looks the quotient up in the sorted
+  table of all finite codes, built from the definition of the format (sign,
+  4 exponent bits of bias 7, 3 mantissa bits; exponent field 0 holds the
+  subnormals m * 2^-9).
 
 The value of a stored element is its decoded value, times ``s`` for fp8.
 ``attend_values`` is decode attention (Eqs. conditional-attention-weight and
@@ -52,31 +52,30 @@ def bf16_values(bits):
         return b.view(np.float32).astype(np.float64)
 
 
-def e4m3_encode(x, scale, chunk=1 << 15):
+def e4m3_encode(x, scale, chunk=1 << 22):
     """E4M3 codes (uint8) of ``x`` (values exactly representable in fp32,
     e.g. bf16 values) divided by the fp32 ``scale``: nearest finite code,
-    ties to even, saturating, NaN to 0x7F | sign."""
+    ties to even, saturating, NaN to 0x7F | sign.  The nearest code is found
+    in the sorted table of the 127 finite magnitudes: of the two table
+    entries around |y|, the closer one, or the one with the even code on a
+    tie."""
     y = np.asarray(x, dtype=np.float64).astype(np.float32)
     with np.errstate(over="ignore", invalid="ignore", divide="ignore"):
         y = (y / np.float32(scale)).astype(np.float32).ravel()
     out = np.empty(y.size, dtype=np.uint8)
     mags = E4M3_TABLE[:127]           # codes 0x00 .. 0x7E, increasing
-    codes = np.arange(127)
     for i0 in range(0, y.size, chunk):
         yy = y[i0:i0 + chunk].astype(np.float64)
         a = np.abs(yy)
         fin = np.isfinite(a)
-        # beyond 448 the nearest finite code is 448 whatever the magnitude;
-        # clamping at 896 keeps every distance below exact in fp64 (far
-        # larger magnitudes would make all 127 distances round alike)
-        af = np.minimum(np.where(fin, a, 0.0), 896.0)
-        d = np.abs(af[:, None] - mags[None, :])
-        dmin = d.min(axis=1, keepdims=True)
-        cand = d == dmin
-        # among the (at most two) nearest codes, the one with an even last bit
-        even = cand & (codes[None, :] % 2 == 0)
-        pick = np.where(even.any(axis=1), even.argmax(axis=1), cand.argmax(axis=1))
-        c = pick.astype(np.uint8)
+        # beyond 448 the nearest finite code is 448 whatever the magnitude
+        af = np.minimum(np.where(fin, a, 0.0), 448.0)
+        hi = np.clip(np.searchsorted(mags, af, side="left"), 1, 126)   # mags[hi-1] < af <= mags[hi]
+        lo = hi - 1
+        dlo = af - mags[lo]            # exact: neighbours of af within a binade or two
+        dhi = mags[hi] - af
+        c = np.where(dlo < dhi, lo, np.where(dhi < dlo, hi, np.where(lo % 2 == 0, lo, hi)))
+        c = np.where(af == 0.0, 0, c).astype(np.uint8)
         c = np.where(np.isinf(a), np.uint8(0x7E), c)
         c = np.where(np.isnan(a), np.uint8(0x7F), c)
         c = c | np.where(np.signbit(yy), np.uint8(0x80), np.uint8(0))
@@ -99,16 +98,28 @@ def f16_values(bits):
     return np.asarray(bits, dtype=np.uint16).view(np.float16).astype(np.float64)
 
 
+_ALL_BF16 = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+_TABLES = {}
+
+
+def _pattern_table(fmt, scale):
+    """The stored element of every bf16 bit pattern (the encoding is a
+    function of the pattern and the scale), computed once per scale."""
+    key = (fmt, float(np.float32(scale)))
+    if key not in _TABLES:
+        x = bf16_values(_ALL_BF16)
+        _TABLES[key] = f16_encode(x) if fmt == "f16" else e4m3_encode(x, scale)
+    return _TABLES[key]
+
+
 def store(bits_bf16, fmt, scale=1.0):
     """Stored elements of bf16 inputs in format ``fmt``: uint16 bf16 bits,
     uint16 binary16 bits or uint8 E4M3 codes."""
     bits_bf16 = np.asarray(bits_bf16, dtype=np.uint16)
     if fmt == "bf16":
         return bits_bf16.copy()
-    if fmt == "f16":
-        return f16_encode(bf16_values(bits_bf16))
-    if fmt == "fp8":
-        return e4m3_encode(bf16_values(bits_bf16), scale)
+    if fmt in ("f16", "fp8"):
+        return _pattern_table(fmt, scale if fmt == "fp8" else 1.0)[bits_bf16]
     raise ValueError(f"unknown format {fmt!r}")
 
 

@@ -176,3 +176,33 @@ def test_fp8_cache_rejects_prefill_attention():
     assert e.value.code == hwkv.EINVAL
     assert hwkv.cache_seq_len(cache, 0, 0) == 0
     cache.free()
+
+
+# ---------------------------------------------------------------------------
+# the 112K, 16-layer workload at full size in fp8, in the launch configuration
+# the benchmark times (fused append + decode per layer, the workload's scales)
+# ---------------------------------------------------------------------------
+@pytest.mark.timeout(1200)
+def test_fp8_ctx112k_workload_full_size():
+    import workloads as W
+    from hwkv_harness import timed
+    cfg = W.CONFIGS["ctx112k"]
+    track = [0, 15]
+    sc = W.fp8_scales(cfg)
+    r = Run(cfg, track=track, device_gen=True, kv_format="fp8", k_scale=sc, v_scale=sc)
+    with timed("fp8 ctx112k prefill"):
+        for l in range(cfg["n_layers"]):
+            r.prefill(l, 0)
+            if l in track:
+                r.check_layer(l)
+    worst = 0.0
+    with timed("fp8 ctx112k 128 steps x 16 layers"):
+        for st in range(cfg["steps"]):
+            for l in range(cfg["n_layers"]):
+                qa, out = r.step(l)
+                if st in (0, cfg["steps"] - 1) and l in track:
+                    worst = max(worst, r.check_out(l, qa, out, f"fp8 ctx112k layer {l} step {st}"))
+    for l in track:
+        r.check_layer(l)
+    log(f"fp8 ctx112k: max rel err {worst:.3e}")
+    r.free()

@@ -134,6 +134,15 @@ def outlier_channels(cfg):
             for h in range(cfg["n_kv_heads"])}
 
 
+def fp8_scales(cfg, sigmas=8.0):
+    """fp8 scales of every (layer, kv head), for K and for V alike: the
+    synthetic keys and values are unit normal (outlier channels scaled by
+    ``outlier_scale``), and ``sigmas`` standard deviations of the largest
+    channel map to the largest E4M3 magnitude, 448."""
+    s = sigmas * max(1.0, float(cfg.get("outlier_scale", 1.0))) / 448.0
+    return np.full((cfg["n_layers"], cfg["n_kv_heads"]), s, dtype=np.float32)
+
+
 def _stored_policies():
     path = os.path.join(HERE, "policies.json")
     with open(path) as f:
