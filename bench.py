@@ -52,6 +52,9 @@ def parse():
     ap.add_argument("--kv-format", default="bf16", choices=["bf16", "f16", "fp8"],
                     help="cache format of the decode workloads (fp8: E4M3 with the "
                          "workload's per-unit scales)")
+    ap.add_argument("--paged", action="store_true",
+                    help="page the full units (pages of 256 rows from a pool sized to the "
+                         "workload's final lengths) instead of reserving max_ctx rows")
     ap.add_argument("--unfused", action="store_true",
                     help="time hwkv_append + hwkv_decode_attn instead of the fused call")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -113,7 +116,18 @@ def main():
     fmt = args.kv_format
     eb = hwkv.KV_FORMATS[fmt][1]                  # bytes per stored element
     scales = W.fp8_scales(cfg) if fmt == "fp8" else None
-    cache = hwkv.cache_alloc(pol, B, max_ctx, kv_format=fmt, k_scale=scales, v_scale=scales)
+    n_pages = None
+    if args.paged:
+        # every full unit of every layer holds ceil(n_b / 256) pages at the
+        # final length n_b = prompt_b + total_steps
+        full = sum(1 for l in range(L) for h in range(Hkv)
+                   if windows[l][h] == 0 or S + windows[l][h] >= max_ctx)
+        n_pages = full * sum((p + total_steps + hwkv.PAGE_TOKENS - 1) // hwkv.PAGE_TOKENS
+                             for p in prompts)
+    cache = hwkv.cache_alloc(pol, B, max_ctx, kv_format=fmt, k_scale=scales, v_scale=scales,
+                             n_pages=n_pages)
+    cache_bytes = hwkv.cache_bytes(pol, B, max_ctx, fmt, n_pages=n_pages)
+    reserved_bytes = hwkv.cache_bytes(pol, B, max_ctx, fmt)
     ws = torch.zeros(hwkv.decode_workspace_bytes(cache), dtype=torch.uint8, device=dev)
     caps = [[hwkv.cache_unit_info(cache, l, h)[0] for h in range(Hkv)] for l in range(L)]
     outl = W.outlier_channels(cfg)
@@ -220,6 +234,9 @@ def main():
         "data": "synthetic",
         "config": {
             "kv_format": fmt,
+            "paged": bool(args.paged),
+            "cache_bytes": int(cache_bytes),
+            "cache_bytes_reserved_layout": int(reserved_bytes),
             "workload": (f"{cfg['name']}: {L} residual global layers, batch {B}, "
                          f"{Hq} q / {Hkv} kv heads, head_dim {D}, {S} sinks, levels "
                          f"{cfg['level_windows']} (0 = full), R={rate:.4f} at {max_ctx} tokens, "
@@ -256,7 +273,7 @@ def measured_traffic(args):
     """HBM bytes per decode_split launch from the committed counter record
     (FETCH_SIZE + WRITE_SIZE, copy-calibrated), if it was taken on the current
     kernel source and on this workload; otherwise None."""
-    if args.workload != "ctx112k" or args.unfused:
+    if args.workload != "ctx112k" or args.unfused or args.paged:
         return None, None
     from paper_2609_02029_amd import profiling
     name = ("decode_split_ctx112k_traffic.json" if args.kv_format == "bf16"

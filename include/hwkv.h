@@ -179,6 +179,44 @@ int hwkv_cache_alloc_format(hwkv_cache **out, const hwkv_policy *policy,
 int hwkv_cache_format(const hwkv_cache *cache, int32_t *kv_format,
                       float *k_scale, float *v_scale);
 
+/* Paged storage of the full units, for ragged batches (the reservation of
+ * max_ctx rows per full unit and sequence is what dominates a batch of short
+ * and long sequences; the paper cites paged memory management as orthogonal
+ * to its retention policy).  In a paged cache the finite units keep their
+ * S + w rows per sequence; the full units hold no fixed storage and take
+ * pages of HWKV_PAGE_TOKENS token rows (K and V of one unit and sequence)
+ * from one pool as their sequences grow.  Calls that need pages take them
+ * from the pool first and fail with ENOMEM, changing nothing, when it has
+ * too few; hwkv_cache_reset_seq returns a sequence's pages.  Results are
+ * those of an unpaged cache. */
+#define HWKV_PAGE_TOKENS 256
+
+/* Exact device bytes of a paged cache: the finite units as in
+ * hwkv_cache_bytes_format, a pool of n_pages pages of
+ * 2 * HWKV_PAGE_TOKENS * head_dim * b bytes, and the page table (4 bytes per
+ * page of every full unit and sequence at max_ctx), each part 256-byte
+ * aligned.  n_pages >= 0.  EINVAL as hwkv_cache_bytes_format. */
+int hwkv_cache_bytes_paged(const hwkv_policy *policy, int32_t batch,
+                           int64_t max_ctx, int32_t kv_format, int64_t n_pages,
+                           size_t *bytes);
+
+/* Allocate a paged cache: arguments as hwkv_cache_alloc_format, plus the pool
+ * size n_pages (pages of HWKV_PAGE_TOKENS rows).  The pool starts free. */
+int hwkv_cache_alloc_paged(hwkv_cache **out, const hwkv_policy *policy,
+                           int32_t batch, int64_t max_ctx, int32_t kv_format,
+                           const float *k_scale, const float *v_scale,
+                           int64_t n_pages, void *dev_buf, size_t buf_bytes);
+
+/* Pool size and free pages of a paged cache (0 and 0 for an unpaged one). */
+int hwkv_cache_pages(const hwkv_cache *cache, int64_t *total,
+                     int64_t *free_pages);
+
+/* Release sequence `seq`: its length becomes 0 in every layer and the pages
+ * of its full units return to the pool (host bookkeeping only: no device
+ * work, ordered with the cache's other calls as they are issued).  Valid on
+ * any cache; a released sequence is filled again from position 0. */
+int hwkv_cache_reset_seq(hwkv_cache *cache, int32_t seq);
+
 /* Release the cache; frees device memory only if the library allocated it.
  * The caller must make sure no enqueued work still uses the cache. */
 int hwkv_cache_free(hwkv_cache *cache);
@@ -205,7 +243,8 @@ int hwkv_cache_unit_info(const hwkv_cache *cache, int32_t layer,
  *   k, v   device bf16 [n_tokens][n_kv_heads][head_dim], post-RoPE keys,
  *          stored in the cache's format.
  * ESTATE if pos0 != n(layer, seq); ECAPACITY if a full unit would pass
- * max_ctx; n_tokens == 0 is a no-op. */
+ * max_ctx; ENOMEM if a paged cache's pool has too few pages; n_tokens == 0
+ * is a no-op. */
 int hwkv_prefill_write(hwkv_cache *cache, int32_t layer, int32_t seq,
                        int64_t pos0, int64_t n_tokens, const void *k,
                        const void *v, void *stream);
@@ -233,7 +272,8 @@ int hwkv_prefill_attn(hwkv_cache *cache, int32_t layer, int32_t seq,
 
 /* Append one token to every sequence of `layer`: token n_b of sequence b
  * goes to slot(n_b) of each unit (once n_b >= S + w this overwrites token
- * n_b - w, the one leaving the window), then n_b += 1.
+ * n_b - w, the one leaving the window), then n_b += 1.  ENOMEM if a paged
+ * cache's pool has too few pages for the tokens.
  *   k_new, v_new   device bf16 [batch][n_kv_heads][head_dim], stored in
  *                  the cache's format.
  * ECAPACITY if a full unit of the layer already holds max_ctx tokens. */

@@ -89,6 +89,9 @@ constexpr int kTilesPerWave = HWKV_DECODE_TPW;   // 64-slot tiles per wave
 constexpr int kPrefetch = HWKV_DECODE_PREFETCH;  // 16-byte loads in flight
 constexpr int kPrefetch8 = HWKV_DECODE_PREFETCH8;  // 8-byte loads in flight
 constexpr int kMinWavesPerEU = HWKV_DECODE_MINWAVES;  // VGPR budget
+// A split is one page of a paged full unit: its workgroup reads one page.
+static_assert(kWaves * kTilesPerWave * kTile == kPageTokens && kTilesPerWave == 1,
+              "a decode split must be one page of 4 tiles, one per wave");
 #ifndef HWKV_COMBINE_THREADS
 #define HWKV_COMBINE_THREADS 512
 #endif
@@ -271,8 +274,22 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
   const int c8 = lane % NC;
   const int rsub = lane / NC;
 
-  uint8_t *kbase = static_cast<uint8_t *>(a.cache) + it.k_off[item] * EB;
-  uint8_t *vbase = static_cast<uint8_t *>(a.cache) + it.v_off[item] * EB;
+  // Region this workgroup reads: the item's rows, or for a paged unit the
+  // page of this split (rows r0 .. r0 + 255 of the unit); every address
+  // below is relative to the region's first row r0.
+  uint8_t *kbase, *vbase;
+  int r0 = 0, rows = nv;
+  if (it.pto[item] >= 0) {
+    const int64_t pg = a.page_table[it.pto[item] + split];
+    kbase = static_cast<uint8_t *>(a.cache) +
+            (a.pool_off + pg * 2 * kPageTokens * D) * EB;
+    vbase = kbase + kPageTokens * D * EB;
+    r0 = split * kPageTokens;
+    rows = min(nv - r0, kPageTokens);
+  } else {
+    kbase = static_cast<uint8_t *>(a.cache) + it.k_off[item] * EB;
+    vbase = static_cast<uint8_t *>(a.cache) + it.v_off[item] * EB;
+  }
   // q is uniform across the workgroup: read it through the scalar path
   // (constant address space), so v_dot2 takes it as an SGPR operand
   const cu32x4_t *qc = (const cu32x4_t *)(a.q + (size_t)it.q_row[item] * D);
@@ -292,12 +309,12 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
     if (threadIdx.x < NC) {
       const int g = threadIdx.x;
       store_chunk<F>(
-          kbase + (((size_t)(new_slot / 64) * NC + g) * 64 + new_slot % 64) * LB,
+          kbase + (((size_t)((new_slot - r0) / 64) * NC + g) * 64 + new_slot % 64) * LB,
           encode8<F>(*reinterpret_cast<const uint4 *>(a.k_new + src + g * 8),
                      it.k_scale[item]));
     } else {
       const int g = threadIdx.x - NC;
-      store_chunk<F>(vbase + (size_t)new_slot * D * EB + g * LB,
+      store_chunk<F>(vbase + (size_t)(new_slot - r0) * D * EB + g * LB,
                      encode8<F>(*reinterpret_cast<const uint4 *>(a.v_new + src + g * 8),
                                 it.v_scale[item]));
     }
@@ -321,8 +338,8 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
 
   // K: every tile up to the last occupied one; V: rows [0, nv) only
   const __amdgpu_buffer_rsrc_t krs =
-      make_rsrc(kbase, (uint32_t)(((nv + 63) / 64) * 64 * D * EB));
-  const __amdgpu_buffer_rsrc_t vrs = make_rsrc(vbase, (uint32_t)(nv * D * EB));
+      make_rsrc(kbase, (uint32_t)(((rows + 63) / 64) * 64 * D * EB));
+  const __amdgpu_buffer_rsrc_t vrs = make_rsrc(vbase, (uint32_t)(rows * D * EB));
   // logit scale (base 2), with the fp8 K scale folded in
   const float zscale =
       F == HWKV_KV_FP8_E4M3 ? a.scale_log2 * it.k_scale[item] : a.scale_log2;
@@ -334,7 +351,7 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
   // first K loads of the wave's next tile while its last V rows are.
   Chunk buf[PF];
   int t = wl;
-  int kofs = t * 64 * D * EB + lane * LB;
+  int kofs = (t * 64 - r0) * D * EB + lane * LB;
   if (t < n_tiles) static_for<PF>([&](auto jc) {
     buf[jc.value] = bload_chunk<F>(krs, kofs + jc.value * 64 * LB);
   });
@@ -343,8 +360,8 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
     const int slot = slot0 + lane;
     const int tn = t + nw;
     const bool has_next = k + 1 < kTilesPerWave && tn < n_tiles;
-    int vofs = (slot0 + rsub) * D * EB + c8 * LB;
-    int kofs_n = tn * 64 * D * EB + lane * LB;
+    int vofs = (slot0 - r0 + rsub) * D * EB + c8 * LB;
+    int kofs_n = (tn * 64 - r0) * D * EB + lane * LB;
     uint64_t qaddr = (uint64_t)qc;
     // load j of this tile's stream: K chunk j, or V step j - NC
     auto ld = [&](auto jc) -> Chunk {

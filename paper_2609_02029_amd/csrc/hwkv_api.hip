@@ -41,6 +41,16 @@ struct hwkv_cache {
   int32_t elem = 2;              // bytes per stored element
   std::vector<float> k_scale;    // per unit (fp8 scales; 1 otherwise)
   std::vector<float> v_scale;
+  // paged caches: full units take pages of kPageTokens rows from a pool
+  bool paged = false;
+  int64_t n_pages = 0;           // pool size
+  int64_t max_pages = 0;         // pages per (full unit, sequence) at max_ctx
+  int64_t pool_off = 0;          // element offset of page 0
+  size_t table_off = 0;          // byte offset of the device page table
+  std::vector<int32_t> full_index;  // per unit: rank among full units, or -1
+  std::vector<int32_t> pt_host;  // host copy of the page table
+  std::vector<int32_t> held;     // pages held per (full unit, sequence)
+  std::vector<int32_t> free_list;  // free pages (taken from the back)
   uint8_t *base = nullptr;
   size_t bytes = 0;
   bool owned = false;
@@ -96,11 +106,16 @@ void unit_shape(const hwkv_policy &p, int32_t u, int64_t max_ctx,
   }
 }
 
+uint64_t round256(uint64_t bytes) { return (bytes + 255) / 256 * 256; }
+
 // Lays out the grouped pools for elements of `elem` bytes; fills per-unit
-// vectors when `c` is non-null.
+// vectors when `c` is non-null.  paged: full units get no region; a pool of
+// n_pages pages and the page table follow the finite units' regions.
 int layout(const hwkv_policy &p, int32_t batch, int64_t max_ctx, int elem,
-           size_t *bytes, hwkv_cache *c) {
+           bool paged, int64_t n_pages, size_t *bytes, hwkv_cache *c) {
   if (batch < 1) return fail(HWKV_EINVAL, "batch must be >= 1");
+  if (paged && (n_pages < 0 || n_pages > (int64_t)INT32_MAX))
+    return fail(HWKV_EINVAL, "n_pages must be in [0, 2^31)");
   // the decode kernels address one (unit, sequence) region with 32-bit byte
   // offsets: round_tile(max_ctx) * head_dim * elem must stay below 2^31
   if (max_ctx < 1 ||
@@ -115,6 +130,11 @@ int layout(const hwkv_policy &p, int32_t batch, int64_t max_ctx, int elem,
     unit_shape(p, u, max_ctx, &win[u], &cap[u]);
     capp[u] = round_tile(cap[u]);
   }
+  std::vector<int32_t> fidx(U, -1);
+  int32_t n_full = 0;
+  if (paged)
+    for (int32_t u = 0; u < U; ++u)
+      if (win[u] == 0) fidx[u] = n_full++;
   // [level][unit in level][seq] K regions, then the V regions of the level
   uint64_t off = 0;  // elements
   auto mul_ok = [&](uint64_t a, uint64_t b, uint64_t *r) {
@@ -124,6 +144,10 @@ int layout(const hwkv_policy &p, int32_t batch, int64_t max_ctx, int elem,
     for (int pass = 0; pass < 2; ++pass) {
       for (int32_t u = 0; u < U; ++u) {
         if (p.level_of_unit[u] != lv) continue;
+        if (fidx[u] >= 0) {            // paged full unit: no region
+          (pass == 0 ? koff : voff)[u] = -1;
+          continue;
+        }
         uint64_t region;
         if (!mul_ok((uint64_t)capp[u] * D, (uint64_t)batch, &region) ||
             __builtin_add_overflow(off, region, &off) ||
@@ -133,16 +157,72 @@ int layout(const hwkv_policy &p, int32_t batch, int64_t max_ctx, int elem,
       }
     }
   }
-  *bytes = (size_t)(off * (uint64_t)elem);
+  uint64_t total = off * (uint64_t)elem;
+  const int64_t max_pages = (max_ctx + hwkv::kPageTokens - 1) / hwkv::kPageTokens;
+  uint64_t pool_off = 0, table_off = 0;
+  if (paged) {
+    // pool: page i at element pool_off + i * 2 * kPageTokens * D
+    total = round256(total);
+    pool_off = total / (uint64_t)elem;
+    uint64_t pool, tab;
+    if (!mul_ok((uint64_t)n_pages, 2ull * hwkv::kPageTokens * D * (uint64_t)elem, &pool) ||
+        __builtin_add_overflow(total, pool, &total))
+      return fail(HWKV_EINVAL, "cache size overflows");
+    // table: int32 [full unit][seq][max_pages]; offsets into it are int32
+    total = round256(total);
+    table_off = total;
+    if (!mul_ok((uint64_t)n_full * (uint64_t)batch, (uint64_t)max_pages, &tab) ||
+        tab > (uint64_t)INT32_MAX || __builtin_add_overflow(total, tab * 4, &total))
+      return fail(HWKV_EINVAL, "page table too large");
+    if (total > (uint64_t)INT64_MAX / 4) return fail(HWKV_EINVAL, "cache size overflows");
+  }
+  *bytes = (size_t)total;
   if (c) {
     c->window = win;
     c->cap = cap;
     c->cap_pad = capp;
     c->k_off = koff;
     c->v_off = voff;
+    c->paged = paged;
+    if (paged) {
+      c->n_pages = n_pages;
+      c->max_pages = max_pages;
+      c->pool_off = (int64_t)pool_off;
+      c->table_off = (size_t)table_off;
+      c->full_index = fidx;
+      c->pt_host.assign((size_t)n_full * batch * max_pages, -1);
+      c->held.assign((size_t)n_full * batch, 0);
+      c->free_list.resize((size_t)n_pages);
+      for (int64_t i = 0; i < n_pages; ++i)  // page 0 is taken first
+        c->free_list[(size_t)i] = (int32_t)(n_pages - 1 - i);
+    }
   }
   return HWKV_OK;
 }
+
+// Page-table offset of (unit, seq) in a paged cache, or -1 if the unit is
+// not paged.
+int32_t page_tab_off(const hwkv_cache *c, int32_t u, int32_t seq) {
+  if (!c->paged || c->full_index[u] < 0) return -1;
+  return (int32_t)(((int64_t)c->full_index[u] * c->batch + seq) * c->max_pages);
+}
+
+int32_t *device_page_table(const hwkv_cache *c) {
+  return c->paged ? reinterpret_cast<int32_t *>(c->base + c->table_off) : nullptr;
+}
+
+// Takes the pages that the full units of `layer` need so that sequence b
+// holds rows [0, len[b]) for every (b, len) in `want`, and installs their
+// page-table entries on stream s (before the call's kernels, which run
+// after them in stream order).  ENOMEM, with nothing changed, if the pool
+// has too few free pages.
+int take_pages(hwkv_cache *c, int32_t layer,
+               const std::vector<std::pair<int32_t, int64_t>> &want, hipStream_t s);
+
+// Shared by hwkv_cache_alloc_format and hwkv_cache_alloc_paged.
+int alloc_impl(hwkv_cache **out, const hwkv_policy *p, int32_t batch, int64_t max_ctx,
+               int32_t kv_format, const float *k_scale, const float *v_scale, bool paged,
+               int64_t n_pages, void *dev_buf, size_t buf_bytes);
 
 int64_t group_size(const hwkv_policy &p) { return p.n_q_heads / p.n_kv_heads; }
 
@@ -182,6 +262,52 @@ int record_event(hwkv_cache *c, hipStream_t s) {
   }
   return check_device(hipEventRecord(c->ev_pool[c->ev_used++], s),
                       "hipEventRecord");
+}
+
+int take_pages(hwkv_cache *c, int32_t layer,
+               const std::vector<std::pair<int32_t, int64_t>> &want, hipStream_t s) {
+  if (!c->paged) return HWKV_OK;
+  const hwkv_policy &p = c->pol;
+  const int32_t H = p.n_kv_heads;
+  // count first: nothing changes unless every page is available
+  int64_t need_total = 0;
+  for (const auto &bw : want)
+    for (int32_t h = 0; h < H; ++h) {
+      const int32_t pto = page_tab_off(c, layer * H + h, bw.first);
+      if (pto < 0) continue;
+      const int64_t need = (bw.second + hwkv::kPageTokens - 1) / hwkv::kPageTokens;
+      const int64_t have = c->held[(size_t)(pto / c->max_pages)];
+      if (need > have) need_total += need - have;
+    }
+  if (need_total == 0) return HWKV_OK;
+  if (need_total > (int64_t)c->free_list.size())
+    return fail(HWKV_ENOMEM, "page pool exhausted: " + std::to_string(need_total) +
+                                 " pages needed, " + std::to_string(c->free_list.size()) +
+                                 " free");
+  hwkv::PageUpdateArgs u;
+  u.table = device_page_table(c);
+  u.n = 0;
+  for (const auto &bw : want)
+    for (int32_t h = 0; h < H; ++h) {
+      const int32_t pto = page_tab_off(c, layer * H + h, bw.first);
+      if (pto < 0) continue;
+      const int64_t need = (bw.second + hwkv::kPageTokens - 1) / hwkv::kPageTokens;
+      int32_t &have = c->held[(size_t)(pto / c->max_pages)];
+      for (; have < need; ++have) {
+        const int32_t pg = c->free_list.back();
+        c->free_list.pop_back();
+        c->pt_host[(size_t)pto + have] = pg;
+        u.idx[u.n] = pto + have;
+        u.page[u.n] = pg;
+        if (++u.n == hwkv::kMaxPageUpdates) {
+          const int rc = check_device(hwkv::launch_page_update(u, s), "page table launch");
+          if (rc != HWKV_OK) return rc;
+          u.n = 0;
+        }
+      }
+    }
+  if (u.n > 0) return check_device(hwkv::launch_page_update(u, s), "page table launch");
+  return HWKV_OK;
 }
 
 // Shared validation of a decode call; fills per-item lengths.
@@ -227,8 +353,14 @@ int decode_impl(hwkv_cache *c, int32_t layer, const void *k_new,
   if (!ws || ws_bytes < need)
     return fail(HWKV_EINVAL, "workspace missing or too small (need " +
                                  std::to_string(need) + " bytes)");
-  // launches of at most kMaxItems items
   const hipStream_t s = (hipStream_t)stream;
+  if (fused) {  // pages for the appended tokens (the last validation)
+    std::vector<std::pair<int32_t, int64_t>> want;
+    for (int32_t b = 0; b < B; ++b) want.push_back({b, seq_len(c, layer, b) + 1});
+    const int rc = take_pages(c, layer, want, s);
+    if (rc != HWKV_OK) return rc;
+  }
+  // launches of at most kMaxItems items
   int ws_split = 0;
   for (int i0 = 0; i0 < n_items_total; i0 += hwkv::kMaxItems) {
     const int cnt = std::min(hwkv::kMaxItems, n_items_total - i0);
@@ -248,6 +380,7 @@ int decode_impl(hwkv_cache *c, int32_t layer, const void *k_new,
       a.it.kv_row[j] = b * H + h;
       a.it.k_scale[j] = c->k_scale[u];
       a.it.v_scale[j] = c->v_scale[u];
+      a.it.pto[j] = page_tab_off(c, u, b);
       a.it.split_begin[j] = splits;
       splits += ns[i];
     }
@@ -255,6 +388,8 @@ int decode_impl(hwkv_cache *c, int32_t layer, const void *k_new,
     a.it.n_items = cnt;
     a.it.ws_split0 = ws_split;
     a.cache = c->base;
+    a.page_table = device_page_table(c);
+    a.pool_off = c->pool_off;
     a.q = static_cast<const uint16_t *>(q);
     a.k_new = static_cast<const uint16_t *>(k_new);
     a.v_new = static_cast<const uint16_t *>(v_new);
@@ -393,7 +528,16 @@ int hwkv_cache_bytes_format(const hwkv_policy *p, int32_t batch,
   if (!p || !bytes) return fail(HWKV_EINVAL, "null argument");
   const int elem = format_bytes(kv_format);
   if (elem == 0) return fail(HWKV_EINVAL, "unknown cache format");
-  const int rc = layout(*p, batch, max_ctx, elem, bytes, nullptr);
+  const int rc = layout(*p, batch, max_ctx, elem, false, 0, bytes, nullptr);
+  return rc == HWKV_OK ? ok() : rc;
+}
+
+int hwkv_cache_bytes_paged(const hwkv_policy *p, int32_t batch, int64_t max_ctx,
+                           int32_t kv_format, int64_t n_pages, size_t *bytes) {
+  if (!p || !bytes) return fail(HWKV_EINVAL, "null argument");
+  const int elem = format_bytes(kv_format);
+  if (elem == 0) return fail(HWKV_EINVAL, "unknown cache format");
+  const int rc = layout(*p, batch, max_ctx, elem, true, n_pages, bytes, nullptr);
   return rc == HWKV_OK ? ok() : rc;
 }
 
@@ -407,6 +551,25 @@ int hwkv_cache_alloc_format(hwkv_cache **out, const hwkv_policy *p,
                             int32_t batch, int64_t max_ctx, int32_t kv_format,
                             const float *k_scale, const float *v_scale,
                             void *dev_buf, size_t buf_bytes) {
+  return alloc_impl(out, p, batch, max_ctx, kv_format, k_scale, v_scale, false, 0,
+                    dev_buf, buf_bytes);
+}
+
+int hwkv_cache_alloc_paged(hwkv_cache **out, const hwkv_policy *p, int32_t batch,
+                           int64_t max_ctx, int32_t kv_format, const float *k_scale,
+                           const float *v_scale, int64_t n_pages, void *dev_buf,
+                           size_t buf_bytes) {
+  return alloc_impl(out, p, batch, max_ctx, kv_format, k_scale, v_scale, true, n_pages,
+                    dev_buf, buf_bytes);
+}
+
+}  // extern "C"
+
+namespace {
+
+int alloc_impl(hwkv_cache **out, const hwkv_policy *p, int32_t batch, int64_t max_ctx,
+               int32_t kv_format, const float *k_scale, const float *v_scale, bool paged,
+               int64_t n_pages, void *dev_buf, size_t buf_bytes) {
   if (!out || !p) return fail(HWKV_EINVAL, "null argument");
   *out = nullptr;
   const int elem = format_bytes(kv_format);
@@ -433,7 +596,7 @@ int hwkv_cache_alloc_format(hwkv_cache **out, const hwkv_policy *p,
     if (k_scale) c->k_scale.assign(k_scale, k_scale + n_units);
     if (v_scale) c->v_scale.assign(v_scale, v_scale + n_units);
     size_t bytes = 0;
-    int rc = layout(*p, batch, max_ctx, elem, &bytes, c);
+    int rc = layout(*p, batch, max_ctx, elem, paged, n_pages, &bytes, c);
     if (rc != HWKV_OK) {
       delete c;
       return rc;
@@ -483,6 +646,10 @@ int hwkv_cache_alloc_format(hwkv_cache **out, const hwkv_policy *p,
   return ok();
 }
 
+}  // namespace
+
+extern "C" {
+
 int hwkv_cache_free(hwkv_cache *c) {
   if (!c) return ok();
   int rc = HWKV_OK;
@@ -501,6 +668,32 @@ int hwkv_cache_format(const hwkv_cache *c, int32_t *kv_format, float *k_scale,
   *kv_format = c->fmt;
   if (k_scale) std::copy(c->k_scale.begin(), c->k_scale.end(), k_scale);
   if (v_scale) std::copy(c->v_scale.begin(), c->v_scale.end(), v_scale);
+  return ok();
+}
+
+int hwkv_cache_pages(const hwkv_cache *c, int64_t *total, int64_t *free_pages) {
+  if (!c || !total || !free_pages) return fail(HWKV_EINVAL, "null argument");
+  *total = c->paged ? c->n_pages : 0;
+  *free_pages = c->paged ? (int64_t)c->free_list.size() : 0;
+  return ok();
+}
+
+int hwkv_cache_reset_seq(hwkv_cache *c, int32_t seq) {
+  if (!c) return fail(HWKV_EINVAL, "cache is null");
+  if (seq < 0 || seq >= c->batch) return fail(HWKV_EINVAL, "seq out of range");
+  const hwkv_policy &p = c->pol;
+  for (int32_t l = 0; l < p.n_layers; ++l) {
+    seq_len(c, l, seq) = 0;
+    for (int32_t h = 0; h < p.n_kv_heads; ++h) {
+      const int32_t pto = page_tab_off(c, l * p.n_kv_heads + h, seq);
+      if (pto < 0) continue;
+      int32_t &have = c->held[(size_t)(pto / c->max_pages)];
+      for (; have > 0; --have) {
+        c->free_list.push_back(c->pt_host[(size_t)pto + have - 1]);
+        c->pt_host[(size_t)pto + have - 1] = -1;
+      }
+    }
+  }
   return ok();
 }
 
@@ -547,6 +740,10 @@ int hwkv_prefill_write(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0,
     if (c->window[u] == 0 && p1 > c->cap[u])
       return fail(HWKV_ECAPACITY, "prefill past max_ctx on a full unit");
   }
+  {
+    const int rc = take_pages(c, layer, {{seq, p1}}, (hipStream_t)stream);
+    if (rc != HWKV_OK) return rc;
+  }
   hwkv::WriteArgs a;
   std::memset(&a, 0, sizeof a);
   int max_tiles = 0;
@@ -557,7 +754,8 @@ int hwkv_prefill_write(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0,
     hwkv::WriteHead &wh = a.head[h];
     wh.k_off = c->k_off[u] + seq_off;
     wh.v_off = c->v_off[u] + seq_off;
-    wh.window = w;
+    wh.window = (int32_t)w;
+    wh.pto = page_tab_off(c, u, seq);
     wh.k_scale = c->k_scale[u];
     wh.v_scale = c->v_scale[u];
     // slot ranges [lo, hi) written by this chunk
@@ -599,6 +797,8 @@ int hwkv_prefill_write(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0,
     max_tiles = std::max(max_tiles, tot);
   }
   a.cache = c->base;
+  a.page_table = device_page_table(c);
+  a.pool_off = c->pool_off;
   a.k = static_cast<const uint16_t *>(k);
   a.v = static_cast<const uint16_t *>(v);
   a.p0 = p0;
@@ -649,6 +849,7 @@ int hwkv_prefill_attn(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0,
     a.head[h].k_off = c->k_off[u] + seq_off;
     a.head[h].v_off = c->v_off[u] + seq_off;
     a.head[h].window = (int32_t)c->window[u];
+    a.head[h].pto = page_tab_off(c, u, seq);
     const int64_t w = c->window[u];
     work.push_back({w == 0 ? p1 : std::min(p1, (int64_t)p.n_sinks + w), h});
   }
@@ -664,6 +865,8 @@ int hwkv_prefill_attn(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0,
   if (nb * H > (int64_t)INT32_MAX)
     return fail(HWKV_EINVAL, "n_tokens too large for one launch");
   a.cache = reinterpret_cast<const uint16_t *>(c->base);
+  a.page_table = device_page_table(c);
+  a.pool_off = c->pool_off;
   a.q = static_cast<const uint16_t *>(q);
   a.k = static_cast<const uint16_t *>(k);
   a.v = static_cast<const uint16_t *>(v);
@@ -1121,6 +1324,12 @@ int hwkv_append(hwkv_cache *c, int32_t layer, const void *k_new,
       if (c->window[u] == 0 && seq_len(c, layer, b) >= c->cap[u])
         return fail(HWKV_ECAPACITY, "append past max_ctx on a full unit");
     }
+  {
+    std::vector<std::pair<int32_t, int64_t>> want;
+    for (int32_t b = 0; b < B; ++b) want.push_back({b, seq_len(c, layer, b) + 1});
+    const int rc = take_pages(c, layer, want, (hipStream_t)stream);
+    if (rc != HWKV_OK) return rc;
+  }
   const int total = B * H;
   for (int i0 = 0; i0 < total; i0 += hwkv::kMaxItems) {
     const int cnt = std::min(hwkv::kMaxItems, total - i0);
@@ -1137,9 +1346,12 @@ int hwkv_append(hwkv_cache *c, int32_t layer, const void *k_new,
       a.kv_row[j] = b * H + h;
       a.k_scale[j] = c->k_scale[u];
       a.v_scale[j] = c->v_scale[u];
+      a.pto[j] = page_tab_off(c, u, b);
     }
     a.n_items = cnt;
     a.cache = c->base;
+    a.page_table = device_page_table(c);
+    a.pool_off = c->pool_off;
     a.k_new = static_cast<const uint16_t *>(k_new);
     a.v_new = static_cast<const uint16_t *>(v_new);
     const int rc = check_device(
@@ -1229,14 +1441,34 @@ int hwkv_cache_read_unit(const hwkv_cache *c, int32_t layer, int32_t kv_head,
   }
   int rc = check_device(hipDeviceSynchronize(), "synchronize");
   if (rc != HWKV_OK) return rc;
-  rc = check_device(hipMemcpy(tiles.data(), c->base + (c->k_off[u] + seq_off) * E,
-                              (size_t)(capp * D * E), hipMemcpyDeviceToHost),
-                    "copy K");
-  if (rc != HWKV_OK) return rc;
-  rc = check_device(hipMemcpy(host_v, c->base + (c->v_off[u] + seq_off) * E,
-                              (size_t)(cap * D * E), hipMemcpyDeviceToHost),
-                    "copy V");
-  if (rc != HWKV_OK) return rc;
+  const int32_t pto = page_tab_off(c, u, seq);
+  if (pto >= 0) {
+    // paged: page j holds tiles 4j .. 4j + 3 (K) and rows 256 j .. (V)
+    const int64_t PT = hwkv::kPageTokens;
+    const int32_t have = c->held[(size_t)(pto / c->max_pages)];
+    for (int32_t j = 0; j < have; ++j) {
+      const int64_t pg = c->pt_host[(size_t)pto + j];
+      const uint8_t *src = c->base + (c->pool_off + pg * 2 * PT * D) * E;
+      const int64_t rows = std::min(PT, cap - j * PT);
+      rc = check_device(hipMemcpy(tiles.data() + j * PT * D * E, src,
+                                  (size_t)(std::min(PT, capp - j * PT) * D * E),
+                                  hipMemcpyDeviceToHost), "copy K page");
+      if (rc != HWKV_OK) return rc;
+      rc = check_device(hipMemcpy(static_cast<uint8_t *>(host_v) + j * PT * D * E,
+                                  src + PT * D * E, (size_t)(rows * D * E),
+                                  hipMemcpyDeviceToHost), "copy V page");
+      if (rc != HWKV_OK) return rc;
+    }
+  } else {
+    rc = check_device(hipMemcpy(tiles.data(), c->base + (c->k_off[u] + seq_off) * E,
+                                (size_t)(capp * D * E), hipMemcpyDeviceToHost),
+                      "copy K");
+    if (rc != HWKV_OK) return rc;
+    rc = check_device(hipMemcpy(host_v, c->base + (c->v_off[u] + seq_off) * E,
+                                (size_t)(cap * D * E), hipMemcpyDeviceToHost),
+                      "copy V");
+    if (rc != HWKV_OK) return rc;
+  }
   // untile K: [tile][D/8][64][8 elements] -> [slot][D]
   uint8_t *hk = static_cast<uint8_t *>(host_k);
   const int64_t NC = D / 8, LB = 8 * E;

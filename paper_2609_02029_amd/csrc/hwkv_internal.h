@@ -13,6 +13,14 @@
 // cap_pad = cap rounded up to a multiple of 64.  Regions are grouped by
 // window level: for each level, the K regions of its units ([unit][seq]),
 // then their V regions.  Offsets below count elements.
+//
+// Paged caches: full units have no region.  Their rows live in pages of
+// kPageTokens rows of one (unit, sequence) -- the K tiles of the page
+// ([4 tiles][head_dim / 8][64][8]), then its V rows ([256][head_dim]) -- in
+// a pool after the finite units' regions; page j of (unit, sequence) is
+// page_table[pto + j], where pto = (full unit index * batch + sequence) *
+// pages per max_ctx.  One page is one decode split and holds whole prefill
+// key tiles.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -23,6 +31,7 @@ namespace hwkv {
 
 constexpr int kTile = 64;        // token slots per K tile (= wavefront width)
 constexpr int kMaxItems = 64;    // (sequence, kv-head) items per launch
+constexpr int kPageTokens = 256; // rows per page of a paged full unit
 
 // Decode work of one launch: items are (sequence b, kv head h) pairs of one
 // layer; item i owns splits [split_begin[i], split_begin[i + 1]) of the
@@ -36,6 +45,7 @@ struct DecodeItems {
   int32_t kv_row[kMaxItems];     // b * n_kv_heads + h (row of k_new/v_new)
   float k_scale[kMaxItems];      // fp8 scales of the item's unit (else 1)
   float v_scale[kMaxItems];
+  int32_t pto[kMaxItems];        // page-table offset of a paged unit, or -1
   int32_t split_begin[kMaxItems + 1];
   int32_t n_items;
   int32_t ws_split0;             // first partial slot of this launch in ws
@@ -49,6 +59,8 @@ struct DecodeArgs {
   const uint16_t *v_new;
   float *out;                    // [B][Hq][D]
   float *ws;                     // partials [split][G][2 + D]
+  const int32_t *page_table;     // paged caches (else null)
+  int64_t pool_off;              // element offset of page 0
   float scale_log2;              // scale * log2(e)
 };
 
@@ -57,7 +69,8 @@ struct DecodeArgs {
 struct WriteHead {
   int64_t k_off;                 // element offset of the (unit, seq) K tiles
   int64_t v_off;                 // element offset of its V rows
-  int64_t window;                // 0 = full
+  int32_t window;                // 0 = full
+  int32_t pto;                   // page-table offset of a paged unit, or -1
   int32_t tile0[3];
   int32_t n_tiles[3];
   float k_scale, v_scale;        // fp8 scales of the unit (else 1)
@@ -66,6 +79,8 @@ struct WriteHead {
 struct WriteArgs {
   WriteHead head[kMaxItems];     // one per kv head of the layer
   void *cache;
+  const int32_t *page_table;     // paged caches (else null)
+  int64_t pool_off;              // element offset of page 0
   const uint16_t *k;             // [n_tokens][Hkv][D]
   const uint16_t *v;
   int64_t p0, p1;                // chunk [p0, p1)
@@ -80,10 +95,23 @@ struct AppendArgs {
   int32_t kv_row[kMaxItems];
   float k_scale[kMaxItems];
   float v_scale[kMaxItems];
+  int32_t pto[kMaxItems];        // page-table offset of a paged unit, or -1
   int32_t n_items;
   void *cache;
+  const int32_t *page_table;     // paged caches (else null)
+  int64_t pool_off;              // element offset of page 0
   const uint16_t *k_new;
   const uint16_t *v_new;
+};
+
+// Page-table entries to install (table[idx[i]] = page[i]) before the
+// kernels of a call that took new pages read them.
+constexpr int kMaxPageUpdates = 496;
+struct PageUpdateArgs {
+  int32_t *table;
+  int32_t n;
+  int32_t idx[kMaxPageUpdates];
+  int32_t page[kMaxPageUpdates];
 };
 
 // Prefill attention of one chunk [p0, p0 + n_tokens) of one sequence: per
@@ -94,13 +122,15 @@ struct PrefillAttnHead {
   int64_t k_off;                 // element offset of the (unit, seq) K tiles
   int64_t v_off;                 // element offset of its V rows
   int32_t window;                // 0 = full
-  int32_t pad;
+  int32_t pto;                   // page-table offset of a paged unit, or -1
 };
 
 struct PrefillAttnArgs {
   PrefillAttnHead head[kMaxItems];
   int32_t head_order[kMaxItems];
   const uint16_t *cache;         // bf16 caches only
+  const int32_t *page_table;     // paged caches (else null)
+  int64_t pool_off;              // element offset of page 0
   const uint16_t *q;             // [n_tokens][Hq][D]
   const uint16_t *k;             // [n_tokens][Hkv][D]
   const uint16_t *v;
@@ -138,6 +168,7 @@ int decode_combine_blocks_per_item(int D, int G);  // merge workgroups
 hipError_t launch_prefill_write(int fmt, int D, const WriteArgs &a,
                                 int max_tiles, hipStream_t s);
 hipError_t launch_append(int fmt, int D, const AppendArgs &a, hipStream_t s);
+hipError_t launch_page_update(const PageUpdateArgs &a, hipStream_t s);
 int prefill_attn_columns_per_block();   // (token, q head) columns
 hipError_t launch_prefill_attn(int D, const PrefillAttnArgs &a, hipStream_t s,
                               int n_splits = 1);
@@ -172,4 +203,5 @@ hipError_t launch_calib_means(const CalibArgs &a, hipStream_t s);
 static_assert(sizeof(hwkv::DecodeArgs) <= 4096, "decode kernarg too large");
 static_assert(sizeof(hwkv::WriteArgs) <= 4096, "write kernarg too large");
 static_assert(sizeof(hwkv::AppendArgs) <= 4096, "append kernarg too large");
+static_assert(sizeof(hwkv::PageUpdateArgs) <= 4096, "page update kernarg too large");
 static_assert(sizeof(hwkv::PrefillAttnArgs) <= 4096, "prefill kernarg too large");

@@ -250,8 +250,18 @@ void prefill_attn(const PrefillAttnArgs a) {
           off = off % W;                           // tiny windows only
         sl = S + off;
       }
-      kp = kc + (size_t)((sl >> 6) * DC) * (kTile * 8) + (sl & 63) * 8;
-      vp = vc + (size_t)sl * D;
+      if (hd.pto >= 0) {
+        // paged full unit: the tile's 32 keys (s0 is a multiple of 32) lie
+        // in page s0 / 256, at rows sl % 256 of it
+        const int64_t pg = a.page_table[hd.pto + (s0 >> 8)];
+        const uint16_t *pk = a.cache + a.pool_off + pg * 2 * kPageTokens * D;
+        const int sp = sl & (kPageTokens - 1);
+        kp = pk + (size_t)((sp >> 6) * DC) * (kTile * 8) + (sp & 63) * 8;
+        vp = pk + (size_t)kPageTokens * D + (size_t)sp * D;
+      } else {
+        kp = kc + (size_t)((sl >> 6) * DC) * (kTile * 8) + (sl & 63) * 8;
+        vp = vc + (size_t)sl * D;
+      }
       kstep = kTile * 8;
     }
     uint8_t *kl = smem + buf * P::STAGE;

@@ -58,8 +58,17 @@ __global__ __launch_bounds__(256) void prefill_write(WriteArgs a) {
   __syncthreads();
 
   uint8_t *const cache = static_cast<uint8_t *>(a.cache);
-  uint8_t *kt = cache + (wh.k_off + (size_t)tile * kTile * D) * EB;
-  uint8_t *vt = cache + (wh.v_off + (size_t)tile * kTile * D) * EB;
+  uint8_t *kt, *vt;     // this tile's K tile and its first V row
+  if (wh.pto >= 0) {    // paged: tile `tile % 4` of page tile / 4
+    constexpr int TPP = kPageTokens / kTile;
+    const int64_t pg = a.page_table[wh.pto + tile / TPP];
+    const int64_t base = a.pool_off + pg * 2 * kPageTokens * D;
+    kt = cache + (base + (int64_t)(tile % TPP) * kTile * D) * EB;
+    vt = cache + (base + (int64_t)kPageTokens * D + (int64_t)(tile % TPP) * kTile * D) * EB;
+  } else {
+    kt = cache + (wh.k_off + (size_t)tile * kTile * D) * EB;
+    vt = cache + (wh.v_off + (size_t)tile * kTile * D) * EB;
+  }
   const size_t row_stride = (size_t)a.n_kv_heads * D;
   // K: thread -> (chunk g, slot), slot fastest: coalesced tile stores
   for (int e = threadIdx.x; e < kTile * NC; e += 256) {
@@ -93,17 +102,35 @@ __global__ __launch_bounds__(64) void append_token(AppendArgs a) {
   const int slot = a.slot[i];
   const size_t src = (size_t)a.kv_row[i] * D;
   uint8_t *const cache = static_cast<uint8_t *>(a.cache);
+  // the K region and V region holding `slot`, and its row r in them
+  int64_t koff, voff;
+  int r = slot;
+  if (a.pto[i] >= 0) {  // paged: row slot % 256 of page slot / 256
+    const int64_t pg = a.page_table[a.pto[i] + slot / kPageTokens];
+    koff = a.pool_off + pg * 2 * kPageTokens * D;
+    voff = koff + (int64_t)kPageTokens * D;
+    r = slot % kPageTokens;
+  } else {
+    koff = a.k_off[i];
+    voff = a.v_off[i];
+  }
   if (t < NC) {
-    uint8_t *kt = cache + (a.k_off[i] + (size_t)(slot / kTile) * kTile * D) * EB;
+    uint8_t *kt = cache + (koff + (size_t)(r / kTile) * kTile * D) * EB;
     const uint4 val = *reinterpret_cast<const uint4 *>(a.k_new + src + t * 8);
-    store_chunk<F>(kt + ((size_t)t * kTile + slot % kTile) * LB,
+    store_chunk<F>(kt + ((size_t)t * kTile + r % kTile) * LB,
                    encode8<F>(val, a.k_scale[i]));
   } else if (t < 2 * NC) {
     const int g = t - NC;
     const uint4 val = *reinterpret_cast<const uint4 *>(a.v_new + src + g * 8);
-    store_chunk<F>(cache + (a.v_off[i] + (size_t)slot * D) * EB + g * LB,
+    store_chunk<F>(cache + (voff + (size_t)r * D) * EB + g * LB,
                    encode8<F>(val, a.v_scale[i]));
   }
+}
+
+// Installs page-table entries before the kernels that read them (kernels
+// on one stream run in order, so the next launch sees the entries).
+__global__ __launch_bounds__(512) void page_update(PageUpdateArgs a) {
+  for (int i = threadIdx.x; i < a.n; i += 512) a.table[a.idx[i]] = a.page[i];
 }
 
 // Calls L<D, F>::run(args...) for the runtime (D, format).
@@ -151,6 +178,11 @@ hipError_t launch_prefill_write(int fmt, int D, const WriteArgs &a,
 
 hipError_t launch_append(int fmt, int D, const AppendArgs &a, hipStream_t s) {
   return dispatch_df<AppendLaunch>(fmt, D, a, s);
+}
+
+hipError_t launch_page_update(const PageUpdateArgs &a, hipStream_t s) {
+  hipLaunchKernelGGL(page_update, dim3(1), dim3(512), 0, s, a);
+  return hipGetLastError();
 }
 
 }  // namespace hwkv

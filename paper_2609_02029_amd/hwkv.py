@@ -15,6 +15,7 @@ LIB_PATH = os.path.join(_HERE, "_lib", "libhwkv.so")
 OK, EINVAL, ENOMEM, ECAPACITY, ESTATE, EDEVICE = 0, 1, 2, 3, 4, 5
 # cache formats (HWKV_KV_*): name -> (code, bytes per element)
 KV_FORMATS = {"bf16": (0, 2), "f16": (1, 2), "fp8": (2, 1)}
+PAGE_TOKENS = 256   # rows per page of a paged cache's full units
 _NAMES = {EINVAL: "EINVAL", ENOMEM: "ENOMEM", ECAPACITY: "ECAPACITY",
           ESTATE: "ESTATE", EDEVICE: "EDEVICE"}
 
@@ -45,6 +46,11 @@ SYMBOLS = {
     "hwkv_cache_alloc_format": ([_P(_vp), _vp, _i32, _i64, _i32, _vp, _vp, _vp, _sz],
                                 ctypes.c_int),
     "hwkv_cache_format": ([_vp, _P(_i32), _vp, _vp], ctypes.c_int),
+    "hwkv_cache_bytes_paged": ([_vp, _i32, _i64, _i32, _i64, _P(_sz)], ctypes.c_int),
+    "hwkv_cache_alloc_paged": ([_P(_vp), _vp, _i32, _i64, _i32, _vp, _vp, _i64, _vp, _sz],
+                               ctypes.c_int),
+    "hwkv_cache_pages": ([_vp, _P(_i64), _P(_i64)], ctypes.c_int),
+    "hwkv_cache_reset_seq": ([_vp, _i32], ctypes.c_int),
     "hwkv_cache_bytes": ([_vp, _i32, _i64, _P(_sz)], ctypes.c_int),
     "hwkv_cache_alloc": ([_P(_vp), _vp, _i32, _i64, _vp, _sz], ctypes.c_int),
     "hwkv_cache_free": ([_vp], ctypes.c_int),
@@ -194,10 +200,16 @@ def policy_rate(policy, ctx):
 # ---------------------------------------------------------------------------
 # cache
 # ---------------------------------------------------------------------------
-def cache_bytes(policy, batch, max_ctx, kv_format="bf16"):
+def cache_bytes(policy, batch, max_ctx, kv_format="bf16", n_pages=None):
+    """Device bytes of a cache; ``n_pages`` (not None): a paged cache with a
+    pool of that many pages."""
     r = _sz()
-    _check(_lib.hwkv_cache_bytes_format(policy.handle, batch, max_ctx, _fmt_code(kv_format),
-                                        ctypes.byref(r)))
+    if n_pages is None:
+        _check(_lib.hwkv_cache_bytes_format(policy.handle, batch, max_ctx,
+                                            _fmt_code(kv_format), ctypes.byref(r)))
+    else:
+        _check(_lib.hwkv_cache_bytes_paged(policy.handle, batch, max_ctx,
+                                           _fmt_code(kv_format), n_pages, ctypes.byref(r)))
     return r.value
 
 
@@ -212,10 +224,11 @@ def _scales(policy, x):
 
 
 def cache_alloc(policy, batch, max_ctx, dev_buf=None, kv_format="bf16", k_scale=None,
-                v_scale=None):
+                v_scale=None, n_pages=None):
     """``dev_buf``: optional uint8 device tensor to adopt (kept alive).
     ``kv_format``: "bf16", "f16" or "fp8"; ``k_scale``/``v_scale``: fp8 scales,
-    a scalar or ``[n_layers, n_kv_heads]`` (None = 1.0)."""
+    a scalar or ``[n_layers, n_kv_heads]`` (None = 1.0).  ``n_pages`` (not
+    None): full units are paged from a pool of that many pages."""
     h = _vp()
     ptr = None
     nbytes = 0
@@ -224,14 +237,29 @@ def cache_alloc(policy, batch, max_ctx, dev_buf=None, kv_format="bf16", k_scale=
         nbytes = dev_buf.numel()
     ks = _scales(policy, k_scale)
     vs = _scales(policy, v_scale)
-    _check(_lib.hwkv_cache_alloc_format(
-        ctypes.byref(h), policy.handle, batch, max_ctx, _fmt_code(kv_format),
-        None if ks is None else ks.ctypes.data_as(_vp),
-        None if vs is None else vs.ctypes.data_as(_vp), ptr, nbytes))
+    kp = None if ks is None else ks.ctypes.data_as(_vp)
+    vp = None if vs is None else vs.ctypes.data_as(_vp)
+    if n_pages is None:
+        _check(_lib.hwkv_cache_alloc_format(ctypes.byref(h), policy.handle, batch, max_ctx,
+                                            _fmt_code(kv_format), kp, vp, ptr, nbytes))
+    else:
+        _check(_lib.hwkv_cache_alloc_paged(ctypes.byref(h), policy.handle, batch, max_ctx,
+                                           _fmt_code(kv_format), kp, vp, n_pages, ptr, nbytes))
     c = Cache(h, policy.n_layers, policy.n_kv_heads, policy.n_q_heads, policy.head_dim, batch)
     c.dev_buf = dev_buf
     c.kv_format = kv_format
     return c
+
+
+def cache_pages(cache):
+    """(pool pages, free pages) of a paged cache; (0, 0) otherwise."""
+    t, f = _i64(), _i64()
+    _check(_lib.hwkv_cache_pages(cache.handle, ctypes.byref(t), ctypes.byref(f)))
+    return t.value, f.value
+
+
+def cache_reset_seq(cache, seq):
+    _check(_lib.hwkv_cache_reset_seq(cache.handle, seq))
 
 
 def cache_format(cache):

@@ -52,7 +52,8 @@ class Run:
     (large workloads) instead of on the host."""
 
     def __init__(self, cfg, dev="cuda:0", fused=True, track=None, device_gen=False,
-                 levels=None, prompts=None, kv_format="bf16", k_scale=None, v_scale=None):
+                 levels=None, prompts=None, kv_format="bf16", k_scale=None, v_scale=None,
+                 n_pages=None):
         self.cfg = cfg
         self.kv_format = kv_format
         self.dev = torch.device(dev)
@@ -73,7 +74,8 @@ class Run:
         self.pol = hwkv.policy_set(self.L, self.Hkv, self.Hq, self.D, self.S,
                                    c["level_windows"], self.levels)
         self.cache = hwkv.cache_alloc(self.pol, self.B, self.max_ctx, kv_format=kv_format,
-                                      k_scale=k_scale, v_scale=v_scale)
+                                      k_scale=k_scale, v_scale=v_scale, n_pages=n_pages)
+        self.gen = [0] * self.B      # refills of each sequence (seeds its new data)
         # per-unit fp8 scales as the library holds them (1.0 otherwise)
         _, self.k_scale, self.v_scale = hwkv.cache_format(self.cache)
         self.ws = torch.zeros(hwkv.decode_workspace_bytes(self.cache), dtype=torch.uint8,
@@ -96,9 +98,21 @@ class Run:
         return up(a, self.dev), a
 
     def prompt_kv(self, layer, b, P):
-        k, kh = self._kv((P, self.Hkv, self.D), layer, W.K, b)
-        v, vh = self._kv((P, self.Hkv, self.D), layer, W.V, b)
+        idx = b + 1000 * self.gen[b]
+        k, kh = self._kv((P, self.Hkv, self.D), layer, W.K, idx)
+        v, vh = self._kv((P, self.Hkv, self.D), layer, W.V, idx)
         return k, v, kh, vh
+
+    def reset(self, b):
+        """Release sequence b (hwkv_cache_reset_seq); its next prompt is drawn
+        from new seeds."""
+        hwkv.cache_reset_seq(self.cache, b)
+        self.n[:, b] = 0
+        self.gen[b] += 1
+        for l in self.track:
+            if self.kh[l][b] is not None:
+                self.kh[l][b][:] = 0
+                self.vh[l][b][:] = 0
 
     def prompt_q(self, layer, b, P):
         """Queries of the prompt tokens, [P, Hq, D] (device, host or None)."""

@@ -1,0 +1,218 @@
+"""GPU parity of paged full-unit storage (pages of 256 rows from a pool).
+
+A paged cache must give exactly what an unpaged one gives: residency
+bit-exact against the oracle's slot table, decode and prefill-attention
+outputs within the bars of the unpaged tests.  Pages are taken as sequences
+grow (prefill chunks and appends crossing page boundaries), returned by a
+sequence reset and reused by other sequences; a call the pool cannot serve
+fails with ENOMEM and changes nothing.
+"""
+import numpy as np
+import pytest
+import torch
+
+from hwkv_harness import REL_TOL, Run, log, rel_err, up
+from paper_2609_02029_amd import hwkv
+
+pytestmark = pytest.mark.gpu
+
+PT = hwkv.PAGE_TOKENS
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.set_device(0)
+
+
+def mini(**kw):
+    c = dict(name="mini", seed=41, n_layers=2, batch=3, n_q_heads=8, n_kv_heads=2,
+             head_dim=64, n_sinks=4, level_windows=[96, 0], levels=[[0, 1], [1, 1]],
+             prompt=[255, 700, 1], steps=4, max_ctx=1200)
+    c.update(kw)
+    return c
+
+
+def pages_in_use(r):
+    """Pages the full units hold: ceil(n / 256) per full unit and sequence."""
+    tot = 0
+    for l in range(r.L):
+        for h in range(r.Hkv):
+            if r.windows[l][h] == 0 or r.S + r.windows[l][h] >= r.max_ctx:
+                tot += int(sum((int(n) + PT - 1) // PT for n in r.n[l]))
+    return tot
+
+
+def check_pages(r, n_pages):
+    total, free = hwkv.cache_pages(r.cache)
+    assert total == n_pages
+    assert free == n_pages - pages_in_use(r), (free, n_pages, pages_in_use(r))
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "fp8"])
+def test_paged_matches_oracle_across_page_boundaries(fmt):
+    cfg = mini()
+    kw = {} if fmt == "bf16" else dict(k_scale=0.02, v_scale=0.015)
+    r = Run(cfg, n_pages=64, kv_format=fmt, **kw)
+    for l in range(2):
+        for b in range(3):
+            r.prefill(l, b, chunks=[100, 256] if b == 1 else None)
+        r.check_layer(l)
+    check_pages(r, 64)
+    worst = 0.0
+    for st in range(6):             # 255 -> 261 and 1 -> 7 rows: the first crosses a page
+        for l in range(2):
+            qa, out = r.step(l, fused=bool((st + l) % 2))
+            worst = max(worst, r.check_out(l, qa, out, f"{fmt} layer {l} step {st}"))
+            r.check_layer(l)
+        check_pages(r, 64)
+    log(f"paged {fmt}: max rel err {worst:.3e}")
+    r.free()
+
+
+def test_paged_equals_unpaged_bitwise_residency_and_outputs():
+    cfg = mini(head_dim=128, n_q_heads=12, n_kv_heads=2, prompt=[513, 256, 1024],
+               levels=[[1, 0], [1, 1]], max_ctx=1100)
+    a = Run(cfg, n_pages=40)
+    b = Run(cfg)
+    for l in range(2):
+        for s in range(3):
+            a.prefill(l, s)
+            b.prefill(l, s)
+    for st in range(3):
+        for l in range(2):
+            qa, oa = a.step(l, fused=bool(st % 2))
+            _, ob = b.step(l, fused=bool(st % 2))
+            torch.cuda.synchronize()
+            # same arithmetic in the same order: identical outputs
+            assert torch.equal(oa, ob), f"layer {l} step {st}"
+    for l in range(2):
+        for s in range(3):
+            for h in range(2):
+                ka, va, na = hwkv.cache_read_unit(a.cache, l, h, s)
+                kb, vb, nb = hwkv.cache_read_unit(b.cache, l, h, s)
+                assert na == nb
+                assert np.array_equal(ka[:na], kb[:nb]) and np.array_equal(va[:na], vb[:nb])
+    a.free()
+    b.free()
+
+
+def test_reset_returns_pages_and_refill_reuses_them():
+    cfg = mini(prompt=[600, 900, 300])
+    r = Run(cfg, n_pages=30)       # 3 full units x 9 pages at most; freed pages are taken first
+    for l in range(2):
+        for b in range(3):
+            r.prefill(l, b)
+    check_pages(r, 30)
+    for st in range(2):
+        for l in range(2):
+            qa, out = r.step(l)
+            r.check_out(l, qa, out, f"before reset step {st}")
+    # release sequence 1, refill it with new data of another length; the
+    # freed pages now hold other rows, and nothing of the old rows may leak
+    r.reset(1)
+    check_pages(r, 30)
+    for l in range(2):
+        r.prefill(l, 1, P=1000)
+        r.check_layer(l)
+    check_pages(r, 30)
+    for st in range(3):
+        for l in range(2):
+            qa, out = r.step(l, fused=bool(st % 2))
+            r.check_out(l, qa, out, f"after refill step {st}")
+            r.check_layer(l)
+    check_pages(r, 30)
+    r.free()
+
+
+def test_exhausted_pool_is_enomem_and_changes_nothing():
+    # one full unit (layer 0 head 1), one sequence, a pool of 2 pages
+    cfg = mini(n_layers=1, batch=1, levels=[[0, 1]], prompt=[500], max_ctx=2000)
+    r = Run(cfg, n_pages=2)
+    dev = torch.device("cuda:0")
+    k, v, _, _ = r.prompt_kv(0, 0, 600)
+    with pytest.raises(hwkv.HwkvError) as e:        # 600 rows need 3 pages
+        hwkv.prefill_write(r.cache, 0, 0, 0, k, v)
+    assert e.value.code == hwkv.ENOMEM
+    assert hwkv.cache_seq_len(r.cache, 0, 0) == 0
+    assert hwkv.cache_pages(r.cache) == (2, 2)
+    r.prefill(0, 0, P=512)                          # exactly 2 pages
+    assert hwkv.cache_pages(r.cache) == (2, 0)
+    r.check_layer(0)
+    kn = torch.zeros((1, 2, 64), dtype=torch.bfloat16, device=dev)
+    q = torch.zeros((1, 8, 64), dtype=torch.bfloat16, device=dev)
+    out = torch.zeros((1, 8, 64), dtype=torch.float32, device=dev)
+    for call in (lambda: hwkv.append(r.cache, 0, kn, kn),
+                 lambda: hwkv.append_decode_attn(r.cache, 0, kn, kn, q, 0.125, out, r.ws)):
+        with pytest.raises(hwkv.HwkvError) as e:    # row 512 needs a third page
+            call()
+        assert e.value.code == hwkv.ENOMEM
+        assert hwkv.cache_seq_len(r.cache, 0, 0) == 512
+    r.check_layer(0)
+    # decode without an append needs no page
+    qa, out = None, torch.empty((1, 8, 64), dtype=torch.float32, device=dev)
+    hwkv.decode_attn(r.cache, 0, q, 0.125, out, r.ws)
+    torch.cuda.synchronize()
+    assert np.all(np.isfinite(out.cpu().numpy()))
+    r.free()
+
+
+def test_paged_prefill_attention_reads_pages():
+    cfg = mini(n_layers=1, batch=2, head_dim=128, n_q_heads=12, n_kv_heads=2,
+               level_windows=[200, 0], levels=[[0, 1]], prompt=[1300, 700], max_ctx=1400,
+               seed=43)
+    r = Run(cfg, n_pages=20)
+    worst = 0.0
+    for b in range(2):
+        chunks = [1, 256, 300, 777] if b == 0 else [511, 512]
+        q, qh, out = r.prefill_with_attn(0, b, chunks=chunks)
+        torch.cuda.synchronize()
+        P = r.prompts[b]
+        rows = np.unique(np.concatenate([np.arange(0, P, 37), [P - 1, 255, 256, 511, 512]]))
+        rows = rows[rows < P]
+        ref = r.oracle_rows(0, b, rows, qh[rows])
+        got = out.cpu().numpy()[rows]
+        e = rel_err(got.reshape(-1, r.D), ref.reshape(-1, r.D))
+        assert e <= REL_TOL, f"sequence {b}: max rel err {e}"
+        worst = max(worst, e)
+    r.check_layer(0)
+    check_pages(r, 20)
+    log(f"paged prefill attention: max rel err {worst:.3e}")
+    r.free()
+
+
+# ---------------------------------------------------------------------------
+# batched serving at full size (16 ragged sequences of 16K..64K, 8 layers,
+# 64 steps) from a pool sized to exactly the final lengths
+# ---------------------------------------------------------------------------
+@pytest.mark.timeout(1200)
+def test_batch16_paged_full_size():
+    import workloads as W
+    from hwkv_harness import timed
+    cfg = W.CONFIGS["batch16"]
+    track = [0, 5]
+    prompts = W.prompts(cfg)
+    wins = W.windows_of(cfg)
+    full = sum(1 for l in range(cfg["n_layers"]) for h in range(cfg["n_kv_heads"])
+               if wins[l][h] == 0 or cfg["n_sinks"] + wins[l][h] >= cfg["max_ctx"])
+    n_pages = full * sum((p + cfg["steps"] + PT - 1) // PT for p in prompts)
+    r = Run(cfg, track=track, device_gen=True, n_pages=n_pages)
+    with timed("batch16 paged prefill"):
+        for l in range(cfg["n_layers"]):
+            for b in range(cfg["batch"]):
+                r.prefill(l, b)
+            if l in track:
+                r.check_layer(l)
+    worst = 0.0
+    with timed("batch16 paged 64 steps x 8 layers"):
+        for st in range(cfg["steps"]):
+            for l in range(cfg["n_layers"]):
+                qa, out = r.step(l)
+                if st in (0, cfg["steps"] - 1) and l in track:
+                    worst = max(worst, r.check_out(l, qa, out, f"batch16 paged layer {l} step {st}"))
+    for l in track:
+        r.check_layer(l)
+    assert hwkv.cache_pages(r.cache) == (n_pages, 0)      # the pool is used exactly
+    log(f"batch16 paged: {n_pages} pages, max rel err {worst:.3e}")
+    r.free()

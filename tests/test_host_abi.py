@@ -473,3 +473,72 @@ def test_format_alloc_validation(hw):
     rc = hw._lib.hwkv_prefill_attn(h, 0, 0, 0, 4, FAKE, FAKE, FAKE, 0.1, FAKE, None)
     assert rc == hw.EINVAL and "bf16" in hw.last_error()
     hw._lib.hwkv_cache_free(h)
+
+
+# --------------------------------------------------------------------------
+# paged full units
+# --------------------------------------------------------------------------
+def _r256(x):
+    return (x + 255) // 256 * 256
+
+
+def test_paged_cache_bytes(hw):
+    r = np.random.default_rng(5)
+    for _ in range(40):
+        L, H, D = int(r.integers(1, 4)), int(r.choice([1, 2, 4])), int(r.choice([64, 128, 256]))
+        lw = [int(x) for x in r.integers(1, 3000, size=3)] + [0]
+        lv = r.integers(0, 4, size=(L, H))
+        S = int(r.integers(0, 8))
+        B = int(r.integers(1, 5))
+        ctx = int(r.integers(1, 6000))
+        n_pages = int(r.integers(0, 50))
+        fmt, b = [("bf16", 2), ("f16", 2), ("fp8", 1)][int(r.integers(0, 3))]
+        p = hw.policy_set(L, H, H, D, S, lw, lv.tolist())
+        finite, n_full = 0, 0
+        for w in np.array(lw)[lv].ravel():
+            if w == 0 or S + w >= ctx:
+                n_full += 1
+            else:
+                finite += B * ((S + int(w) + 63) // 64 * 64) * D * 2 * b
+        exp = _r256(_r256(finite) + n_pages * 2 * 256 * D * b) + n_full * B * ((ctx + 255) // 256) * 4
+        assert hw.cache_bytes(p, B, ctx, fmt, n_pages=n_pages) == exp
+        # with no full unit and no pool, only the 256-byte rounding remains
+        if n_full == 0 and n_pages == 0:
+            assert hw.cache_bytes(p, B, ctx, fmt, n_pages=0) == _r256(hw.cache_bytes(p, B, ctx, fmt))
+    p = _pol(hw)
+    for bad in (-1, 1 << 31):
+        with pytest.raises(hw.HwkvError):
+            hw.cache_bytes(p, 1, 300, n_pages=bad)
+
+
+def _fake_paged(hw, p, B, max_ctx, n_pages):
+    h = ctypes.c_void_p()
+    nbytes = hw.cache_bytes(p, B, max_ctx, n_pages=n_pages)
+    rc = hw._lib.hwkv_cache_alloc_paged(ctypes.byref(h), p.handle, B, max_ctx, 0, None, None,
+                                        n_pages, FAKE, nbytes)
+    assert rc == hw.OK, hw.last_error()
+    return h
+
+
+def test_paged_pool_checks_before_device_work(hw):
+    p = _pol(hw)                        # 2 layers x 2 kv heads: one full unit per layer
+    L = hw._lib
+    h = _fake_paged(hw, p, 2, 1000, 1)
+    t, f = ctypes.c_int64(), ctypes.c_int64()
+    assert L.hwkv_cache_pages(h, ctypes.byref(t), ctypes.byref(f)) == hw.OK
+    assert (t.value, f.value) == (1, 1)
+    # 300 rows of the full unit need 2 pages: ENOMEM before any launch
+    assert L.hwkv_prefill_write(h, 0, 0, 0, 300, FAKE, FAKE, None) == hw.ENOMEM
+    assert "page" in hw.last_error()
+    n = ctypes.c_int64()
+    assert L.hwkv_cache_seq_len(h, 0, 0, ctypes.byref(n)) == hw.OK and n.value == 0
+    assert L.hwkv_cache_pages(h, ctypes.byref(t), ctypes.byref(f)) == hw.OK and f.value == 1
+    assert L.hwkv_cache_reset_seq(h, 1) == hw.OK
+    assert L.hwkv_cache_reset_seq(h, 2) == hw.EINVAL
+    assert L.hwkv_cache_reset_seq(h, -1) == hw.EINVAL
+    L.hwkv_cache_free(h)
+    # an unpaged cache reports no pool
+    h = _fake_cache(hw, p, 1, 300)
+    assert L.hwkv_cache_pages(h, ctypes.byref(t), ctypes.byref(f)) == hw.OK
+    assert (t.value, f.value) == (0, 0)
+    L.hwkv_cache_free(h)
