@@ -109,6 +109,7 @@ typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
 typedef const __attribute__((address_space(4))) u32x4_t cu32x4_t;
 
 __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
@@ -164,6 +165,13 @@ template <bool HI>
 __device__ __forceinline__ uint32_t fp8x2_bf16x2(uint32_t w) {
   return __builtin_bit_cast(uint32_t,
                             __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, HI));
+}
+
+// fp8 codes 2i, 2i + 1 of a word as one binary16 pair (exact: every E4M3
+// value is a binary16 value), low code first.
+template <bool HI>
+__device__ __forceinline__ f16x2_t fp8x2_f16x2(uint32_t w) {
+  return __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w, 1.0f, HI);
 }
 
 // The 8 elements of a V chunk widened to fp32 (exact for every format).
@@ -251,6 +259,12 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
   // 8-byte loads keep twice as many in flight, for the same bytes.
   constexpr int PFW = EB == 2 ? kPrefetch : kPrefetch8;
   constexpr int PF = PFW < NC ? PFW : NC;
+  // fp8 values: p.v over token pairs with v_dot2_f32_f16 -- a lane's two
+  // consecutive p.v steps read rows r and r + RPS of the same channels, whose
+  // codes widen exactly to binary16 pairs; the weights enter the product
+  // rounded to binary16 (the normaliser keeps the fp32 weights)
+  constexpr bool PAIR = F == HWKV_KV_FP8_E4M3;
+  static_assert(NC % 2 == 0, "p.v steps come in pairs");
   static_assert((2 * NC) % PF == 0, "prefetch depth must divide 2 NC");
   __shared__ SplitSmem<D, G> sm;
 
@@ -442,6 +456,10 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
 
     // ---- online softmax, base 2 (the first V loads are already in flight)
     const bool valid = slot < nv;
+    // token-pair order of the binary16 weights: token t is half (t / RPS) % 2
+    // of pair (t / 2 RPS) RPS + t % RPS, whose G weights are G dwords
+    const int ppid = (lane / (2 * RPS)) * RPS + lane % RPS;
+    const int phalf = (lane / RPS) & 1;
 #pragma unroll
     for (int h = 0; h < G; ++h) {
       const float z = valid ? s[h] * zscale : -INFINITY;
@@ -455,7 +473,10 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
       }
       const float p = exp2f(z - mnew);
       l[h] += p;
-      pl[lane * PST + h] = p;
+      if constexpr (PAIR)
+        reinterpret_cast<_Float16 *>(pl)[2 * (ppid * G + h) + phalf] = (_Float16)p;
+      else
+        pl[lane * PST + h] = p;
     }
 
     // ---- p.v, one step of RPS rows per step; lanes own channels 8 c8 ..
@@ -468,6 +489,49 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
         if (has_next) buf[j % PF] = bload_chunk<F>(krs, kofs_n + (jn - 2 * NC) * 64 * LB);
       }
     };
+    if constexpr (PAIR) {
+      // steps 2s and 2s + 1 read rows r = rsub + 2s RPS and r + RPS: the
+      // first step keeps its chunk and reads the pair's weights (so the LDS
+      // latency overlaps a step), the second builds the binary16 pairs
+      // (v_r[c], v_r+RPS[c]) and takes one v_dot2 per (head, channel)
+      const uint32_t *pp = reinterpret_cast<const uint32_t *>(pl);
+      int pofs = rsub * G;
+      uint32_t pw[G];
+      Chunk xp;
+      static_for<NC>([&](auto jc) {
+        constexpr int js = decltype(jc)::value;
+        constexpr int j = NC + js;
+#pragma unroll
+        for (int h = 0; h < G; ++h)
+#pragma unroll
+          for (int e = 0; e < 8; e += 2)
+            asm volatile("" : "+v"(acc[h][e]), "+v"(acc[h][e + 1]));
+        asm volatile("" : "+v"(vofs), "+v"(kofs_n), "+v"(pofs));
+        const Chunk x = buf[j % PF];
+        issue(std::integral_constant<int, j>{});
+        if constexpr (js % 2 == 0) {
+          xp = x;
+#pragma unroll
+          for (int h = 0; h < G; ++h) pw[h] = pp[pofs + (js / 2) * RPS * G + h];
+        } else {
+          const uint32_t w0 = __builtin_amdgcn_perm(x.x, xp.x, 0x05010400u);
+          const uint32_t w1 = __builtin_amdgcn_perm(x.x, xp.x, 0x07030602u);
+          const uint32_t w2 = __builtin_amdgcn_perm(x.y, xp.y, 0x05010400u);
+          const uint32_t w3 = __builtin_amdgcn_perm(x.y, xp.y, 0x07030602u);
+          const f16x2_t v[8] = {fp8x2_f16x2<false>(w0), fp8x2_f16x2<true>(w0),
+                                fp8x2_f16x2<false>(w1), fp8x2_f16x2<true>(w1),
+                                fp8x2_f16x2<false>(w2), fp8x2_f16x2<true>(w2),
+                                fp8x2_f16x2<false>(w3), fp8x2_f16x2<true>(w3)};
+#pragma unroll
+          for (int h = 0; h < G; ++h) {
+            const f16x2_t ph = __builtin_bit_cast(f16x2_t, pw[h]);
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              acc[h][e] = __builtin_amdgcn_fdot2(ph, v[e], acc[h][e], false);
+          }
+        }
+      });
+    } else {
     // p of a step's rows is read from LDS one step ahead (pc: this step,
     // pn: the next), so the LDS latency overlaps a step of work.
     int pofs = rsub * PST;
@@ -501,6 +565,7 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
         for (int h = 0; h < G; ++h) pc[h] = pn[h];
       }
     });
+    }
     t = tn;
     kofs = kofs_n;
   }

@@ -991,6 +991,7 @@ int hwkv_calib_replay(int32_t n_kv_heads, int32_t n_q_heads, int32_t head_dim,
         (max_tiles + hwkv::kReplayTilesPerSplit - 1) / hwkv::kReplayTilesPerSplit;
     for (int32_t h = 0; h < n_kv_heads; ++h) {
       a.head[h].window = (int32_t)w;
+      a.head[h].pto = -1;          // no cache: every key comes from the trace
       a.head_order[h] = h;
     }
     a.q = static_cast<const uint16_t *>(q);
