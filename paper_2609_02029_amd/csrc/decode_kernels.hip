@@ -16,23 +16,33 @@ extern template hipError_t launch_decode_split_fmt<HWKV_KV_FP8_E4M3>(
 namespace {
 
 // One workgroup per (item, query head of the group, kCombineChan-channel
-// chunk).  Thread (r, c) merges channel c of splits r, r + R, r + 2R, ...
-// (R = rows of the workgroup); each round issues the loads of kCombineUnroll
-// splits before using any of them, so a round costs one memory round trip.
-// The rows are then merged in LDS.  The merge is a kernel of its own:
-// ordering the partials of other workgroups inside the split kernel would
-// need device-scope fences, which write back and invalidate the L2 under
-// every workgroup's stream.
+// chunk).  Its threads are R rows of kCombineChan / 4 lanes, a lane owning 4
+// channels (one 16-byte load per split, so a row reads whole 128-byte
+// lines).  Thread (r, q) merges its channels over splits r, r + R, r + 2R,
+// ...; each round issues the loads of kCombineUnroll splits before using any
+// of them, so a round costs one memory round trip, and R * kCombineUnroll
+// splits (512) fit in one round.  The rows are then merged: the common
+// shift through LDS, the weighted sums across the rows of a wavefront by
+// lane shuffles, and across the wavefronts in LDS.  The merge is a
+// kernel of its own: ordering the partials of other workgroups inside the
+// split kernel would need device-scope fences, which write back and
+// invalidate the L2 under every workgroup's stream.
 template <int D, int G>
 __global__ __launch_bounds__(kCombineThreads) void decode_combine(
     DecodeArgs a) {
   constexpr int CW = kCombineChan < D ? kCombineChan : D;
   constexpr int CH = D / CW;
-  constexpr int R = kCombineThreads / CW;
+  constexpr int LPR = CW / 4;                     // lanes per row
+  constexpr int R = kCombineThreads / LPR;        // rows
   constexpr int PS = G * (D + 2);
   constexpr int U = kCombineUnroll;
-  __shared__ float sM[R], sL[R];
-  __shared__ float sA[R][CW];
+  // 16-byte partial loads need the acc block 16-byte aligned: G even
+  constexpr bool VEC = (2 * G) % 4 == 0;
+  constexpr int NWV = kCombineThreads / 64;      // wavefronts
+  static_assert(R <= 64, "the row shifts are reduced by one wavefront");
+  static_assert(64 % LPR == 0, "a row lies within one wavefront");
+  __shared__ float sM[R], sL[NWV], sMx;
+  __shared__ float4 sA[NWV][LPR];
   const DecodeItems &it = a.it;
   const int bid = blockIdx.x;
   const int item = bid / (G * CH);
@@ -42,20 +52,27 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine(
   const int sb = it.split_begin[item];
   const int ns = it.split_begin[item + 1] - sb;
   if (ns <= 1) return;
-  const int r = threadIdx.x / CW, cl = threadIdx.x % CW;
-  const int c = ch * CW + cl;
+  const int tid = threadIdx.x;
+  const int r = tid / LPR, q = tid % LPR;
+  const int c = ch * CW + 4 * q;
   const float *base = a.ws + (size_t)(it.ws_split0 + sb) * PS;
 
-  float M = -INFINITY, L = 0.f, A = 0.f;
+  float M = -INFINITY, L = 0.f;
+  float4 A = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int j0 = r; j0 < ns; j0 += R * U) {
-    float mj[U], lj[U], aj[U];
+    float mj[U], lj[U];
+    float4 aj[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {  // every load of the round is in flight
       const int j = min(j0 + u * R, ns - 1);
       const float *pj = base + (size_t)j * PS;
       mj[u] = pj[h];
       lj[u] = pj[G + h];
-      aj[u] = pj[2 * G + h * D + c];
+      const float *pa = pj + 2 * G + h * D + c;
+      if constexpr (VEC)
+        aj[u] = *reinterpret_cast<const float4 *>(pa);
+      else
+        aj[u] = make_float4(pa[0], pa[1], pa[2], pa[3]);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u)
@@ -65,31 +82,69 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine(
     for (int u = 0; u < U; ++u) Mn = fmaxf(Mn, mj[u]);
     const float f = exp2f(M - Mn);
     L *= f;
-    A *= f;
+    A.x *= f;
+    A.y *= f;
+    A.z *= f;
+    A.w *= f;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const float e = exp2f(mj[u] - Mn);
       L += lj[u] * e;
-      A += aj[u] * e;
+      A.x += aj[u].x * e;
+      A.y += aj[u].y * e;
+      A.z += aj[u].z * e;
+      A.w += aj[u].w * e;
     }
     M = Mn;
   }
-  if (cl == 0) {
-    sM[r] = M;
-    sL[r] = L;
-  }
-  sA[r][cl] = A;
+  // rows: the common shift max_r M_r (row 0 always has a split, ns >= 2);
+  // rows without a split have M_r = -inf, weight 0 and zero sums
+  if (q == 0) sM[r] = M;
   __syncthreads();
-  if (threadIdx.x < CW) {
-    float Mx = sM[0];
-    for (int w = 1; w < R; ++w) Mx = fmaxf(Mx, sM[w]);
-    float Lx = 0.f, Ax = 0.f;
-    for (int w = 0; w < R; ++w) {
-      const float f = exp2f(sM[w] - Mx);
-      Lx += sL[w] * f;
-      Ax += sA[w][threadIdx.x] * f;
+  if (tid < 64) {
+    float mx = tid < R ? sM[tid] : -INFINITY;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+    if (tid == 0) sMx = mx;
+  }
+  __syncthreads();
+  const float f = (M == -INFINITY) ? 0.f : exp2f(M - sMx);
+  L *= f;
+  A.x *= f;
+  A.y *= f;
+  A.z *= f;
+  A.w *= f;
+  // sum over the rows of a wavefront (lanes q, q + LPR, ...), then over the
+  // wavefronts in LDS
+#pragma unroll
+  for (int off = LPR; off < 64; off <<= 1) {
+    L += __shfl_xor(L, off);
+    A.x += __shfl_xor(A.x, off);
+    A.y += __shfl_xor(A.y, off);
+    A.z += __shfl_xor(A.z, off);
+    A.w += __shfl_xor(A.w, off);
+  }
+  const int wv = tid >> 6, lane = tid & 63;
+  if (lane < LPR) {
+    sA[wv][lane] = A;
+    if (lane == 0) sL[wv] = L;
+  }
+  __syncthreads();
+  if (tid < LPR) {
+    float Lx = 0.f;
+    float4 Ax = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int w = 0; w < NWV; ++w) {
+      const float4 x = sA[w][tid];
+      Lx += sL[w];
+      Ax.x += x.x;
+      Ax.y += x.y;
+      Ax.z += x.z;
+      Ax.w += x.w;
     }
-    a.out[((size_t)it.q_row[item] + h) * D + c] = Ax / Lx;
+    const float inv = 1.0f / Lx;
+    *reinterpret_cast<float4 *>(&a.out[((size_t)it.q_row[item] + h) * D + ch * CW + 4 * tid]) =
+        make_float4(Ax.x * inv, Ax.y * inv, Ax.z * inv, Ax.w * inv);
   }
 }
 

@@ -99,11 +99,11 @@ static_assert(kWaves * kTilesPerWave * kTile == kPageTokens && kTilesPerWave == 
 #define HWKV_COMBINE_CHAN 32
 #endif
 #ifndef HWKV_COMBINE_UNROLL
-#define HWKV_COMBINE_UNROLL 16
+#define HWKV_COMBINE_UNROLL 8
 #endif
 constexpr int kCombineThreads = HWKV_COMBINE_THREADS;  // per merge workgroup
 constexpr int kCombineChan = HWKV_COMBINE_CHAN;        // channels per workgroup
-constexpr int kCombineUnroll = HWKV_COMBINE_UNROLL;  // splits per wave per round
+constexpr int kCombineUnroll = HWKV_COMBINE_UNROLL;  // splits per thread per round
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
