@@ -15,6 +15,20 @@ extern template hipError_t launch_decode_split_fmt<HWKV_KV_FP8_E4M3>(
 
 namespace {
 
+// Merge geometry (compile-time).
+#ifndef HWKV_COMBINE_THREADS
+#define HWKV_COMBINE_THREADS 512
+#endif
+#ifndef HWKV_COMBINE_CHAN
+#define HWKV_COMBINE_CHAN 32
+#endif
+#ifndef HWKV_COMBINE_UNROLL
+#define HWKV_COMBINE_UNROLL 8
+#endif
+constexpr int kCombineThreads = HWKV_COMBINE_THREADS;  // per merge workgroup
+constexpr int kCombineChan = HWKV_COMBINE_CHAN;        // channels per workgroup
+constexpr int kCombineUnroll = HWKV_COMBINE_UNROLL;  // splits per thread per round
+
 // One workgroup per (item, query head of the group, kCombineChan-channel
 // chunk).  Its threads are R rows of kCombineChan / 4 lanes, a lane owning 4
 // channels (one 16-byte load per split, so a row reads whole 128-byte

@@ -92,18 +92,6 @@ constexpr int kMinWavesPerEU = HWKV_DECODE_MINWAVES;  // VGPR budget
 // A split is one page of a paged full unit: its workgroup reads one page.
 static_assert(kWaves * kTilesPerWave * kTile == kPageTokens && kTilesPerWave == 1,
               "a decode split must be one page of 4 tiles, one per wave");
-#ifndef HWKV_COMBINE_THREADS
-#define HWKV_COMBINE_THREADS 512
-#endif
-#ifndef HWKV_COMBINE_CHAN
-#define HWKV_COMBINE_CHAN 32
-#endif
-#ifndef HWKV_COMBINE_UNROLL
-#define HWKV_COMBINE_UNROLL 8
-#endif
-constexpr int kCombineThreads = HWKV_COMBINE_THREADS;  // per merge workgroup
-constexpr int kCombineChan = HWKV_COMBINE_CHAN;        // channels per workgroup
-constexpr int kCombineUnroll = HWKV_COMBINE_UNROLL;  // splits per thread per round
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
