@@ -17,13 +17,13 @@ namespace {
 
 // Merge geometry (compile-time).
 #ifndef HWKV_COMBINE_THREADS
-#define HWKV_COMBINE_THREADS 512
+#define HWKV_COMBINE_THREADS 256
 #endif
 #ifndef HWKV_COMBINE_CHAN
 #define HWKV_COMBINE_CHAN 32
 #endif
 #ifndef HWKV_COMBINE_UNROLL
-#define HWKV_COMBINE_UNROLL 8
+#define HWKV_COMBINE_UNROLL 4
 #endif
 constexpr int kCombineThreads = HWKV_COMBINE_THREADS;  // per merge workgroup
 constexpr int kCombineChan = HWKV_COMBINE_CHAN;        // channels per workgroup
@@ -34,8 +34,8 @@ constexpr int kCombineUnroll = HWKV_COMBINE_UNROLL;  // splits per thread per ro
 // channels (one 16-byte load per split, so a row reads whole 128-byte
 // lines).  Thread (r, q) merges its channels over splits r, r + R, r + 2R,
 // ...; each round issues the loads of kCombineUnroll splits before using any
-// of them, so a round costs one memory round trip, and R * kCombineUnroll
-// splits (512) fit in one round.  The rows are then merged: the common
+// of them, so a round costs one memory round trip (R * kCombineUnroll = 128
+// splits per round).  The rows are then merged: the common
 // shift through LDS, the weighted sums across the rows of a wavefront by
 // lane shuffles, and across the wavefronts in LDS.  The merge is a
 // kernel of its own: ordering the partials of other workgroups inside the
