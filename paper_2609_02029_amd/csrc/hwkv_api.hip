@@ -972,6 +972,12 @@ int hwkv_calib_replay(int32_t n_kv_heads, int32_t n_q_heads, int32_t head_dim,
   rc = check_device(hipStreamSynchronize(st), "hipStreamSynchronize");
   if (rc != HWKV_OK) return rc;
 
+  int dev = 0, n_cus = 256;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&n_cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      n_cus < 1)
+    n_cus = 256;  // only the split sizes depend on it
+  (void)hipGetLastError();
   const size_t vec = (size_t)n_rows * n_q_heads * head_dim;
   float *part = reinterpret_cast<float *>(static_cast<uint8_t *>(ws) +
                                           replay_rows_bytes(n_rows));
@@ -987,8 +993,16 @@ int hwkv_calib_replay(int32_t n_kv_heads, int32_t n_q_heads, int32_t head_dim,
       const int64_t c0 = b * per, c1 = std::min(c0 + per, n_rows * G) - 1;
       max_tiles = std::max(max_tiles, replay_tiles(rows[c0 / G], rows[c1 / G], w, n_sinks));
     }
-    const int64_t n_splits =
-        (max_tiles + hwkv::kReplayTilesPerSplit - 1) / hwkv::kReplayTilesPerSplit;
+    // splits: about one workgroup per CU (a workgroup holds a CU), never
+    // more than the workspace holds (the longest candidate's count at
+    // kReplayTilesPerSplit tiles each), each of at least the minimum size
+    const int64_t ws_splits = replay_max_splits(n_hist, n_sinks);
+    const int64_t want = std::min<int64_t>(
+        ws_splits, std::max<int64_t>(1, n_cus / (nb * n_kv_heads)));
+    const int64_t tps = std::max<int64_t>(
+        hwkv::kReplayMinTilesPerSplit,
+        std::max<int64_t>((max_tiles + want - 1) / want, (max_tiles + ws_splits - 1) / ws_splits));
+    const int64_t n_splits = (max_tiles + tps - 1) / tps;
     for (int32_t h = 0; h < n_kv_heads; ++h) {
       a.head[h].window = (int32_t)w;
       a.head[h].pto = -1;          // no cache: every key comes from the trace
@@ -1008,7 +1022,7 @@ int hwkv_calib_replay(int32_t n_kv_heads, int32_t n_q_heads, int32_t head_dim,
     a.scale_log2 = scale * 1.4426950408889634f;
     if (n_splits > 1) {
       a.part = part;
-      a.tiles_per_split = hwkv::kReplayTilesPerSplit;
+      a.tiles_per_split = (int32_t)tps;
     }
     rc = check_device(hwkv::launch_prefill_attn(head_dim, a, st, (int)n_splits),
                       "calib replay launch");

@@ -194,7 +194,14 @@ struct ReplayMergeArgs {
   float scale_log2;
 };
 hipError_t launch_replay_merge(int D, const ReplayMergeArgs &a, hipStream_t s);
-constexpr int kReplayTilesPerSplit = 128;   // 32-key tiles per split
+constexpr int kReplayTilesPerSplit = 128;   // 32-key tiles per split, at most
+#ifndef HWKV_REPLAY_MIN_TILES
+#define HWKV_REPLAY_MIN_TILES 8
+#endif
+// A candidate with fewer tiles takes smaller splits (as many as the
+// workspace holds, of at least this many tiles), so that its launch still
+// has workgroups for every CU.
+constexpr int kReplayMinTilesPerSplit = HWKV_REPLAY_MIN_TILES;
 hipError_t launch_calib_means(const CalibArgs &a, hipStream_t s);
 
 }  // namespace hwkv
