@@ -14,10 +14,12 @@
 // item's slots are cut into splits of kWaves * kTilesPerWave * 64 tokens and
 // every split is one workgroup, so the grid is balanced by bytes, not by unit
 // (full and windowed heads of one layer differ by up to ~56x in length).  The
-// G query heads of an item share every K/V byte read.
+// G query heads of an item share every K/V byte read.  A split is one page
+// of a paged full unit, whose workgroup reads that page only.
 //
-// Inside a wave, per 64-slot tile (one stream of 16-byte buffer loads per
-// lane, kPrefetch loads always in flight):
+// Inside a wave, per 64-slot tile (one stream of chunk-sized buffer loads per
+// lane -- 16 bytes, or 8 for fp8 -- with kPrefetch, or kPrefetch8, loads
+// always in flight):
 //   q.k   one lane per slot: the K tile is stored slot-minor in 8-element
 //         channel chunks, so chunk g of the tile is contiguous and lane t
 //         reads its own slot's chunk; q is uniform and comes through scalar
@@ -30,10 +32,12 @@
 //   softmax  online, base 2 (log2(e) folded into the scale); the tile max is
 //         one DPP row reduction plus four lane reads per head.
 //   p.v   lanes own 8 channels of one row (V row-major, a wave reads whole
-//         rows contiguously); p stays fp32 and is broadcast through a
-//         per-wave LDS slice; the values are widened to fp32 (exact for
-//         every format) and take one fp32 FMA per (row, channel, head); the
-//         fp8 V scale multiplies the workgroup's result.
+//         rows contiguously); p is broadcast through a per-wave LDS slice.
+//         bf16 and binary16 values are widened to fp32 (exactly) and take
+//         one fp32 FMA per (row, channel, head) with the fp32 weights; fp8
+//         values go over token pairs in binary16 (v_dot2_f32_f16, the
+//         weights rounded to binary16, the normaliser in fp32), and the fp8
+//         V scale multiplies the workgroup's result.
 //         The V buffer descriptor ends at row n_valid, so rows past it read
 //         as zero (and their p is zero).
 // The fused append writes the new token, in the cache format, into its slot
@@ -113,7 +117,7 @@ __device__ __forceinline__ float bf_hi(uint32_t x) {
   return __uint_as_float(x & 0xffff0000u);
 }
 
-// 16-byte raw buffer load: SGPR descriptor + 32-bit byte offset; reads past
+// Raw buffer loads: SGPR descriptor + 32-bit byte offset; reads past
 // the descriptor's num_records return zero.
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base,
