@@ -216,3 +216,81 @@ def test_batch16_paged_full_size():
     assert hwkv.cache_pages(r.cache) == (n_pages, 0)      # the pool is used exactly
     log(f"batch16 paged: {n_pages} pages, max rel err {worst:.3e}")
     r.free()
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "f16", "fp8"])
+@pytest.mark.parametrize("D,G", [(64, 1), (128, 8), (256, 6), (256, 1)])
+def test_paged_dims_groups_formats(fmt, D, G):
+    cfg = mini(n_layers=1, batch=2, head_dim=D, n_kv_heads=2, n_q_heads=2 * G,
+               level_windows=[300, 0], levels=[[1, 0]], prompt=[511, 770], max_ctx=900,
+               seed=44)
+    kw = {} if fmt != "fp8" else dict(k_scale=0.017, v_scale=0.011)
+    r = Run(cfg, n_pages=12, kv_format=fmt, **kw)
+    for b in range(2):
+        r.prefill(0, b, chunks=[200])
+    r.check_layer(0)
+    for st in range(3):                    # 511 -> 514 crosses into the third page
+        qa, out = r.step(0, fused=bool(st % 2))
+        r.check_out(0, qa, out, f"{fmt} D={D} G={G} step {st}")
+    r.check_layer(0)
+    check_pages(r, 12)
+    r.free()
+
+
+def test_paged_more_items_than_one_launch():
+    # 17 sequences x 4 kv heads = 68 items: two launch groups per call
+    cfg = mini(batch=17, n_layers=1, n_kv_heads=4, n_q_heads=16, level_windows=[30, 0],
+               levels=[[0, 1, 1, 0]], prompt=[int(x) for x in range(40, 40 + 17 * 23, 23)],
+               max_ctx=600, seed=45)
+    n_pages = 2 * sum((p + 2 + PT - 1) // PT for p in cfg["prompt"])
+    r = Run(cfg, n_pages=n_pages)
+    for b in range(17):
+        r.prefill(0, b)
+    for st in range(2):
+        qa, out = r.step(0, fused=bool(st))
+        r.check_out(0, qa, out, f"step {st}")
+    r.check_layer(0)
+    check_pages(r, n_pages)
+    r.free()
+
+
+def test_paged_canonical_full_and_unaligned_capacity():
+    # S + w >= max_ctx makes the 500-token window a full unit (paged too);
+    # max_ctx = 300 is not a multiple of the page size: the second page is
+    # only partly within the capacity
+    cfg = mini(n_layers=1, batch=1, level_windows=[500, 40], levels=[[0, 1]],
+               prompt=[290], max_ctx=300, seed=46)
+    r = Run(cfg, n_pages=2)
+    cap, win = hwkv.cache_unit_info(r.cache, 0, 0)
+    assert (cap, win) == (300, 0)
+    r.prefill(0, 0)
+    r.check_layer(0)
+    for st in range(10):                   # fills the unit to its capacity
+        qa, out = r.step(0, fused=bool(st % 2))
+        r.check_out(0, qa, out, f"step {st}")
+    r.check_layer(0)
+    assert hwkv.cache_pages(r.cache) == (2, 0)
+    dev = torch.device("cuda:0")
+    kn = torch.zeros((1, 2, 64), dtype=torch.bfloat16, device=dev)
+    with pytest.raises(hwkv.HwkvError) as e:
+        hwkv.append(r.cache, 0, kn, kn)
+    assert e.value.code == hwkv.ECAPACITY  # the capacity, not the pool, is the limit
+    r.free()
+
+
+def test_reset_on_an_unpaged_cache():
+    cfg = mini(n_layers=1, batch=2, prompt=[400, 300], seed=47)
+    r = Run(cfg)
+    for b in range(2):
+        r.prefill(0, b)
+    qa, out = r.step(0)
+    r.check_out(0, qa, out, "before reset")
+    r.reset(0)
+    assert hwkv.cache_seq_len(r.cache, 0, 0) == 0
+    r.prefill(0, 0, P=123)
+    r.check_layer(0)
+    for st in range(2):
+        qa, out = r.step(0, fused=bool(st))
+        r.check_out(0, qa, out, f"after reset step {st}")
+    r.check_layer(0)
+    r.free()
