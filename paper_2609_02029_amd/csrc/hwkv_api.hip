@@ -310,6 +310,172 @@ int take_pages(hwkv_cache *c, int32_t layer,
   return HWKV_OK;
 }
 
+// Element offsets (bf16) of the prefill-attention staging image of an fp8
+// cache: per kv head of the layer its K tiles and V rows in the bf16 cache
+// layout (cap_pad rows each), then the chunk's K and V ([n_tokens][Hkv][D]);
+// returns the bytes.
+struct StageLayout {
+  std::vector<int64_t> k_img, v_img;
+  int64_t k_in = 0, v_in = 0;
+};
+size_t stage_layout(const hwkv_cache *c, int32_t layer, int64_t n_tokens, StageLayout *out) {
+  const hwkv_policy &p = c->pol;
+  const int64_t D = p.head_dim;
+  int64_t off = 0;
+  StageLayout L;
+  for (int32_t h = 0; h < p.n_kv_heads; ++h) {
+    const int32_t u = layer * p.n_kv_heads + h;
+    L.k_img.push_back(off);
+    off += c->cap_pad[u] * D;
+    L.v_img.push_back(off);
+    off += c->cap_pad[u] * D;
+  }
+  off = (off + 127) / 128 * 128;                    // 256-byte aligned
+  L.k_in = off;
+  off += n_tokens * p.n_kv_heads * D;
+  L.v_in = off;
+  off += n_tokens * p.n_kv_heads * D;
+  if (out) *out = L;
+  return (size_t)off * 2;
+}
+
+int prefill_attn_impl(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0,
+                      int64_t n_tokens, const void *q, const void *k, const void *v,
+                      float scale, void *out, void *ws, size_t ws_bytes, void *stream) {
+  if (!c) return fail(HWKV_EINVAL, "cache is null");
+  if (c->fmt == HWKV_KV_F16)
+    return fail(HWKV_EINVAL, "prefill attention reads bf16 or fp8 caches (binary16 "
+                             "values are not bf16 values)");
+  const bool staged = c->fmt == HWKV_KV_FP8_E4M3;
+  const hwkv_policy &p = c->pol;
+  if (layer < 0 || layer >= p.n_layers || seq < 0 || seq >= c->batch)
+    return fail(HWKV_EINVAL, "layer or seq out of range");
+  if (n_tokens < 0) return fail(HWKV_EINVAL, "n_tokens must be >= 0");
+  if (!std::isfinite(scale) || !(scale > 0.0f))
+    return fail(HWKV_EINVAL, "scale must be finite and > 0");
+  if (pos0 != seq_len(c, layer, seq))
+    return fail(HWKV_ESTATE, "pos0 " + std::to_string(pos0) +
+                                 " != sequence length " +
+                                 std::to_string(seq_len(c, layer, seq)));
+  if (pos0 + n_tokens > c->max_ctx)
+    return fail(HWKV_ECAPACITY, "prefill past max_ctx");
+  if (n_tokens == 0) return ok();
+  if (!q || !k || !v || !out)
+    return fail(HWKV_EINVAL, "q, k, v and out must be non-null");
+  StageLayout SL;
+  if (staged) {
+    const size_t need = stage_layout(c, layer, n_tokens, &SL);
+    if (!ws || ws_bytes < need)
+      return fail(HWKV_EINVAL, "workspace missing or too small (need " +
+                                   std::to_string(need) + " bytes)");
+  }
+  const int32_t H = p.n_kv_heads;
+  const int32_t G = (int32_t)group_size(p);
+  const int64_t D = p.head_dim;
+  const hipStream_t st = (hipStream_t)stream;
+  hwkv::PrefillAttnArgs a;
+  std::memset(&a, 0, sizeof a);
+  const int64_t p1 = pos0 + n_tokens;
+  std::vector<std::pair<int64_t, int32_t>> work;  // (keys of the last token, h)
+  for (int32_t h = 0; h < H; ++h) {
+    const int32_t u = layer * H + h;
+    const int64_t seq_off = (int64_t)seq * c->cap_pad[u] * D;
+    if (staged) {         // the bf16 image of the unit
+      a.head[h].k_off = SL.k_img[h];
+      a.head[h].v_off = SL.v_img[h];
+      a.head[h].pto = -1;
+      a.head[h].k_scale = c->k_scale[u];
+      a.head[h].v_scale = c->v_scale[u];
+    } else {
+      a.head[h].k_off = c->k_off[u] + seq_off;
+      a.head[h].v_off = c->v_off[u] + seq_off;
+      a.head[h].pto = page_tab_off(c, u, seq);
+      a.head[h].k_scale = 1.0f;
+      a.head[h].v_scale = 1.0f;
+    }
+    a.head[h].window = (int32_t)c->window[u];
+    const int64_t w = c->window[u];
+    work.push_back({w == 0 ? p1 : std::min(p1, (int64_t)p.n_sinks + w), h});
+  }
+  std::stable_sort(work.begin(), work.end(),
+                   [](const std::pair<int64_t, int32_t> &x,
+                      const std::pair<int64_t, int32_t> &y) {
+                     return x.first > y.first;
+                   });
+  for (int32_t r = 0; r < H; ++r) a.head_order[r] = work[r].second;
+  const int64_t cols = n_tokens * G;
+  const int64_t per = hwkv::prefill_attn_columns_per_block();
+  const int64_t nb = (cols + per - 1) / per;
+  if (nb * H > (int64_t)INT32_MAX)
+    return fail(HWKV_EINVAL, "n_tokens too large for one launch");
+  if (staged) {
+    uint16_t *img = static_cast<uint16_t *>(ws);
+    // the occupied rows of every unit (the keys below pos0), widened
+    hwkv::StageArgs sa;
+    std::memset(&sa, 0, sizeof sa);
+    int64_t max_chunks = 0;
+    for (int32_t h = 0; h < H; ++h) {
+      const int32_t u = layer * H + h;
+      const int64_t seq_off = (int64_t)seq * c->cap_pad[u] * D;
+      hwkv::StageUnit &su = sa.unit[h];
+      su.src_k_off = c->k_off[u] + seq_off;
+      su.src_v_off = c->v_off[u] + seq_off;
+      su.dst_k_off = SL.k_img[h];
+      su.dst_v_off = SL.v_img[h];
+      su.pto = page_tab_off(c, u, seq);
+      su.n_rows = (int32_t)std::min(pos0, c->cap[u]);
+      max_chunks = std::max(max_chunks, (int64_t)((su.n_rows + 63) / 64) * 64 * (D / 8));
+    }
+    sa.cache = c->base;
+    sa.page_table = device_page_table(c);
+    sa.pool_off = c->pool_off;
+    sa.image = img;
+    sa.n_units = H;
+    sa.max_chunks = (int32_t)max_chunks;
+    int rc;
+    if (max_chunks > 0 &&
+        (rc = check_device(hwkv::launch_stage_units((int)D, sa, st), "stage launch")) != HWKV_OK)
+      return rc;
+    // the chunk's own keys and values as the cache will store them
+    hwkv::StageChunkArgs ca;
+    std::memset(&ca, 0, sizeof ca);
+    ca.k = static_cast<const uint16_t *>(k);
+    ca.v = static_cast<const uint16_t *>(v);
+    ca.k_out = img + SL.k_in;
+    ca.v_out = img + SL.v_in;
+    for (int32_t h = 0; h < H; ++h) {
+      ca.k_scale[h] = c->k_scale[layer * H + h];
+      ca.v_scale[h] = c->v_scale[layer * H + h];
+    }
+    ca.n_chunks = n_tokens * H * (D / 8);
+    ca.n_kv_heads = H;
+    if ((rc = check_device(hwkv::launch_stage_chunk((int)D, ca, st), "stage launch")) != HWKV_OK)
+      return rc;
+    a.cache = img;
+    a.k = img + SL.k_in;
+    a.v = img + SL.v_in;
+  } else {
+    a.cache = reinterpret_cast<const uint16_t *>(c->base);
+    a.page_table = device_page_table(c);
+    a.pool_off = c->pool_off;
+    a.k = static_cast<const uint16_t *>(k);
+    a.v = static_cast<const uint16_t *>(v);
+  }
+  a.q = static_cast<const uint16_t *>(q);
+  a.out = static_cast<float *>(out);
+  a.p0 = (int32_t)pos0;
+  a.n_tokens = (int32_t)n_tokens;
+  a.n_kv_heads = H;
+  a.group = G;
+  a.n_sinks = p.n_sinks;
+  a.n_col_blocks = (int32_t)nb;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  return check_device(hwkv::launch_prefill_attn(p.head_dim, a, st), "prefill_attn launch") ==
+                 HWKV_OK
+             ? ok()
+             : HWKV_EDEVICE;
+}
+
 // Shared validation of a decode call; fills per-item lengths.
 int decode_impl(hwkv_cache *c, int32_t layer, const void *k_new,
                 const void *v_new, const void *q, float scale, void *out,
@@ -819,70 +985,31 @@ int hwkv_prefill_write(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0,
 int hwkv_prefill_attn(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0,
                       int64_t n_tokens, const void *q, const void *k,
                       const void *v, float scale, void *out, void *stream) {
-  if (!c) return fail(HWKV_EINVAL, "cache is null");
-  if (c->fmt != HWKV_KV_BF16)
-    return fail(HWKV_EINVAL, "prefill attention needs a bf16 cache");
-  const hwkv_policy &p = c->pol;
-  if (layer < 0 || layer >= p.n_layers || seq < 0 || seq >= c->batch)
-    return fail(HWKV_EINVAL, "layer or seq out of range");
+  if (c && c->fmt != HWKV_KV_BF16)
+    return fail(HWKV_EINVAL, "prefill attention needs a bf16 cache here "
+                             "(hwkv_prefill_attn_ws takes fp8 caches)");
+  return prefill_attn_impl(c, layer, seq, pos0, n_tokens, q, k, v, scale, out,
+                           nullptr, 0, stream);
+}
+
+int hwkv_prefill_attn_workspace_bytes(const hwkv_cache *c, int64_t n_tokens,
+                                      size_t *bytes) {
+  if (!c || !bytes) return fail(HWKV_EINVAL, "null argument");
   if (n_tokens < 0) return fail(HWKV_EINVAL, "n_tokens must be >= 0");
-  if (!std::isfinite(scale) || !(scale > 0.0f))
-    return fail(HWKV_EINVAL, "scale must be finite and > 0");
-  if (pos0 != seq_len(c, layer, seq))
-    return fail(HWKV_ESTATE, "pos0 " + std::to_string(pos0) +
-                                 " != sequence length " +
-                                 std::to_string(seq_len(c, layer, seq)));
-  if (pos0 + n_tokens > c->max_ctx)
-    return fail(HWKV_ECAPACITY, "prefill past max_ctx");
-  if (n_tokens == 0) return ok();
-  if (!q || !k || !v || !out)
-    return fail(HWKV_EINVAL, "q, k, v and out must be non-null");
-  const int32_t H = p.n_kv_heads;
-  const int32_t G = (int32_t)group_size(p);
-  hwkv::PrefillAttnArgs a;
-  std::memset(&a, 0, sizeof a);
-  const int64_t p1 = pos0 + n_tokens;
-  std::vector<std::pair<int64_t, int32_t>> work;  // (keys of the last token, h)
-  for (int32_t h = 0; h < H; ++h) {
-    const int32_t u = layer * H + h;
-    const int64_t seq_off = (int64_t)seq * c->cap_pad[u] * p.head_dim;
-    a.head[h].k_off = c->k_off[u] + seq_off;
-    a.head[h].v_off = c->v_off[u] + seq_off;
-    a.head[h].window = (int32_t)c->window[u];
-    a.head[h].pto = page_tab_off(c, u, seq);
-    const int64_t w = c->window[u];
-    work.push_back({w == 0 ? p1 : std::min(p1, (int64_t)p.n_sinks + w), h});
-  }
-  std::stable_sort(work.begin(), work.end(),
-                   [](const std::pair<int64_t, int32_t> &x,
-                      const std::pair<int64_t, int32_t> &y) {
-                     return x.first > y.first;
-                   });
-  for (int32_t r = 0; r < H; ++r) a.head_order[r] = work[r].second;
-  const int64_t cols = n_tokens * G;
-  const int64_t per = hwkv::prefill_attn_columns_per_block();
-  const int64_t nb = (cols + per - 1) / per;
-  if (nb * H > (int64_t)INT32_MAX)
-    return fail(HWKV_EINVAL, "n_tokens too large for one launch");
-  a.cache = reinterpret_cast<const uint16_t *>(c->base);
-  a.page_table = device_page_table(c);
-  a.pool_off = c->pool_off;
-  a.q = static_cast<const uint16_t *>(q);
-  a.k = static_cast<const uint16_t *>(k);
-  a.v = static_cast<const uint16_t *>(v);
-  a.out = static_cast<float *>(out);
-  a.p0 = (int32_t)pos0;
-  a.n_tokens = (int32_t)n_tokens;
-  a.n_kv_heads = H;
-  a.group = G;
-  a.n_sinks = p.n_sinks;
-  a.n_col_blocks = (int32_t)nb;
-  a.scale_log2 = scale * 1.4426950408889634f;
-  return check_device(
-             hwkv::launch_prefill_attn(p.head_dim, a, (hipStream_t)stream),
-             "prefill_attn launch") == HWKV_OK
-             ? ok()
-             : HWKV_EDEVICE;
+  size_t best = 0;
+  if (c->fmt == HWKV_KV_FP8_E4M3)
+    for (int32_t l = 0; l < c->pol.n_layers; ++l)
+      best = std::max(best, stage_layout(c, l, n_tokens, nullptr));
+  *bytes = best;
+  return ok();
+}
+
+int hwkv_prefill_attn_ws(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0,
+                         int64_t n_tokens, const void *q, const void *k,
+                         const void *v, float scale, void *out, void *ws,
+                         size_t ws_bytes, void *stream) {
+  return prefill_attn_impl(c, layer, seq, pos0, n_tokens, q, k, v, scale, out, ws,
+                           ws_bytes, stream);
 }
 
 namespace {
@@ -1006,6 +1133,8 @@ int hwkv_calib_replay(int32_t n_kv_heads, int32_t n_q_heads, int32_t head_dim,
     for (int32_t h = 0; h < n_kv_heads; ++h) {
       a.head[h].window = (int32_t)w;
       a.head[h].pto = -1;          // no cache: every key comes from the trace
+      a.head[h].k_scale = 1.0f;
+      a.head[h].v_scale = 1.0f;
       a.head_order[h] = h;
     }
     a.q = static_cast<const uint16_t *>(q);

@@ -123,6 +123,8 @@ struct PrefillAttnHead {
   int64_t v_off;                 // element offset of its V rows
   int32_t window;                // 0 = full
   int32_t pto;                   // page-table offset of a paged unit, or -1
+  float k_scale;                 // logit multiplier of the stored keys (fp8: s_K)
+  float v_scale;                 // output multiplier (fp8: s_V)
 };
 
 struct PrefillAttnArgs {
@@ -169,6 +171,35 @@ hipError_t launch_prefill_write(int fmt, int D, const WriteArgs &a,
                                 int max_tiles, hipStream_t s);
 hipError_t launch_append(int fmt, int D, const AppendArgs &a, hipStream_t s);
 hipError_t launch_page_update(const PageUpdateArgs &a, hipStream_t s);
+
+// Staging of an fp8 cache for prefill attention: rows [0, n_rows) of one
+// (unit, sequence) widened to bf16 code values in the bf16 cache layout, and
+// a chunk's K or V quantised as the cache stores it and widened.
+struct StageUnit {
+  int64_t src_k_off, src_v_off;  // fp8 element offsets (unpaged units)
+  int64_t dst_k_off, dst_v_off;  // bf16 element offsets in the image
+  int32_t pto;                   // page-table offset of a paged unit, or -1
+  int32_t n_rows;                // occupied slots to stage
+};
+struct StageArgs {
+  StageUnit unit[kMaxItems];     // one per kv head of the layer
+  const uint8_t *cache;          // fp8 cache base
+  const int32_t *page_table;
+  int64_t pool_off;
+  uint16_t *image;               // bf16 image base
+  int32_t n_units;
+  int32_t max_chunks;            // max over units of n_rows * D / 8 (per K or V)
+};
+hipError_t launch_stage_units(int D, const StageArgs &a, hipStream_t s);
+struct StageChunkArgs {
+  const uint16_t *k, *v;         // [n_tokens][Hkv][D] bf16 inputs
+  uint16_t *k_out, *v_out;       // the same layout, bf16 code values
+  float k_scale[kMaxItems];      // per kv head of the layer
+  float v_scale[kMaxItems];
+  int64_t n_chunks;              // n_tokens * Hkv * D / 8
+  int32_t n_kv_heads;
+};
+hipError_t launch_stage_chunk(int D, const StageChunkArgs &a, hipStream_t s);
 int prefill_attn_columns_per_block();   // (token, q head) columns
 hipError_t launch_prefill_attn(int D, const PrefillAttnArgs &a, hipStream_t s,
                               int n_splits = 1);
@@ -211,4 +242,6 @@ static_assert(sizeof(hwkv::DecodeArgs) <= 4096, "decode kernarg too large");
 static_assert(sizeof(hwkv::WriteArgs) <= 4096, "write kernarg too large");
 static_assert(sizeof(hwkv::AppendArgs) <= 4096, "append kernarg too large");
 static_assert(sizeof(hwkv::PageUpdateArgs) <= 4096, "page update kernarg too large");
+static_assert(sizeof(hwkv::StageArgs) <= 4096, "stage kernarg too large");
+static_assert(sizeof(hwkv::StageChunkArgs) <= 4096, "stage chunk kernarg too large");
 static_assert(sizeof(hwkv::PrefillAttnArgs) <= 4096, "prefill kernarg too large");

@@ -276,7 +276,8 @@ void prefill_attn(const PrefillAttnArgs a) {
     }
   };
 
-  const float c2 = a.scale_log2;
+  // logit scale, base 2, with the stored keys' scale (1 but for fp8 caches)
+  const float c2 = a.scale_log2 * hd.k_scale;
   const float tau = 8.0f / c2;                  // lazy-rescale slack (raw units)
   float m = -1e30f;                              // running shift (raw units)
   float l = 0.0f;                                // this lane's partial sum
@@ -401,7 +402,7 @@ void prefill_attn(const PrefillAttnArgs a) {
                         o[db][4 * rq + 3]);
     return;
   }
-  const float inv = 1.0f / lt;
+  const float inv = hd.v_scale / lt;     // the stored values' scale (fp8)
   // the output row, recomputed here rather than kept live through the loop
   int c_out = c;
   asm volatile("" : "+v"(c_out));

@@ -12,6 +12,8 @@
 // [p0, p1).  Iterating over destination slots makes every K tile write a
 // full, coalesced chunk-per-lane store and never touches slots the chunk
 // does not own, so prefill never forms a full-length cache.
+#include <algorithm>
+
 #include "hwkv_internal.h"
 #include "kv_format.h"
 
@@ -133,6 +135,66 @@ __global__ __launch_bounds__(512) void page_update(PageUpdateArgs a) {
   for (int i = threadIdx.x; i < a.n; i += 512) a.table[a.idx[i]] = a.page[i];
 }
 
+// 8 fp8 codes as 8 bf16 values (exact: every E4M3 value is a bf16 value).
+__device__ __forceinline__ uint4 widen_fp8x8(uint2 c) {
+  auto w = [](uint32_t x, bool hi) -> uint32_t {
+    return __builtin_bit_cast(uint32_t, hi ? __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x, 1.0f, true)
+                                           : __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x, 1.0f, false));
+  };
+  return make_uint4(w(c.x, false), w(c.x, true), w(c.y, false), w(c.y, true));
+}
+
+// Staging of an fp8 cache for prefill attention: the occupied rows of each
+// (unit, sequence) of a layer widened to bf16 code values, in the layout of
+// a bf16 cache (K tiles chunk for chunk, V rows), into an image the bf16
+// kernel reads.  blockIdx.y: the unit; blockIdx.z: 0 = K, 1 = V.  Whole K
+// tiles are staged (rows past the occupied ones are never read).
+template <int D>
+__global__ __launch_bounds__(256) void stage_units(StageArgs a) {
+  constexpr int NC = D / 8;
+  constexpr int TPP = kPageTokens / kTile;
+  const StageUnit &su = a.unit[blockIdx.y];
+  const bool isv = blockIdx.z != 0;
+  const int64_t n = isv ? (int64_t)su.n_rows * NC
+                        : (int64_t)((su.n_rows + kTile - 1) / kTile) * kTile * NC;
+  for (int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x; c < n;
+       c += (int64_t)gridDim.x * 256) {
+    int64_t src;
+    if (su.pto < 0) {
+      src = (isv ? su.src_v_off : su.src_k_off) + c * 8;
+    } else if (!isv) {          // K chunk c: tile t, position r in the tile
+      const int64_t t = c / (kTile * NC), r = c % (kTile * NC);
+      const int64_t pg = a.page_table[su.pto + t / TPP];
+      src = a.pool_off + pg * 2 * kPageTokens * D + (t % TPP) * kTile * D + r * 8;
+    } else {                    // V chunk c: row j, chunk g
+      const int64_t j = c / NC, g = c % NC;
+      const int64_t pg = a.page_table[su.pto + j / kPageTokens];
+      src = a.pool_off + pg * 2 * kPageTokens * D + (int64_t)kPageTokens * D +
+            (j % kPageTokens) * D + g * 8;
+    }
+    const uint2 codes = *reinterpret_cast<const uint2 *>(a.cache + src);
+    *reinterpret_cast<uint4 *>(a.image + (isv ? su.dst_v_off : su.dst_k_off) + c * 8) =
+        widen_fp8x8(codes);
+  }
+}
+
+// The chunk's own K and V as the fp8 cache will store them (code(x / s) of
+// the unit's scale), widened to bf16 code values.
+template <int D>
+__global__ __launch_bounds__(256) void stage_chunk(StageChunkArgs a) {
+  constexpr int NC = D / 8;
+  for (int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x; c < a.n_chunks;
+       c += (int64_t)gridDim.x * 256) {
+    const int h = (int)((c / NC) % a.n_kv_heads);
+    const uint4 k = *reinterpret_cast<const uint4 *>(a.k + c * 8);
+    const uint4 v = *reinterpret_cast<const uint4 *>(a.v + c * 8);
+    *reinterpret_cast<uint4 *>(a.k_out + c * 8) =
+        widen_fp8x8(encode8<HWKV_KV_FP8_E4M3>(k, a.k_scale[h]));
+    *reinterpret_cast<uint4 *>(a.v_out + c * 8) =
+        widen_fp8x8(encode8<HWKV_KV_FP8_E4M3>(v, a.v_scale[h]));
+  }
+}
+
 // Calls L<D, F>::run(args...) for the runtime (D, format).
 template <template <int, int> class L, typename... Args>
 hipError_t dispatch_df(int fmt, int D, Args &&...args) {
@@ -178,6 +240,30 @@ hipError_t launch_prefill_write(int fmt, int D, const WriteArgs &a,
 
 hipError_t launch_append(int fmt, int D, const AppendArgs &a, hipStream_t s) {
   return dispatch_df<AppendLaunch>(fmt, D, a, s);
+}
+
+hipError_t launch_stage_units(int D, const StageArgs &a, hipStream_t s) {
+  const int64_t per = 256;
+  const dim3 grid((unsigned)std::max<int64_t>(1, std::min<int64_t>((a.max_chunks + per - 1) / per, 2048)),
+                  (unsigned)a.n_units, 2);
+  switch (D) {
+    case 64: hipLaunchKernelGGL(stage_units<64>, grid, dim3(256), 0, s, a); break;
+    case 128: hipLaunchKernelGGL(stage_units<128>, grid, dim3(256), 0, s, a); break;
+    case 256: hipLaunchKernelGGL(stage_units<256>, grid, dim3(256), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_stage_chunk(int D, const StageChunkArgs &a, hipStream_t s) {
+  const dim3 grid((unsigned)std::max<int64_t>(1, std::min<int64_t>((a.n_chunks + 255) / 256, 4096)));
+  switch (D) {
+    case 64: hipLaunchKernelGGL(stage_chunk<64>, grid, dim3(256), 0, s, a); break;
+    case 128: hipLaunchKernelGGL(stage_chunk<128>, grid, dim3(256), 0, s, a); break;
+    case 256: hipLaunchKernelGGL(stage_chunk<256>, grid, dim3(256), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_page_update(const PageUpdateArgs &a, hipStream_t s) {

@@ -59,6 +59,9 @@ SYMBOLS = {
     "hwkv_prefill_write": ([_vp, _i32, _i32, _i64, _i64, _vp, _vp, _vp], ctypes.c_int),
     "hwkv_prefill_attn": ([_vp, _i32, _i32, _i64, _i64, _vp, _vp, _vp, ctypes.c_float, _vp,
                            _vp], ctypes.c_int),
+    "hwkv_prefill_attn_workspace_bytes": ([_vp, _i64, _P(_sz)], ctypes.c_int),
+    "hwkv_prefill_attn_ws": ([_vp, _i32, _i32, _i64, _i64, _vp, _vp, _vp, ctypes.c_float, _vp,
+                              _vp, _sz, _vp], ctypes.c_int),
     "hwkv_append": ([_vp, _i32, _vp, _vp, _vp], ctypes.c_int),
     "hwkv_decode_workspace_bytes": ([_vp, _P(_sz)], ctypes.c_int),
     "hwkv_decode_attn": ([_vp, _i32, _vp, _flt, _vp, _vp, _sz, _vp], ctypes.c_int),
@@ -320,9 +323,17 @@ def prefill_write(cache, layer, seq, pos0, k, v, stream=None):
                                    _stream(stream)))
 
 
-def prefill_attn(cache, layer, seq, pos0, q, k, v, scale, out, stream=None):
+def prefill_attn_workspace_bytes(cache, n_tokens):
+    r = _sz()
+    _check(_lib.hwkv_prefill_attn_workspace_bytes(cache.handle, n_tokens, ctypes.byref(r)))
+    return r.value
+
+
+def prefill_attn(cache, layer, seq, pos0, q, k, v, scale, out, ws=None, stream=None):
     """``q``: bf16 [n_tokens, n_q_heads, head_dim]; ``k``, ``v``: bf16
-    [n_tokens, n_kv_heads, head_dim]; ``out``: fp32 like ``q`` (device)."""
+    [n_tokens, n_kv_heads, head_dim]; ``out``: fp32 like ``q`` (device).
+    ``ws``: uint8 device workspace (hwkv_prefill_attn_ws; needed by fp8
+    caches, see prefill_attn_workspace_bytes)."""
     n = q.shape[0]
     if tuple(q.shape) != (n, cache.n_q_heads, cache.head_dim):
         raise ValueError("q must be [n_tokens, n_q_heads, head_dim]")
@@ -330,9 +341,17 @@ def prefill_attn(cache, layer, seq, pos0, q, k, v, scale, out, stream=None):
         raise ValueError("k and v must be [n_tokens, n_kv_heads, head_dim]")
     if tuple(out.shape) != tuple(q.shape):
         raise ValueError("out must be [n_tokens, n_q_heads, head_dim]")
-    _check(_lib.hwkv_prefill_attn(cache.handle, layer, seq, pos0, n, _dev(q, "bfloat16", "q"),
-                                  _dev(k, "bfloat16", "k"), _dev(v, "bfloat16", "v"),
-                                  float(scale), _dev(out, "float32", "out"), _stream(stream)))
+    if ws is None:
+        _check(_lib.hwkv_prefill_attn(cache.handle, layer, seq, pos0, n,
+                                      _dev(q, "bfloat16", "q"), _dev(k, "bfloat16", "k"),
+                                      _dev(v, "bfloat16", "v"), float(scale),
+                                      _dev(out, "float32", "out"), _stream(stream)))
+    else:
+        _check(_lib.hwkv_prefill_attn_ws(cache.handle, layer, seq, pos0, n,
+                                         _dev(q, "bfloat16", "q"), _dev(k, "bfloat16", "k"),
+                                         _dev(v, "bfloat16", "v"), float(scale),
+                                         _dev(out, "float32", "out"), _dev(ws, "uint8", "ws"),
+                                         ws.numel(), _stream(stream)))
 
 
 def append(cache, layer, k_new, v_new, stream=None):

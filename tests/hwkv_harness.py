@@ -159,7 +159,7 @@ class Run:
                 continue
             before = self._snapshot(layer, b) if check_untouched else None
             hwkv.prefill_attn(self.cache, layer, b, p0, q[p0:p1], k[p0:p1], v[p0:p1],
-                              self.scale, out[p0:p1])
+                              self.scale, out[p0:p1], ws=self.prefill_ws(P))
             if check_untouched:
                 after = self._snapshot(layer, b)
                 for x, y in zip(before, after):
@@ -172,6 +172,16 @@ class Run:
         self.n[layer, b] = P
         del k, v
         return q, qh, out
+
+    def prefill_ws(self, n_tokens):
+        """Workspace of hwkv_prefill_attn_ws for chunks of up to n_tokens
+        (None for a bf16 cache)."""
+        if self.kv_format == "bf16":
+            return None
+        need = hwkv.prefill_attn_workspace_bytes(self.cache, n_tokens)
+        if getattr(self, "_pws", None) is None or self._pws.numel() < need:
+            self._pws = torch.zeros(max(need, 1), dtype=torch.uint8, device=self.dev)
+        return self._pws
 
     def _snapshot(self, layer, b):
         res = []
@@ -186,6 +196,11 @@ class Run:
         the full host history.  ``q_rows`` [len(rows), Hq, D] bf16 bits."""
         rows = np.asarray(rows, dtype=np.int64)
         hk, hv = self.kh[layer][b], self.vh[layer][b]
+        if self.kv_format != "bf16":   # attention over the stored values
+            n = int(rows[-1]) + 1
+            kv, vv = self.stored_values(layer, hk[:n], hv[:n])
+            return KF.attend_values(KF.bf16_values(q_rows), [kv] * len(rows), [vv] * len(rows),
+                                    rows, self.S, self.windows[layer], self.scale)
         return oracle.decode_layer(q_rows, [hk] * len(rows), [hv] * len(rows), rows, self.S,
                                    self.windows[layer], self.scale, n_threads=n_threads)
 

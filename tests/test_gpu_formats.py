@@ -206,3 +206,88 @@ def test_fp8_ctx112k_workload_full_size():
         r.check_layer(l)
     log(f"fp8 ctx112k: max rel err {worst:.3e}")
     r.free()
+
+
+# ---------------------------------------------------------------------------
+# prefill attention over an fp8 cache: keys below the chunk as stored, the
+# chunk's own as the cache will store them (hwkv_prefill_attn_ws)
+# ---------------------------------------------------------------------------
+def _check_stored_rows(r, layer, b, rows, q_rows, out, what):
+    """The 1e-2 row bar, and per channel the bound of the bf16 weights:
+    |o - ref| <= (2^-8 + 2e-5) max |v| over the row's retained stored values."""
+    from hwkv_harness import REL_TOL, rel_err
+    torch.cuda.synchronize()
+    rows = np.asarray(rows, dtype=np.int64)
+    ref = r.oracle_rows(layer, b, rows, q_rows)
+    got = out[torch.from_numpy(rows).to(out.device)].cpu().numpy()
+    e = rel_err(got.reshape(-1, r.D), ref.reshape(-1, r.D))
+    assert np.all(np.isfinite(got)) and e <= REL_TOL, f"{what}: max rel err {e}"
+    n = int(rows[-1]) + 1
+    _, vv = r.stored_values(layer, r.kh[layer][b][:n], r.vh[layer][b][:n])
+    vb = np.empty((len(rows), r.Hkv, r.D))
+    for i, t in enumerate(rows):
+        for h in range(r.Hkv):
+            pos = KF.retained_positions(int(t), r.S, r.windows[layer][h])
+            vb[i, h] = np.abs(vv[pos, h]).max(axis=0)
+    vb = np.repeat(vb, r.G, axis=1)
+    ratio = float((np.abs(got - ref) / ((2.0 ** -8 + 2e-5) * vb)).max())
+    assert ratio <= 1.0, f"{what}: error {ratio:.3f} x the weight-rounding bound"
+    return e, ratio
+
+
+@pytest.mark.parametrize("paged", [False, True])
+@pytest.mark.parametrize("D,G,S,w", [(64, 4, 4, 150), (256, 6, 3, 40), (128, 8, 0, 700)])
+def test_fp8_prefill_attention(paged, D, G, S, w):
+    cfg = mini(head_dim=D, n_q_heads=2 * G, n_sinks=S, level_windows=[w, 0], prompt=[700],
+               max_ctx=800, seed=35)
+    r = Run(cfg, n_pages=8 if paged else None, **fmt_args("fp8", 0.013, 0.009, 1, 2))
+    q, qh, out = r.prefill_with_attn(0, 0, chunks=[1, 100, 333, 512])
+    rows = np.arange(700)
+    e, ratio = _check_stored_rows(r, 0, 0, rows, qh[rows], out, f"paged={paged} D={D} G={G}")
+    r.check_layer(0)
+    for st in range(2):            # decode continues from the materialised cache
+        qa, o = r.step(0, fused=bool(st))
+        r.check_out(0, qa, o, f"step {st}")
+    log(f"fp8 prefill paged={paged} D={D} G={G}: max rel err {e:.3e}, {ratio:.3f} of the bound")
+    r.free()
+
+
+def test_prefill_attention_ws_errors_and_bf16_equivalence():
+    dev = torch.device("cuda:0")
+    q = torch.zeros((4, 8, 64), dtype=torch.bfloat16, device=dev)
+    kv = torch.zeros((4, 2, 64), dtype=torch.bfloat16, device=dev)
+    out = torch.zeros((4, 8, 64), dtype=torch.float32, device=dev)
+    pol = hwkv.policy_set(1, 2, 8, 64, 4, [256, 0], [[0, 1]])
+    # binary16: not bf16 values, rejected with or without a workspace
+    c16 = hwkv.cache_alloc(pol, 1, 400, kv_format="f16")
+    ws = torch.zeros(1 << 20, dtype=torch.uint8, device=dev)
+    with pytest.raises(hwkv.HwkvError) as e:
+        hwkv.prefill_attn(c16, 0, 0, 0, q, kv, kv, 0.125, out, ws=ws)
+    assert e.value.code == hwkv.EINVAL
+    c16.free()
+    # fp8: a short workspace is EINVAL and changes nothing
+    c8 = hwkv.cache_alloc(pol, 1, 400, kv_format="fp8")
+    need = hwkv.prefill_attn_workspace_bytes(c8, 4)
+    assert need > 0
+    short = torch.zeros(need - 1, dtype=torch.uint8, device=dev)
+    with pytest.raises(hwkv.HwkvError) as e:
+        hwkv.prefill_attn(c8, 0, 0, 0, q, kv, kv, 0.125, out, ws=short)
+    assert e.value.code == hwkv.EINVAL
+    assert hwkv.cache_seq_len(c8, 0, 0) == 0
+    c8.free()
+    # bf16: the workspace path is the plain path, bit for bit
+    cfg = mini(head_dim=128, n_q_heads=12, level_windows=[90, 0], prompt=[300], seed=36)
+    a, b = Run(cfg), Run(cfg)
+    assert hwkv.prefill_attn_workspace_bytes(a.cache, 300) == 0
+    _, _, oa = a.prefill_with_attn(0, 0, chunks=[77])
+    qd, _ = b.prompt_q(0, 0, 300)
+    kd, vd, _, _ = b.prompt_kv(0, 0, 300)
+    ob = torch.empty_like(oa)
+    for p0, p1 in ((0, 77), (77, 300)):
+        hwkv.prefill_attn(b.cache, 0, 0, p0, qd[p0:p1], kd[p0:p1], vd[p0:p1], b.scale,
+                          ob[p0:p1], ws=torch.zeros(16, dtype=torch.uint8, device=dev))
+        hwkv.prefill_write(b.cache, 0, 0, p0, kd[p0:p1], vd[p0:p1])
+    torch.cuda.synchronize()
+    assert torch.equal(oa, ob)
+    a.free()
+    b.free()
