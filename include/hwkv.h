@@ -383,6 +383,33 @@ int hwkv_calib_replay(int32_t n_kv_heads, int32_t n_q_heads, int32_t head_dim,
                       void *means, const void *ref_full, void *check, void *ws,
                       size_t ws_bytes, void *stream);
 
+/* hwkv_calib_workspace_bytes for hwkv_calib_replay_format: the same, plus
+ * for an fp8 format the trace's K and V staged as bf16 code values
+ * (2 * n_hist * n_kv_heads * head_dim * 2 bytes). */
+int hwkv_calib_workspace_bytes_format(int32_t n_kv_heads, int32_t n_q_heads,
+                                      int32_t head_dim, int32_t n_sinks,
+                                      int64_t n_hist, int64_t n_rows,
+                                      int32_t kv_format, size_t *bytes);
+
+/* hwkv_calib_replay under cache format kv_format.  When the format changes
+ * numerical execution, the full-cache reference, the compressed policy and
+ * the calibration scores all use it (Method, the paragraph after Eq.
+ * nominal-storage): every candidate, the full one included, attends over the
+ * trace's keys and values as a cache of that format stores them, code(x / s)
+ * with the per-KV-head fp32 scales k_scale, v_scale [n_kv_heads] (NULL =
+ * 1.0; fp8 only).  bf16 is hwkv_calib_replay; EINVAL for binary16.  ws of
+ * at least hwkv_calib_workspace_bytes_format bytes. */
+int hwkv_calib_replay_format(int32_t n_kv_heads, int32_t n_q_heads,
+                             int32_t head_dim, int32_t n_sinks,
+                             int32_t n_windows, const int64_t *windows,
+                             int64_t n_hist, const void *k, const void *v,
+                             int64_t n_rows, const int64_t *rows, const void *q,
+                             float scale, void *outs, void *scores, void *means,
+                             const void *ref_full, void *check,
+                             int32_t kv_format, const float *k_scale,
+                             const float *v_scale, void *ws, size_t ws_bytes,
+                             void *stream);
+
 /* Eq. threshold-selection for one layer (host only): for each KV head h, the
  * codebook candidate of lowest cost min(n_sinks + w, ctx) whose mean score
  * means[k][h] is at least tau; equal costs go to the earlier codebook entry;

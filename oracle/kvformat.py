@@ -164,3 +164,15 @@ def attend_values(q, k_vals, v_vals, t, n_sinks, windows, scale):
             p = np.exp(z - z.max(axis=1, keepdims=True))
             out[b, h * G:(h + 1) * G] = (p @ V) / p.sum(axis=1, keepdims=True)
     return out
+
+
+def replay_outputs_values(q_rows, k_vals, v_vals, rows, n_sinks, windows, scale):
+    """Calibration candidate outputs o^(w) over fp64 K/V values (a traced
+    layer as a cache of some format stores it): for every window of
+    ``windows`` (0 = full), the attention of each row at its own position.
+    ``q_rows`` [R, Hq, d], ``k_vals``/``v_vals`` [N, Hkv, d] fp64.  Returns
+    [len(windows), R, Hq, d]."""
+    rows = np.asarray(rows, dtype=np.int64)
+    Hkv = np.asarray(k_vals).shape[1]
+    return np.stack([attend_values(q_rows, [k_vals] * len(rows), [v_vals] * len(rows), rows,
+                                   n_sinks, [int(w)] * Hkv, scale) for w in windows])

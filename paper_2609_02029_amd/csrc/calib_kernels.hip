@@ -103,6 +103,8 @@ __global__ __launch_bounds__(256) void replay_merge(const ReplayMergeArgs a) {
   if (col >= a.n_cols) return;                     // uniform per wave
   const size_t stride = (size_t)a.n_cols * (D + 4);
   const float *p = a.part + (size_t)col * (D + 4);
+  const int h = (col % a.n_q_heads) / a.group;     // the column's kv head
+  const float c2 = a.scale_log2 * a.k_scale[h];
   float M = -1e30f;
   for (int j = 0; j < a.n_splits; ++j) {
     const float *pj = p + (size_t)j * stride;
@@ -115,12 +117,12 @@ __global__ __launch_bounds__(256) void replay_merge(const ReplayMergeArgs a) {
     const float *pj = p + (size_t)j * stride;
     const float lj = pj[1];
     if (!(lj > 0.0f)) continue;                    // uniform: empty split
-    const float f = __builtin_amdgcn_exp2f((pj[0] - M) * a.scale_log2);
+    const float f = __builtin_amdgcn_exp2f((pj[0] - M) * c2);
     L += lj * f;
 #pragma unroll
     for (int i = 0; i < PER; ++i) acc[i] += pj[4 + lane + 64 * i] * f;
   }
-  const float inv = 1.0f / L;
+  const float inv = a.v_scale[h] / L;
 #pragma unroll
   for (int i = 0; i < PER; ++i) a.out[(size_t)col * D + lane + 64 * i] = acc[i] * inv;
 }

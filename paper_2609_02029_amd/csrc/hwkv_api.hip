@@ -1046,6 +1046,24 @@ int hwkv_calib_workspace_bytes(int32_t n_q_heads, int32_t head_dim, int32_t n_si
   return ok();
 }
 
+int hwkv_calib_workspace_bytes_format(int32_t n_kv_heads, int32_t n_q_heads,
+                                      int32_t head_dim, int32_t n_sinks, int64_t n_hist,
+                                      int64_t n_rows, int32_t kv_format, size_t *bytes) {
+  if (!bytes) return fail(HWKV_EINVAL, "bytes is null");
+  if (kv_format != HWKV_KV_BF16 && kv_format != HWKV_KV_FP8_E4M3)
+    return fail(HWKV_EINVAL, "the replay takes bf16 or fp8 formats");
+  if (n_kv_heads < 1 || n_kv_heads > hwkv::kMaxItems)
+    return fail(HWKV_EINVAL, "n_kv_heads must be in [1, 64]");
+  size_t base = 0;
+  const int rc = hwkv_calib_workspace_bytes(n_q_heads, head_dim, n_sinks, n_hist, n_rows, &base);
+  if (rc != HWKV_OK) return rc;
+  if (kv_format == HWKV_KV_FP8_E4M3)       // the staged trace, 256-byte aligned
+    base = (base + 255) / 256 * 256 +
+           2 * (size_t)n_hist * (size_t)n_kv_heads * (size_t)head_dim * 2;
+  *bytes = base;
+  return ok();
+}
+
 int hwkv_calib_replay(int32_t n_kv_heads, int32_t n_q_heads, int32_t head_dim,
                       int32_t n_sinks, int32_t n_windows,
                       const int64_t *windows, int64_t n_hist, const void *k,
@@ -1053,6 +1071,19 @@ int hwkv_calib_replay(int32_t n_kv_heads, int32_t n_q_heads, int32_t head_dim,
                       const void *q, float scale, void *outs, void *scores,
                       void *means, const void *ref_full, void *check, void *ws,
                       size_t ws_bytes, void *stream) {
+  return hwkv_calib_replay_format(n_kv_heads, n_q_heads, head_dim, n_sinks, n_windows, windows,
+                                  n_hist, k, v, n_rows, rows, q, scale, outs, scores, means,
+                                  ref_full, check, HWKV_KV_BF16, nullptr, nullptr, ws, ws_bytes,
+                                  stream);
+}
+
+int hwkv_calib_replay_format(int32_t n_kv_heads, int32_t n_q_heads, int32_t head_dim,
+                             int32_t n_sinks, int32_t n_windows, const int64_t *windows,
+                             int64_t n_hist, const void *k, const void *v, int64_t n_rows,
+                             const int64_t *rows, const void *q, float scale, void *outs,
+                             void *scores, void *means, const void *ref_full, void *check,
+                             int32_t kv_format, const float *k_scale, const float *v_scale,
+                             void *ws, size_t ws_bytes, void *stream) {
   if (n_kv_heads < 1 || n_kv_heads > hwkv::kMaxItems || n_q_heads < 1 ||
       n_q_heads % n_kv_heads != 0 || !valid_group(n_q_heads / n_kv_heads))
     return fail(HWKV_EINVAL, "n_kv_heads in [1, 64] and n_q_heads = G * n_kv_heads "
@@ -1078,11 +1109,28 @@ int hwkv_calib_replay(int32_t n_kv_heads, int32_t n_q_heads, int32_t head_dim,
     return fail(HWKV_EINVAL, "k, v, q, outs, ws (and scores, means) must be non-null");
   if ((ref_full == nullptr) != (check == nullptr))
     return fail(HWKV_EINVAL, "check is required exactly when ref_full is given");
+  if (kv_format != HWKV_KV_BF16 && kv_format != HWKV_KV_FP8_E4M3)
+    return fail(HWKV_EINVAL, "the replay takes bf16 or fp8 formats (binary16 values are "
+                             "not bf16 values)");
+  const bool staged = kv_format == HWKV_KV_FP8_E4M3;
+  if (!staged && (k_scale || v_scale))
+    return fail(HWKV_EINVAL, "scales are for fp8 only");
+  for (const float *sc : {k_scale, v_scale}) {
+    if (!sc) continue;
+    for (int32_t h = 0; h < n_kv_heads; ++h)
+      if (!(std::isnormal(sc[h]) && sc[h] > 0.f))
+        return fail(HWKV_EINVAL, "fp8 scales must be positive, finite and normal");
+  }
   size_t need = 0;
-  if (hwkv_calib_workspace_bytes(n_q_heads, head_dim, n_sinks, n_hist, n_rows, &need) !=
-      HWKV_OK)
+  if (hwkv_calib_workspace_bytes_format(n_kv_heads, n_q_heads, head_dim, n_sinks, n_hist,
+                                        n_rows, kv_format, &need) != HWKV_OK)
     return HWKV_EINVAL;
   if (ws_bytes < need) return fail(HWKV_EINVAL, "workspace too small");
+  float ks[hwkv::kMaxItems], vs[hwkv::kMaxItems];
+  for (int32_t h = 0; h < n_kv_heads; ++h) {
+    ks[h] = k_scale ? k_scale[h] : 1.0f;
+    vs[h] = v_scale ? v_scale[h] : 1.0f;
+  }
   const int32_t G = n_q_heads / n_kv_heads;
   const int64_t per = hwkv::prefill_attn_columns_per_block();
   const int64_t nb = (n_rows * G + per - 1) / per;
@@ -1108,6 +1156,32 @@ int hwkv_calib_replay(int32_t n_kv_heads, int32_t n_q_heads, int32_t head_dim,
   const size_t vec = (size_t)n_rows * n_q_heads * head_dim;
   float *part = reinterpret_cast<float *>(static_cast<uint8_t *>(ws) +
                                           replay_rows_bytes(n_rows));
+  // fp8: the trace's keys and values as a cache of that format stores them,
+  // staged after the partials as bf16 code values
+  const void *k_src = k, *v_src = v;
+  if (staged) {
+    size_t base = 0;
+    hwkv_calib_workspace_bytes(n_q_heads, head_dim, n_sinks, n_hist, n_rows, &base);
+    base = (base + 255) / 256 * 256;
+    uint16_t *kst = reinterpret_cast<uint16_t *>(static_cast<uint8_t *>(ws) + base);
+    uint16_t *vst = kst + (size_t)n_hist * n_kv_heads * head_dim;
+    hwkv::StageChunkArgs ca;
+    std::memset(&ca, 0, sizeof ca);
+    ca.k = static_cast<const uint16_t *>(k);
+    ca.v = static_cast<const uint16_t *>(v);
+    ca.k_out = kst;
+    ca.v_out = vst;
+    for (int32_t h = 0; h < n_kv_heads; ++h) {
+      ca.k_scale[h] = ks[h];
+      ca.v_scale[h] = vs[h];
+    }
+    ca.n_chunks = n_hist * n_kv_heads * (head_dim / 8);
+    ca.n_kv_heads = n_kv_heads;
+    rc = check_device(hwkv::launch_stage_chunk(head_dim, ca, st), "stage launch");
+    if (rc != HWKV_OK) return rc;
+    k_src = kst;
+    v_src = vst;
+  }
   for (int32_t c = 0; c <= n_windows; ++c) {
     hwkv::PrefillAttnArgs a;
     std::memset(&a, 0, sizeof a);
@@ -1133,13 +1207,13 @@ int hwkv_calib_replay(int32_t n_kv_heads, int32_t n_q_heads, int32_t head_dim,
     for (int32_t h = 0; h < n_kv_heads; ++h) {
       a.head[h].window = (int32_t)w;
       a.head[h].pto = -1;          // no cache: every key comes from the trace
-      a.head[h].k_scale = 1.0f;
-      a.head[h].v_scale = 1.0f;
+      a.head[h].k_scale = ks[h];
+      a.head[h].v_scale = vs[h];
       a.head_order[h] = h;
     }
     a.q = static_cast<const uint16_t *>(q);
-    a.k = static_cast<const uint16_t *>(k);
-    a.v = static_cast<const uint16_t *>(v);
+    a.k = static_cast<const uint16_t *>(k_src);
+    a.v = static_cast<const uint16_t *>(v_src);
     a.out = static_cast<float *>(outs) + (size_t)c * vec;
     a.rows = static_cast<const int32_t *>(ws);
     a.p0 = 0;
@@ -1158,11 +1232,18 @@ int hwkv_calib_replay(int32_t n_kv_heads, int32_t n_q_heads, int32_t head_dim,
     if (rc != HWKV_OK) return rc;
     if (n_splits > 1) {
       hwkv::ReplayMergeArgs ma;
+      std::memset(&ma, 0, sizeof ma);
       ma.part = part;
       ma.out = a.out;
       ma.n_splits = (int32_t)n_splits;
       ma.n_cols = (int32_t)(n_rows * n_q_heads);
+      ma.n_q_heads = n_q_heads;
+      ma.group = G;
       ma.scale_log2 = a.scale_log2;
+      for (int32_t h = 0; h < n_kv_heads; ++h) {
+        ma.k_scale[h] = ks[h];
+        ma.v_scale[h] = vs[h];
+      }
       rc = check_device(hwkv::launch_replay_merge(head_dim, ma, st), "calib merge launch");
       if (rc != HWKV_OK) return rc;
     }

@@ -222,7 +222,10 @@ struct ReplayMergeArgs {
   const float *part;             // [n_splits][n_cols][D + 4]
   float *out;                    // [n_cols][D]
   int32_t n_splits, n_cols;
+  int32_t n_q_heads, group;      // column c is q head c % n_q_heads
   float scale_log2;
+  float k_scale[kMaxItems];      // per kv head: the stored keys' logit scale
+  float v_scale[kMaxItems];      //   and the stored values' scale (fp8)
 };
 hipError_t launch_replay_merge(int D, const ReplayMergeArgs &a, hipStream_t s);
 constexpr int kReplayTilesPerSplit = 128;   // 32-key tiles per split, at most

@@ -72,6 +72,11 @@ SYMBOLS = {
     "hwkv_calib_workspace_bytes": ([_i32, _i32, _i32, _i64, _i64, _P(_sz)], ctypes.c_int),
     "hwkv_calib_replay": ([_i32, _i32, _i32, _i32, _i32, _vp, _i64, _vp, _vp, _i64, _vp, _vp,
                            _flt, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp], ctypes.c_int),
+    "hwkv_calib_workspace_bytes_format": ([_i32, _i32, _i32, _i32, _i64, _i64, _i32, _P(_sz)],
+                                          ctypes.c_int),
+    "hwkv_calib_replay_format": ([_i32, _i32, _i32, _i32, _i32, _vp, _i64, _vp, _vp, _i64, _vp, _vp,
+                                  _flt, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp, _vp, _sz, _vp],
+                                 ctypes.c_int),
     "hwkv_calib_select": ([_i32, _i32, _vp, _i32, _i64, _vp, _dbl, _vp, _P(_dbl)], ctypes.c_int),
     "hwkv_budget_select": ([_i32, _vp, _vp, _dbl, _P(_i32)], ctypes.c_int),
     "hwkv_policy_shape": ([_vp, _P(_i32), _P(_i32), _P(_i32), _P(_i32), _P(_i32), _P(_i32)],
@@ -405,10 +410,18 @@ def decode_timing_read(cache):
     return sp.value, mg.value, n.value
 
 
-def calib_workspace_bytes(n_q_heads, head_dim, n_sinks, n_hist, n_rows):
+def calib_workspace_bytes(n_q_heads, head_dim, n_sinks, n_hist, n_rows, n_kv_heads=None,
+                          kv_format="bf16"):
+    """Workspace of the replay; an fp8 ``kv_format`` also needs ``n_kv_heads``
+    (the staged trace)."""
     n = _sz()
-    _check(_lib.hwkv_calib_workspace_bytes(int(n_q_heads), int(head_dim), int(n_sinks),
-                                           int(n_hist), int(n_rows), ctypes.byref(n)))
+    if kv_format == "bf16":
+        _check(_lib.hwkv_calib_workspace_bytes(int(n_q_heads), int(head_dim), int(n_sinks),
+                                               int(n_hist), int(n_rows), ctypes.byref(n)))
+    else:
+        _check(_lib.hwkv_calib_workspace_bytes_format(
+            int(n_kv_heads), int(n_q_heads), int(head_dim), int(n_sinks), int(n_hist),
+            int(n_rows), _fmt_code(kv_format), ctypes.byref(n)))
     return n.value
 
 
@@ -418,13 +431,16 @@ def _i64_array(x):
 
 
 def calib_replay(k, v, rows, q, windows, n_sinks, scale, outs, scores, means, ws,
-                 ref_full=None, check=None, stream=None):
+                 ref_full=None, check=None, stream=None, kv_format="bf16", k_scale=None,
+                 v_scale=None):
     """Candidate replay of one traced layer (see ``hwkv_calib_replay``).
 
     ``k``, ``v``: bf16 [n_hist, Hkv, D]; ``q``: bf16 [R, Hq, D]; ``rows``:
     R increasing positions (host); ``windows``: the finite codebook in
     order; ``outs``: fp32 [K + 1, R, Hq, D]; ``scores``: fp32 [K, R, Hq];
-    ``means``: fp32 [K, Hkv]; ``ws``: device workspace tensor."""
+    ``means``: fp32 [K, Hkv]; ``ws``: device workspace tensor.  ``kv_format``
+    "fp8": attend over the trace as an fp8 cache stores it, with per-KV-head
+    ``k_scale``, ``v_scale`` (host arrays or scalars; None = 1.0)."""
     n_hist, hkv, d = k.shape
     R, hq, _ = q.shape
     w = _i64_array(windows)
@@ -436,13 +452,19 @@ def calib_replay(k, v, rows, q, windows, n_sinks, scale, outs, scores, means, ws
         raise ValueError("outs must be [n_windows + 1, n_rows, n_q_heads, head_dim]")
     if K and (tuple(scores.shape) != (K, R, hq) or tuple(means.shape) != (K, hkv)):
         raise ValueError("scores must be [n_windows, n_rows, n_q_heads], means [n_windows, n_kv_heads]")
-    _check(_lib.hwkv_calib_replay(
+    import numpy as np
+    sc = lambda x: None if x is None else np.ascontiguousarray(
+        np.broadcast_to(np.asarray(x, dtype=np.float32), (hkv,)))
+    ks, vs = sc(k_scale), sc(v_scale)
+    _check(_lib.hwkv_calib_replay_format(
         hkv, hq, d, int(n_sinks), K, w.ctypes.data if K else None, n_hist,
         _dev(k, "bfloat16", "k"), _dev(v, "bfloat16", "v"), R, r.ctypes.data,
         _dev(q, "bfloat16", "q"), float(scale), _dev(outs, "float32", "outs"),
         _dev(scores, "float32", "scores") if K else None,
         _dev(means, "float32", "means") if K else None,
         _dev(ref_full, "float32", "ref_full"), _dev(check, "float32", "check"),
+        _fmt_code(kv_format), None if ks is None else ks.ctypes.data_as(_vp),
+        None if vs is None else vs.ctypes.data_as(_vp),
         _dev(ws, "uint8", "ws"), ws.numel(), _stream(stream)))
 
 

@@ -34,21 +34,25 @@ def _gpu():
     torch.cuda.set_device(0)
 
 
-def replay(k, v, q, rows, windows, S, scale, ref_full=None, dev="cuda:0"):
-    """Runs hwkv_calib_replay on device tensors; returns host arrays."""
+def replay(k, v, q, rows, windows, S, scale, ref_full=None, dev="cuda:0", kv_format="bf16",
+           k_scale=None, v_scale=None):
+    """Runs hwkv_calib_replay (hwkv_calib_replay_format for another format)
+    on device tensors; returns host arrays."""
     R, Hq, D = q.shape
     Hkv = k.shape[1]
     K = len(windows)
     outs = torch.full((K + 1, R, Hq, D), float("nan"), dtype=torch.float32, device=dev)
     scores = torch.full((max(K, 1), R, Hq), float("nan"), dtype=torch.float32, device=dev)[:K]
     means = torch.full((max(K, 1), Hkv), float("nan"), dtype=torch.float32, device=dev)[:K]
-    ws = torch.zeros(hwkv.calib_workspace_bytes(Hq, D, S, k.shape[0], R), dtype=torch.uint8,
-                     device=dev)
+    ws = torch.zeros(hwkv.calib_workspace_bytes(Hq, D, S, k.shape[0], R, n_kv_heads=Hkv,
+                                                kv_format=kv_format),
+                     dtype=torch.uint8, device=dev)
     check = None
     if ref_full is not None:
         check = torch.full((R, Hq), float("nan"), dtype=torch.float32, device=dev)
     hwkv.calib_replay(k, v, rows, q, windows, S, scale, outs, scores.contiguous(),
-                      means.contiguous(), ws, ref_full=ref_full, check=check)
+                      means.contiguous(), ws, ref_full=ref_full, check=check,
+                      kv_format=kv_format, k_scale=k_scale, v_scale=v_scale)
     torch.cuda.synchronize()
     res = dict(outs=outs.cpu().numpy().astype(np.float64),
                scores=scores.cpu().numpy().astype(np.float64),
@@ -219,3 +223,66 @@ def test_calib128k_workload():
         got, _ = hwkv.calib_select(res["means"], windows, S, N, tau)
         assert got == oracle.select_windows(res["means"], windows, S, N, tau)
     log(f"calib128k: outputs {ratio:.3f} of the (global-max) bound; means {res['means'].round(4)}")
+
+
+# ---------------------------------------------------------------------------
+# the replay under an fp8 cache format: every candidate, the full one
+# included, over the trace as an fp8 cache stores it
+# ---------------------------------------------------------------------------
+def _fp8_values(x_bits, scales):
+    from oracle import kvformat as KF
+    return np.stack([KF.values(KF.store(x_bits[:, h], "fp8", scales[h]), "fp8", scales[h])
+                     for h in range(x_bits.shape[1])], axis=1)
+
+
+def _vmax_values(vals, rows, windows, S):
+    av = np.abs(vals)
+    pos = np.arange(av.shape[0])
+    out = np.empty((len(windows) + 1, len(rows), av.shape[1], av.shape[2]))
+    for ki, w in enumerate(list(windows) + [0]):
+        for i, t in enumerate(rows):
+            keep = pos <= t
+            if w:
+                keep &= (pos < S) | (pos >= t + 1 - w)
+            out[ki, i] = av[keep].max(axis=0)
+    return out
+
+
+@pytest.mark.parametrize("N,windows,D,G", [(600, [16, 64, 200], 64, 4),
+                                           (600, [16, 64, 200], 256, 6),
+                                           (9000, [100, 5000], 128, 4)])
+def test_replay_fp8(N, windows, D, G):
+    from oracle import kvformat as KF
+    S = 4
+    kh, vh, qh, rows = small_case(37, N, 2, G, D, windows, S, extra_rows=24)
+    ks = np.array([0.013, 0.021], dtype=np.float32)
+    vs = np.array([0.009, 0.017], dtype=np.float32)
+    scale = 1.0 / math.sqrt(D)
+    res = replay(up(kh, "cuda:0"), up(vh, "cuda:0"), up(qh, "cuda:0"), rows, windows, S, scale,
+                 kv_format="fp8", k_scale=ks, v_scale=vs)
+    kv, vv = _fp8_values(kh, ks), _fp8_values(vh, vs)
+    ref = KF.replay_outputs_values(KF.bf16_values(qh), kv, vv, rows, S, list(windows) + [0],
+                                   scale)
+    ratio, serr = check_all(res, ref, kh, vh, rows, windows, S, G, f"fp8 N={N} D={D} G={G}",
+                            vmax=_vmax_values(vv, rows, windows, S))
+    log(f"replay fp8 N={N} D={D} G={G}: outputs {ratio:.3f} of the bound, score error {serr:.2e}")
+
+
+def test_replay_format_errors():
+    dev = "cuda:0"
+    kh = up(W.normal_bf16((64, 1, 64), 38, 0, W.K, 0), dev)
+    qh = up(W.normal_bf16((2, 2, 64), 38, 0, W.Q_PROMPT, 0), dev)
+    outs = torch.zeros((2, 2, 2, 64), dtype=torch.float32, device=dev)
+    sc = torch.zeros((1, 2, 2), dtype=torch.float32, device=dev)
+    mn = torch.zeros((1, 1), dtype=torch.float32, device=dev)
+    ws = torch.zeros(1 << 22, dtype=torch.uint8, device=dev)
+    for kw in (dict(kv_format="f16"), dict(kv_format="bf16", k_scale=0.5),
+               dict(kv_format="fp8", k_scale=0.0), dict(kv_format="fp8", v_scale=float("inf"))):
+        with pytest.raises(hwkv.HwkvError) as e:
+            hwkv.calib_replay(kh, kh, [10, 20], qh, [8], 0, 0.125, outs, sc, mn, ws, **kw)
+        assert e.value.code == hwkv.EINVAL, kw
+    need = hwkv.calib_workspace_bytes(2, 64, 0, 64, 2, n_kv_heads=1, kv_format="fp8")
+    assert need > hwkv.calib_workspace_bytes(2, 64, 0, 64, 2)
+    with pytest.raises(hwkv.HwkvError):
+        hwkv.calib_replay(kh, kh, [10, 20], qh, [8], 0, 0.125, outs, sc, mn, ws[: need - 1],
+                          kv_format="fp8")
