@@ -295,3 +295,40 @@ def test_batch16_workload_full_size():
         r.check_layer(l)
     log(f"batch16: max rel err {worst:.3e}")
     r.free()
+
+
+# ---------------------------------------------------------------------------
+# the largest documented capacity: one full unit of 4,194,240 rows at
+# head_dim 256 (2,147,450,880 bytes of K or V, just under the 2^31 byte
+# offsets the kernels use), filled to its last row
+# ---------------------------------------------------------------------------
+@pytest.mark.timeout(1200)
+def test_largest_capacity():
+    cap = 4194240
+    assert (cap + 63) // 64 * 64 * 256 * 2 < 2 ** 31
+    cfg = dict(name="maxcap", seed=19, n_layers=1, batch=1, n_q_heads=2, n_kv_heads=1,
+               head_dim=256, n_sinks=0, level_windows=[0], levels=[[0]],
+               prompt=[cap - 24], steps=24, max_ctx=cap)
+    r = Run(cfg, device_gen=True)
+    with timed("max capacity prefill"):
+        r.prefill(0, 0, chunks=[1 << 20, 2 << 20, 3 << 20])
+    worst = 0.0
+    with timed("max capacity 24 steps"):
+        for st in range(24):
+            qa, out = r.step(0, fused=bool(st % 2))
+            if st in (0, 23):
+                worst = max(worst, r.check_out(0, qa, out, f"max capacity step {st}"))
+    assert hwkv.cache_seq_len(r.cache, 0, 0) == cap
+    with timed("max capacity residency"):
+        r.check_layer(0)
+    dev = torch.device("cuda:0")
+    kn = torch.zeros((1, 1, 256), dtype=torch.bfloat16, device=dev)
+    with pytest.raises(hwkv.HwkvError) as e:
+        hwkv.append(r.cache, 0, kn, kn)
+    assert e.value.code == hwkv.ECAPACITY
+    log(f"max capacity: max rel err {worst:.3e}")
+    r.free()
+    # one row more does not fit the 32-bit offsets
+    pol = hwkv.policy_set(1, 1, 2, 256, 0, [0], [[0]])
+    with pytest.raises(hwkv.HwkvError):
+        hwkv.cache_bytes(pol, 1, cap + 64)
