@@ -199,9 +199,10 @@ def main():
     gbs = bytes_per_step / (ms_per_step * 1e-3) / 1e9
 
     # Kernel-timing region: the next K steps again, with the library
-    # recording HIP events on the same stream around each decode call's
-    # split kernel (the dominant kernel: it streams every resident K/V byte)
-    # and its merge kernel.
+    # launching each decode call's split kernel (the dominant kernel: it
+    # streams every resident K/V byte) and its merge kernel with start and
+    # stop HIP events on the same stream, which take the kernels' own start
+    # and end times.
     hwkv.decode_timing(cache, True)
     for i in range(args.steps):
         run_step(args.warmup + args.steps + i)

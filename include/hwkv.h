@@ -457,11 +457,12 @@ int hwkv_policy_deserialize(const char *buf, size_t len, hwkv_policy **out,
                             double *floor);
 
 /* Kernel timing, for profiling.  While enabled (enable != 0) on a cache,
- * every hwkv_decode_attn / hwkv_append_decode_attn call records HIP events
- * on its stream before its split kernel, between the split and the merge
- * kernel, and after the merge kernel (per launch group).  The events add
- * work to the stream; leave timing disabled when measuring end-to-end time.
- * Disabling keeps what was recorded. */
+ * every hwkv_decode_attn / hwkv_append_decode_attn call launches its split
+ * and merge kernels with start and stop HIP events (hipExtLaunchKernel), per
+ * launch group, so that each event pair spans the kernel's own execution and
+ * not its dispatch.  Timed launches take profiling work on the stream; leave
+ * timing disabled when measuring end-to-end time.  Disabling keeps what was
+ * recorded. */
 int hwkv_decode_timing(hwkv_cache *cache, int32_t enable);
 
 /* Waits for the recorded calls to complete and returns the summed durations

@@ -7,11 +7,11 @@ namespace hwkv {
 
 // Instantiated in the per-format sources.
 extern template hipError_t launch_decode_split_fmt<HWKV_KV_BF16>(
-    int, int, const DecodeArgs &, int, hipStream_t);
+    int, int, const DecodeArgs &, int, hipStream_t, hipEvent_t, hipEvent_t);
 extern template hipError_t launch_decode_split_fmt<HWKV_KV_F16>(
-    int, int, const DecodeArgs &, int, hipStream_t);
+    int, int, const DecodeArgs &, int, hipStream_t, hipEvent_t, hipEvent_t);
 extern template hipError_t launch_decode_split_fmt<HWKV_KV_FP8_E4M3>(
-    int, int, const DecodeArgs &, int, hipStream_t);
+    int, int, const DecodeArgs &, int, hipStream_t, hipEvent_t, hipEvent_t);
 
 namespace {
 
@@ -164,16 +164,17 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine(
 
 template <int D, int G>
 hipError_t launch_combine_dg(const DecodeArgs &a, int n_combine,
-                             hipStream_t s) {
-  hipLaunchKernelGGL((decode_combine<D, G>), dim3(n_combine),
-                     dim3(kCombineThreads), 0, s, a);
+                             hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  hipExtLaunchKernelGGL((decode_combine<D, G>), dim3(n_combine),
+                        dim3(kCombineThreads), 0, s, e0, e1, 0, a);
   return hipGetLastError();
 }
 
 template <int D, int G>
 struct CombineLaunch {
-  static hipError_t run(const DecodeArgs &a, int n, hipStream_t s) {
-    return launch_combine_dg<D, G>(a, n, s);
+  static hipError_t run(const DecodeArgs &a, int n, hipStream_t s, hipEvent_t e0,
+                        hipEvent_t e1) {
+    return launch_combine_dg<D, G>(a, n, s, e0, e1);
   }
 };
 
@@ -185,22 +186,23 @@ int decode_combine_blocks_per_item(int D, int G) {
 }
 
 hipError_t launch_decode_split(int fmt, int D, int G, const DecodeArgs &a,
-                               int n_splits, hipStream_t s) {
+                               int n_splits, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   switch (fmt) {
     case HWKV_KV_BF16:
-      return launch_decode_split_fmt<HWKV_KV_BF16>(D, G, a, n_splits, s);
+      return launch_decode_split_fmt<HWKV_KV_BF16>(D, G, a, n_splits, s, e0, e1);
     case HWKV_KV_F16:
-      return launch_decode_split_fmt<HWKV_KV_F16>(D, G, a, n_splits, s);
+      return launch_decode_split_fmt<HWKV_KV_F16>(D, G, a, n_splits, s, e0, e1);
     case HWKV_KV_FP8_E4M3:
-      return launch_decode_split_fmt<HWKV_KV_FP8_E4M3>(D, G, a, n_splits, s);
+      return launch_decode_split_fmt<HWKV_KV_FP8_E4M3>(D, G, a, n_splits, s, e0, e1);
     default:
       return hipErrorInvalidValue;
   }
 }
 
 hipError_t launch_decode_combine(int D, int G, const DecodeArgs &a,
-                                 int n_combine_blocks, hipStream_t s) {
-  return dispatch_dg<CombineLaunch>(D, G, a, n_combine_blocks, s);
+                                 int n_combine_blocks, hipStream_t s, hipEvent_t e0,
+                                 hipEvent_t e1) {
+  return dispatch_dg<CombineLaunch>(D, G, a, n_combine_blocks, s, e0, e1);
 }
 
 }  // namespace hwkv

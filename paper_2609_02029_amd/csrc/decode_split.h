@@ -49,6 +49,8 @@
 // out = sum acc_j 2^(m_j - m*) / l*.
 #pragma once
 
+#include <hip/hip_ext.h>
+
 #include <utility>
 
 #include "hwkv_internal.h"
@@ -672,9 +674,10 @@ template <int F>
 struct SplitLaunch {
   template <int D, int G>
   struct At {
-    static hipError_t run(const DecodeArgs &a, int n, hipStream_t s) {
-      hipLaunchKernelGGL((decode_split<D, G, F>), dim3(n), dim3(kWaves * 64), 0,
-                         s, a);
+    static hipError_t run(const DecodeArgs &a, int n, hipStream_t s, hipEvent_t e0,
+                          hipEvent_t e1) {
+      hipExtLaunchKernelGGL((decode_split<D, G, F>), dim3(n), dim3(kWaves * 64), 0,
+                            s, e0, e1, 0, a);
       return hipGetLastError();
     }
   };
@@ -684,8 +687,9 @@ struct SplitLaunch {
 
 template <int F>
 hipError_t launch_decode_split_fmt(int D, int G, const DecodeArgs &a,
-                                   int n_splits, hipStream_t s) {
-  return dispatch_dg<SplitLaunch<F>::template At>(D, G, a, n_splits, s);
+                                   int n_splits, hipStream_t s, hipEvent_t e0,
+                                   hipEvent_t e1) {
+  return dispatch_dg<SplitLaunch<F>::template At>(D, G, a, n_splits, s, e0, e1);
 }
 
 }  // namespace hwkv

@@ -3,6 +3,6 @@
 #include "decode_split.h"
 
 namespace hwkv {
-template hipError_t launch_decode_split_fmt<HWKV_KV_FP8_E4M3>(int, int, const DecodeArgs &,
-                                                   int, hipStream_t);
+template hipError_t launch_decode_split_fmt<HWKV_KV_FP8_E4M3>(int, int, const DecodeArgs &, int,
+                                                              hipStream_t, hipEvent_t, hipEvent_t);
 }  // namespace hwkv

@@ -252,16 +252,17 @@ int check_device(hipError_t e, const char *what) {
   return fail(HWKV_EDEVICE, std::string(what) + ": " + hipGetErrorString(e));
 }
 
-// Records the next timing event of the cache on stream s.
-int record_event(hwkv_cache *c, hipStream_t s) {
+// The next timing event of the cache (created on first use, then reused);
+// the launch it is handed to records it.
+int next_event(hwkv_cache *c, hipEvent_t *e) {
   if (c->ev_used == c->ev_pool.size()) {
-    hipEvent_t e;
-    const int rc = check_device(hipEventCreate(&e), "hipEventCreate");
+    hipEvent_t ne;
+    const int rc = check_device(hipEventCreate(&ne), "hipEventCreate");
     if (rc != HWKV_OK) return rc;
-    c->ev_pool.push_back(e);
+    c->ev_pool.push_back(ne);
   }
-  return check_device(hipEventRecord(c->ev_pool[c->ev_used++], s),
-                      "hipEventRecord");
+  *e = c->ev_pool[c->ev_used++];
+  return HWKV_OK;
 }
 
 int take_pages(hwkv_cache *c, int32_t layer,
@@ -564,18 +565,19 @@ int decode_impl(hwkv_cache *c, int32_t layer, const void *k_new,
     a.scale_log2 = scale * 1.4426950408889634f;
     const int n_combine =
         cnt * hwkv::decode_combine_blocks_per_item(p.head_dim, G);
+    // timing: each kernel's own start and end (four events per launch group)
+    hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
     int rc;
-    if (c->timing && (rc = record_event(c, s)) != HWKV_OK) return rc;
+    for (int e = 0; c->timing && e < 4; ++e)
+      if ((rc = next_event(c, &ev[e])) != HWKV_OK) return rc;
     rc = check_device(
-        hwkv::launch_decode_split(c->fmt, p.head_dim, G, a, splits, s),
+        hwkv::launch_decode_split(c->fmt, p.head_dim, G, a, splits, s, ev[0], ev[1]),
         "decode split launch");
     if (rc != HWKV_OK) return rc;  // earlier launches of this call may run
-    if (c->timing && (rc = record_event(c, s)) != HWKV_OK) return rc;
     rc = check_device(
-        hwkv::launch_decode_combine(p.head_dim, G, a, n_combine, s),
+        hwkv::launch_decode_combine(p.head_dim, G, a, n_combine, s, ev[2], ev[3]),
         "decode merge launch");
     if (rc != HWKV_OK) return rc;
-    if (c->timing && (rc = record_event(c, s)) != HWKV_OK) return rc;
     ws_split += splits;
   }
   if (fused)
@@ -1619,19 +1621,19 @@ int hwkv_decode_timing_read(hwkv_cache *c, double *split_ms, double *merge_ms,
   if (!c || !split_ms || !merge_ms || !launches)
     return fail(HWKV_EINVAL, "null argument");
   double sp = 0.0, mg = 0.0;
-  const size_t n = c->ev_used / 3;
+  const size_t n = c->ev_used / 4;
   if (n > 0) {
     int rc = check_device(hipEventSynchronize(c->ev_pool[c->ev_used - 1]),
                           "hipEventSynchronize");
     if (rc != HWKV_OK) return rc;
     for (size_t i = 0; i < n; ++i) {
       float t0 = 0.f, t1 = 0.f;
-      rc = check_device(hipEventElapsedTime(&t0, c->ev_pool[3 * i],
-                                            c->ev_pool[3 * i + 1]),
+      rc = check_device(hipEventElapsedTime(&t0, c->ev_pool[4 * i],
+                                            c->ev_pool[4 * i + 1]),
                         "hipEventElapsedTime");
       if (rc != HWKV_OK) return rc;
-      rc = check_device(hipEventElapsedTime(&t1, c->ev_pool[3 * i + 1],
-                                            c->ev_pool[3 * i + 2]),
+      rc = check_device(hipEventElapsedTime(&t1, c->ev_pool[4 * i + 2],
+                                            c->ev_pool[4 * i + 3]),
                         "hipEventElapsedTime");
       if (rc != HWKV_OK) return rc;
       sp += t0;

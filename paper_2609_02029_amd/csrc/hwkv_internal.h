@@ -157,14 +157,19 @@ struct PrefillAttnArgs {
 constexpr int kPrefillWaves = HWKV_PREFILL_WAVES;
 
 // Launchers (return the launch status).  D in {64, 128, 256}; G in
-// {1, 2, 4, 6, 8}; fmt one of the HWKV_KV_* formats.
+// {1, 2, 4, 6, 8}; fmt one of the HWKV_KV_* formats.  Non-null events e0, e1
+// take the kernel's own start and end times (hipExtLaunchKernel), so their
+// elapsed time excludes the dispatch of the launch.
 hipError_t launch_decode_split(int fmt, int D, int G, const DecodeArgs &a,
-                               int n_splits, hipStream_t s);
+                               int n_splits, hipStream_t s, hipEvent_t e0 = nullptr,
+                               hipEvent_t e1 = nullptr);
 template <int F>
 hipError_t launch_decode_split_fmt(int D, int G, const DecodeArgs &a,
-                                   int n_splits, hipStream_t s);
+                                   int n_splits, hipStream_t s, hipEvent_t e0,
+                                   hipEvent_t e1);
 hipError_t launch_decode_combine(int D, int G, const DecodeArgs &a,
-                                 int n_combine_blocks, hipStream_t s);
+                                 int n_combine_blocks, hipStream_t s,
+                                 hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
 int decode_split_tokens();       // tokens per split (a multiple of 64)
 int decode_combine_blocks_per_item(int D, int G);  // merge workgroups
 hipError_t launch_prefill_write(int fmt, int D, const WriteArgs &a,

@@ -276,8 +276,11 @@ void prefill_attn(const PrefillAttnArgs a) {
     }
   };
 
-  // logit scale, base 2, with the stored keys' scale (1 but for fp8 caches)
-  const float c2 = a.scale_log2 * hd.k_scale;
+  // logit scale, base 2, with the stored keys' scale (1 but for fp8 caches);
+  // uniform, so kept in a scalar register (the 256-channel kernel has no
+  // vector register to spare for it)
+  const float c2 = __builtin_bit_cast(
+      float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, a.scale_log2 * hd.k_scale)));
   const float tau = 8.0f / c2;                  // lazy-rescale slack (raw units)
   float m = -1e30f;                              // running shift (raw units)
   float l = 0.0f;                                // this lane's partial sum
