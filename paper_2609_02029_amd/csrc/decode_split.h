@@ -90,6 +90,9 @@ __device__ __forceinline__ void static_for(F &&f) {
 #ifndef HWKV_DECODE_MINWAVES
 #define HWKV_DECODE_MINWAVES 4
 #endif
+#ifndef HWKV_DECODE_ROT
+#define HWKV_DECODE_ROT 7  // a tile's starting step: (ROT * tile) mod steps
+#endif
 constexpr int kWaves = HWKV_DECODE_WAVES;        // waves per workgroup
 constexpr int kTilesPerWave = HWKV_DECODE_TPW;   // 64-slot tiles per wave
 constexpr int kPrefetch = HWKV_DECODE_PREFETCH;  // 16-byte loads in flight
@@ -277,7 +280,7 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
   const int nsplit = it.split_begin[item + 1] - it.split_begin[item];
   const int nv = it.n_valid[item];
   const int new_slot = it.new_slot[item];
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int c8 = lane % NC;
   const int rsub = lane / NC;
@@ -357,27 +360,40 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
   // is consumed with PF loads always in flight: the V loads of a tile are on
   // their way while its last K chunks and the softmax are computed, and the
   // first K loads of the wave's next tile while its last V rows are.
+  //
+  // The wave walks its tile's K chunks, and its V rows, from a tile-dependent
+  // starting step and wraps round (the q chunks and the weights follow).
+  // Every wave starts at the same moment; without the rotation all of them
+  // would read the same offset of tiles a whole tile apart at each step,
+  // which crowds their requests onto a few HBM channels.  The V steps keep
+  // the fp8 token pairs (steps 2s, 2s + 1) together.
+  auto rot_k = [](int tile) { return (HWKV_DECODE_ROT * tile) & (NC - 1); };
+  auto rot_v = [](int tile) { return (HWKV_DECODE_ROT * tile) & (NC - 1) & (PAIR ? ~1 : ~0); };
   Chunk buf[PF];
   int t = wl;
+  int rk = rot_k(t), rv = rot_v(t);
   int kofs = (t * 64 - r0) * D * EB + lane * LB;
   if (t < n_tiles) static_for<PF>([&](auto jc) {
-    buf[jc.value] = bload_chunk<F>(krs, kofs + jc.value * 64 * LB);
+    buf[jc.value] = bload_chunk<F>(krs, kofs + ((jc.value + rk) & (NC - 1)) * 64 * LB);
   });
   for (int k = 0; k < kTilesPerWave && t < n_tiles; ++k) {
     const int slot0 = t * 64;
     const int slot = slot0 + lane;
     const int tn = t + nw;
     const bool has_next = k + 1 < kTilesPerWave && tn < n_tiles;
+    int rk_n = rot_k(tn);
     int vofs = (slot0 - r0 + rsub) * D * EB + c8 * LB;
     int kofs_n = (tn * 64 - r0) * D * EB + lane * LB;
     uint64_t qaddr = (uint64_t)qc;
-    // load j of this tile's stream: K chunk j, or V step j - NC
+    // load j of this tile's stream: K chunk (j + rk) mod NC, or V step
+    // (j - NC + rv) mod NC; the row offset stays in the range-checked part
+    // of the buffer address, so V rows past n_valid still read as zero
     auto ld = [&](auto jc) -> Chunk {
       constexpr int j = decltype(jc)::value;
       if constexpr (j < NC)
-        return bload_chunk<F>(krs, kofs + j * 64 * LB);
+        return bload_chunk<F>(krs, kofs + ((j + rk) & (NC - 1)) * 64 * LB);
       else
-        return bload_chunk<F>(vrs, vofs + (j - NC) * RPS * D * EB);
+        return bload_chunk<F>(vrs, vofs + ((j - NC + rv) & (NC - 1)) * RPS * D * EB);
     };
     float s[G];
 #pragma unroll
@@ -394,20 +410,21 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
     {
       const cu32x4_t *q0 = (const cu32x4_t *)qaddr;
 #pragma unroll
-      for (int h = 0; h < G; ++h) qc[h] = q0[h * NC];
+      for (int h = 0; h < G; ++h) qc[h] = q0[h * NC + rk];
     }
     static_for<NC>([&](auto jc) {
       constexpr int j = decltype(jc)::value;
 #pragma unroll
       for (int h = 0; h < G; ++h) asm volatile("" : "+v"(s[h]));
-      asm volatile("" : "+v"(kofs), "+v"(vofs), "+s"(qaddr));
+      asm volatile("" : "+v"(kofs), "+v"(vofs), "+s"(qaddr), "+s"(rk), "+s"(rv));
       const Chunk x = buf[j % PF];
       buf[j % PF] = ld(std::integral_constant<int, j + PF>{});
       u32x4_t qn[G];
       if constexpr (j + 1 < NC) {
         const cu32x4_t *qj = (const cu32x4_t *)qaddr;
+        const int qi = (j + 1 + rk) & (NC - 1);
 #pragma unroll
-        for (int h = 0; h < G; ++h) qn[h] = qj[h * NC + j + 1];
+        for (int h = 0; h < G; ++h) qn[h] = qj[h * NC + qi];
       }
       if constexpr (F == HWKV_KV_BF16) {
 #pragma unroll
@@ -480,7 +497,8 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
       if constexpr (jn < 2 * NC) {
         buf[j % PF] = ld(std::integral_constant<int, jn>{});
       } else {
-        if (has_next) buf[j % PF] = bload_chunk<F>(krs, kofs_n + (jn - 2 * NC) * 64 * LB);
+        if (has_next)
+          buf[j % PF] = bload_chunk<F>(krs, kofs_n + ((jn - 2 * NC + rk_n) & (NC - 1)) * 64 * LB);
       }
     };
     if constexpr (PAIR) {
@@ -500,13 +518,14 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
 #pragma unroll
           for (int e = 0; e < 8; e += 2)
             asm volatile("" : "+v"(acc[h][e]), "+v"(acc[h][e + 1]));
-        asm volatile("" : "+v"(vofs), "+v"(kofs_n), "+v"(pofs));
+        asm volatile("" : "+v"(vofs), "+v"(kofs_n), "+v"(pofs), "+s"(rv), "+s"(rk_n));
         const Chunk x = buf[j % PF];
         issue(std::integral_constant<int, j>{});
         if constexpr (js % 2 == 0) {
           xp = x;
+          const int pi = ((js + rv) & (NC - 1)) / 2;   // the step pair's weights
 #pragma unroll
-          for (int h = 0; h < G; ++h) pw[h] = pp[pofs + (js / 2) * RPS * G + h];
+          for (int h = 0; h < G; ++h) pw[h] = pp[pofs + pi * RPS * G + h];
         } else {
           const uint32_t w0 = __builtin_amdgcn_perm(x.x, xp.x, 0x05010400u);
           const uint32_t w1 = __builtin_amdgcn_perm(x.x, xp.x, 0x07030602u);
@@ -531,7 +550,7 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
     int pofs = rsub * PST;
     float pc[G];
 #pragma unroll
-    for (int h = 0; h < G; ++h) pc[h] = pl[pofs + h];
+    for (int h = 0; h < G; ++h) pc[h] = pl[pofs + (rv & (NC - 1)) * RPS * PST + h];
     static_for<NC>([&](auto jc) {
       constexpr int js = decltype(jc)::value;
       constexpr int j = NC + js;
@@ -540,13 +559,14 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
 #pragma unroll
         for (int e = 0; e < 8; e += 2)
           asm volatile("" : "+v"(acc[h][e]), "+v"(acc[h][e + 1]));
-      asm volatile("" : "+v"(vofs), "+v"(kofs_n), "+v"(pofs));
+      asm volatile("" : "+v"(vofs), "+v"(kofs_n), "+v"(pofs), "+s"(rv), "+s"(rk_n));
       const Chunk x = buf[j % PF];
       issue(std::integral_constant<int, j>{});
       float pn[G];
       if constexpr (js + 1 < NC) {
+        const int pi = (js + 1 + rv) & (NC - 1);
 #pragma unroll
-        for (int h = 0; h < G; ++h) pn[h] = pl[pofs + (js + 1) * RPS * PST + h];
+        for (int h = 0; h < G; ++h) pn[h] = pl[pofs + pi * RPS * PST + h];
       }
       float vf[8];
       widen8<F>(x, vf);
@@ -562,6 +582,8 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
     }
     t = tn;
     kofs = kofs_n;
+    rk = rk_n;
+    rv = rot_v(tn);
   }
 
   // ---- wave partials: l over all lanes; acc over the lanes that share a

@@ -17,13 +17,8 @@ import pytest
 
 from paper_2609_02029_amd import build
 
-# kernels allowed a little scratch, with the reason
-SCRATCH_ALLOWED = {
-    # binary16 cache, head_dim 128, 8 q heads per kv head: two dwords stored
-    # and reloaded once per wave outside the key loop (the kernel has none),
-    # at the 128-register budget of four waves per SIMD
-    "decode_split<128, 8, 1>": 12,
-}
+# kernels allowed a little scratch (bytes), each with its reason
+SCRATCH_ALLOWED = {}
 
 
 def _demangle(name):
@@ -88,9 +83,12 @@ def test_no_scratch_spills(kernel_table):
 
 
 def test_register_budgets(kernel_table):
-    # decode splits: four waves per SIMD (128 registers each, with the
-    # accumulation registers the allocator may borrow beyond that); prefill
-    # attention: two waves of eight per SIMD, 256 registers
+    # decode splits: four waves per SIMD (128 registers), three (168) for 8 q
+    # heads per kv head at head_dim 256, whose 64 value accumulators per lane
+    # do not fit 128; prefill attention: two waves of eight per SIMD (256)
     for n, (vg, _) in kernel_table.items():
         if n.startswith("prefill_attn<"):
             assert vg <= 256, (n, vg)
+        if n.startswith("decode_split<"):
+            d, g, _f = (int(x) for x in n[n.index("<") + 1:-1].split(","))
+            assert vg <= (168 if (d, g) == (256, 8) else 128), (n, vg)
