@@ -341,9 +341,10 @@ int hwkv_append_decode_attn(hwkv_cache *cache, int32_t layer,
 /* ------------------------------------------------------------------------ */
 
 /* Device workspace bytes hwkv_calib_replay needs for n_rows sampled rows of
- * an n_hist-token trace: the row positions and the split-K partials of the
- * longest candidate (rows x n_q_heads x (head_dim + 4) fp32 per split of
- * 4,096 keys). */
+ * an n_hist-token trace: the row positions and ceil(n_hist / 4096) + 3 sets
+ * of n_rows x n_q_heads x (head_dim + 4) fp32 partials -- one per split of
+ * the keys (at most 4,096 keys each), one for the sinks, and two for the
+ * candidates' edge (m, l) pairs.  Independent of the number of windows. */
 int hwkv_calib_workspace_bytes(int32_t n_q_heads, int32_t head_dim,
                                int32_t n_sinks, int64_t n_hist, int64_t n_rows,
                                size_t *bytes);
@@ -372,9 +373,16 @@ int hwkv_calib_workspace_bytes(int32_t n_q_heads, int32_t head_dim,
  *             check; the paper's runs abort below 0.99)
  *   check     device fp32 [n_rows][n_q_heads], required iff ref_full
  *   ws        device workspace of ws_bytes >= hwkv_calib_workspace_bytes
- * Same arithmetic as hwkv_prefill_attn (bf16 MFMA, fp32 accumulation);
- * scores and means in fp32.  Waits for the stream once (the row positions
- * are uploaded from host memory).  EINVAL on bad shapes, rows or windows. */
+ * One pass over the trace serves every candidate: the windows are nested
+ * suffixes of each row's history (plus the common sinks), so each row's keys
+ * are visited once, from the row's position down, and each window's share
+ * is taken where the walk crosses the window's edge; a merge then assembles
+ * the candidates.  Same arithmetic as hwkv_prefill_attn (bf16 MFMA, fp32
+ * accumulation; the weights enter the value product rounded to bf16 under a
+ * shift shared by all candidates); scores and means in fp32.  outs is also
+ * used as scratch before the merge writes it.  Waits for the stream once
+ * (the row positions are uploaded from host memory).  EINVAL on bad shapes,
+ * rows or windows, or if (n_windows + 1) * n_rows * n_q_heads >= 2^31. */
 int hwkv_calib_replay(int32_t n_kv_heads, int32_t n_q_heads, int32_t head_dim,
                       int32_t n_sinks, int32_t n_windows,
                       const int64_t *windows, int64_t n_hist, const void *k,

@@ -8,7 +8,7 @@
 // head's G query heads (Eq. conditional-similarity).  fp32 throughout: one
 // wavefront per (row, q head) with lanes over channels and DPP/lane-read
 // reductions; one workgroup per (candidate, kv head) for the means.  The
-// replay's split-K partials are merged here too.
+// partials of the one-pass replay are merged into candidates here too.
 #include "hwkv_internal.h"
 
 namespace hwkv {
@@ -92,29 +92,71 @@ __global__ __launch_bounds__(256) void calib_means(const CalibArgs a) {
     a.means[(size_t)k * hkv + h] = ((part[0] + part[1]) + (part[2] + part[3])) / (float)n;
 }
 
-// Replay split-K merge: one wavefront per (row, q head) column, lanes over
-// channels: out = sum_j acc_j 2^((m_j - M) c) / sum_j l_j 2^((m_j - M) c),
-// M = max over splits with l_j > 0 (m in logit units, c = scale * log2 e).
+// Merge of the one-pass replay: one wavefront per (candidate k, column c),
+// lanes over channels.  Candidate k < K of column c (row position t) holds
+// the sinks and the keys s >= e = t + 1 - w_k; e <= S means every key, as the
+// full candidate (k = K) does.  Its parts: the sinks' partial; the partial of
+// split j (keys [j T, (j + 1) T), T = 32 tiles_per_split) when all of the
+// split's keys are >= e (e <= max(j T, S)); the window's edge partial when e
+// lies inside split j (max(j T, S) < e < (j + 1) T); nothing from splits at
+// or above e otherwise.  out = sum acc 2^((m - M) c) / sum l 2^((m - M) c),
+// M = max m over the parts with l > 0 (m in logit units, c = scale log2 e).
 template <int D>
 __global__ __launch_bounds__(256) void replay_merge(const ReplayMergeArgs a) {
   constexpr int PER = D / 64;
-  const int col = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int wid = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  if (col >= a.n_cols) return;                     // uniform per wave
-  const size_t stride = (size_t)a.n_cols * (D + 4);
-  const float *p = a.part + (size_t)col * (D + 4);
+  const int K = a.n_windows;
+  if (wid >= (K + 1) * a.n_cols) return;           // uniform per wave
+  const int k = wid / a.n_cols, col = wid - k * a.n_cols;
   const int h = (col % a.n_q_heads) / a.group;     // the column's kv head
+  const int t = a.rows[col / a.n_q_heads];
+  const int S = a.n_sinks;
+  const int T = 32 * a.tiles_per_split;
+  const int e = k < K ? t + 1 - a.windows[k] : INT_MIN;
+  const bool all = e <= S;
+  const int je = all ? -1 : e / T;                 // the split holding the edge
+  const bool edge_part = !all && e > je * T;       // else split je lies inside
   const float c2 = a.scale_log2 * a.k_scale[h];
+  const size_t stride = (size_t)a.n_cols * (D + 4);
+  const float *pc = a.part + (size_t)col * (D + 4);
+  float *orow = a.outs + ((size_t)k * a.n_cols + col) * D;
+  // the splits whose keys all lie in the candidate: every split for the full
+  // candidate, else those above the edge split (split je too when the edge
+  // is its first key)
+  const int j_begin = all ? 0 : (edge_part ? je + 1 : je);
+  float em = -1e30f, el = 0.0f;
+  if (edge_part) {
+    const float2 ml = *reinterpret_cast<const float2 *>(a.win_ml + ((size_t)k * a.n_cols + col) * 2);
+    em = ml.x;
+    el = ml.y;
+  }
+  const float *ps = pc + (size_t)a.n_splits * stride;   // the sinks' partial
+  const bool sinks = S > 0 && ps[1] > 0.0f;
   float M = -1e30f;
-  for (int j = 0; j < a.n_splits; ++j) {
-    const float *pj = p + (size_t)j * stride;
+  if (sinks) M = ps[0];
+  if (el > 0.0f) M = fmaxf(M, em);
+  for (int j = j_begin; j < a.n_splits; ++j) {
+    const float *pj = pc + (size_t)j * stride;
     if (pj[1] > 0.0f) M = fmaxf(M, pj[0]);
   }
   float L = 0.f, acc[PER];
 #pragma unroll
   for (int i = 0; i < PER; ++i) acc[i] = 0.f;
-  for (int j = 0; j < a.n_splits; ++j) {
-    const float *pj = p + (size_t)j * stride;
+  if (el > 0.0f) {
+    const float f = __builtin_amdgcn_exp2f((em - M) * c2);
+    L += el * f;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) acc[i] += orow[lane + 64 * i] * f;
+  }
+  if (sinks) {
+    const float f = __builtin_amdgcn_exp2f((ps[0] - M) * c2);
+    L += ps[1] * f;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) acc[i] += ps[4 + lane + 64 * i] * f;
+  }
+  for (int j = j_begin; j < a.n_splits; ++j) {
+    const float *pj = pc + (size_t)j * stride;
     const float lj = pj[1];
     if (!(lj > 0.0f)) continue;                    // uniform: empty split
     const float f = __builtin_amdgcn_exp2f((pj[0] - M) * c2);
@@ -124,13 +166,13 @@ __global__ __launch_bounds__(256) void replay_merge(const ReplayMergeArgs a) {
   }
   const float inv = a.v_scale[h] / L;
 #pragma unroll
-  for (int i = 0; i < PER; ++i) a.out[(size_t)col * D + lane + 64 * i] = acc[i] * inv;
+  for (int i = 0; i < PER; ++i) orow[lane + 64 * i] = acc[i] * inv;
 }
 
 }  // namespace
 
 hipError_t launch_replay_merge(int D, const ReplayMergeArgs &a, hipStream_t s) {
-  const dim3 grid((unsigned)((a.n_cols + 3) / 4)), block(256);
+  const dim3 grid((unsigned)(((size_t)(a.n_windows + 1) * a.n_cols + 3) / 4)), block(256);
   switch (D) {
     case 64: hipLaunchKernelGGL(replay_merge<64>, grid, block, 0, s, a); break;
     case 128: hipLaunchKernelGGL(replay_merge<128>, grid, block, 0, s, a); break;

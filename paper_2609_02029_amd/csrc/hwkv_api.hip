@@ -1016,22 +1016,19 @@ int hwkv_prefill_attn_ws(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0
 
 namespace {
 
-// Key tiles (32 keys) the replay kernel visits for the column block whose
-// first and last query positions are ta and tb, with window w (0 = full).
-int64_t replay_tiles(int64_t ta, int64_t tb, int64_t w, int64_t S) {
-  const int64_t lo = w == 0 ? 0 : std::max<int64_t>(0, ta + 1 - w);
-  if (lo <= S) return (tb + 1 + 31) / 32;
-  return (S + 31) / 32 + (tb + 1 - lo + 31) / 32;
-}
-
 size_t replay_rows_bytes(int64_t n_rows) { return (size_t)((n_rows * 4 + 255) / 256 * 256); }
 
-// Upper bound of the splits of any candidate: every column block visits at
-// most ceil(n_hist / 32) + ceil(S / 32) tiles.
-int64_t replay_max_splits(int64_t n_hist, int64_t S) {
-  const int64_t t = (n_hist + 31) / 32 + (S + 31) / 32;
+// Upper bound of the replay's splits: a column block visits at most
+// ceil(n_hist / 32) key tiles, at most kReplayTilesPerSplit per split.
+int64_t replay_max_splits(int64_t n_hist) {
+  const int64_t t = (n_hist + 31) / 32;
   return (t + hwkv::kReplayTilesPerSplit - 1) / hwkv::kReplayTilesPerSplit;
 }
+
+// Partial sets of the workspace ([n_cols][D + 4] fp32 each): one per split,
+// one for the sinks, and two holding the windows' edge (m, l) pairs (at most
+// 64 windows x 2 floats <= 2 (D + 4) per column).
+int64_t replay_partial_sets(int64_t n_hist) { return replay_max_splits(n_hist) + 3; }
 
 }  // namespace
 
@@ -1042,7 +1039,7 @@ int hwkv_calib_workspace_bytes(int32_t n_q_heads, int32_t head_dim, int32_t n_si
       n_hist > (int64_t)(1 << 24) || n_q_heads < 1 || n_q_heads > 64 * 8 ||
       (head_dim != 64 && head_dim != 128 && head_dim != 256) || n_sinks < 0)
     return fail(HWKV_EINVAL, "bad replay shape");
-  const uint64_t part = (uint64_t)replay_max_splits(n_hist, n_sinks) * (uint64_t)n_rows *
+  const uint64_t part = (uint64_t)replay_partial_sets(n_hist) * (uint64_t)n_rows *
                         (uint64_t)n_q_heads * (uint64_t)(head_dim + 4) * 4u;
   *bytes = replay_rows_bytes(n_rows) + (size_t)part;
   return ok();
@@ -1136,7 +1133,8 @@ int hwkv_calib_replay_format(int32_t n_kv_heads, int32_t n_q_heads, int32_t head
   const int32_t G = n_q_heads / n_kv_heads;
   const int64_t per = hwkv::prefill_attn_columns_per_block();
   const int64_t nb = (n_rows * G + per - 1) / per;
-  if (nb * n_kv_heads > (int64_t)INT32_MAX)
+  if (nb * n_kv_heads > (int64_t)INT32_MAX ||
+      (int64_t)(n_windows + 1) * n_rows * n_q_heads > (int64_t)INT32_MAX)
     return fail(HWKV_EINVAL, "n_rows too large for one launch");
   hipStream_t st = (hipStream_t)stream;
 
@@ -1184,72 +1182,70 @@ int hwkv_calib_replay_format(int32_t n_kv_heads, int32_t n_q_heads, int32_t head
     k_src = kst;
     v_src = vst;
   }
-  for (int32_t c = 0; c <= n_windows; ++c) {
-    hwkv::PrefillAttnArgs a;
-    std::memset(&a, 0, sizeof a);
-    // a window reaching back past the history is the full candidate
-    const int64_t w0 = c < n_windows ? windows[c] : 0;
-    const int64_t w = (w0 >= n_hist) ? 0 : w0;
-    // splits: the most tiles any column block of this candidate visits
-    int64_t max_tiles = 1;
-    for (int64_t b = 0; b < nb; ++b) {
-      const int64_t c0 = b * per, c1 = std::min(c0 + per, n_rows * G) - 1;
-      max_tiles = std::max(max_tiles, replay_tiles(rows[c0 / G], rows[c1 / G], w, n_sinks));
-    }
-    // splits: about one workgroup per CU (a workgroup holds a CU), never
-    // more than the workspace holds (the longest candidate's count at
-    // kReplayTilesPerSplit tiles each), each of at least the minimum size
-    const int64_t ws_splits = replay_max_splits(n_hist, n_sinks);
-    const int64_t want = std::min<int64_t>(
-        ws_splits, std::max<int64_t>(1, n_cus / (nb * n_kv_heads)));
-    const int64_t tps = std::max<int64_t>(
-        hwkv::kReplayMinTilesPerSplit,
-        std::max<int64_t>((max_tiles + want - 1) / want, (max_tiles + ws_splits - 1) / ws_splits));
-    const int64_t n_splits = (max_tiles + tps - 1) / tps;
-    for (int32_t h = 0; h < n_kv_heads; ++h) {
-      a.head[h].window = (int32_t)w;
-      a.head[h].pto = -1;          // no cache: every key comes from the trace
-      a.head[h].k_scale = ks[h];
-      a.head[h].v_scale = vs[h];
-      a.head_order[h] = h;
-    }
-    a.q = static_cast<const uint16_t *>(q);
-    a.k = static_cast<const uint16_t *>(k_src);
-    a.v = static_cast<const uint16_t *>(v_src);
-    a.out = static_cast<float *>(outs) + (size_t)c * vec;
-    a.rows = static_cast<const int32_t *>(ws);
-    a.p0 = 0;
-    a.n_tokens = (int32_t)n_rows;
-    a.n_kv_heads = n_kv_heads;
-    a.group = G;
-    a.n_sinks = n_sinks;
-    a.n_col_blocks = (int32_t)nb;
-    a.scale_log2 = scale * 1.4426950408889634f;
-    if (n_splits > 1) {
-      a.part = part;
-      a.tiles_per_split = (int32_t)tps;
-    }
-    rc = check_device(hwkv::launch_prefill_attn(head_dim, a, st, (int)n_splits),
-                      "calib replay launch");
-    if (rc != HWKV_OK) return rc;
-    if (n_splits > 1) {
-      hwkv::ReplayMergeArgs ma;
-      std::memset(&ma, 0, sizeof ma);
-      ma.part = part;
-      ma.out = a.out;
-      ma.n_splits = (int32_t)n_splits;
-      ma.n_cols = (int32_t)(n_rows * n_q_heads);
-      ma.n_q_heads = n_q_heads;
-      ma.group = G;
-      ma.scale_log2 = a.scale_log2;
-      for (int32_t h = 0; h < n_kv_heads; ++h) {
-        ma.k_scale[h] = ks[h];
-        ma.v_scale[h] = vs[h];
-      }
-      rc = check_device(hwkv::launch_replay_merge(head_dim, ma, st), "calib merge launch");
-      if (rc != HWKV_OK) return rc;
-    }
+  // One pass over the trace for every candidate.  Splits: the key tiles of
+  // the longest column block (its last row's position) in about one
+  // workgroup per CU, never more than the workspace holds, each of at least
+  // the minimum size.
+  int64_t max_tiles = 1;
+  for (int64_t b = 0; b < nb; ++b) {
+    const int64_t c1 = std::min((b + 1) * per, n_rows * G) - 1;
+    max_tiles = std::max<int64_t>(max_tiles, rows[c1 / G] / 32 + 1);
   }
+  const int64_t ws_splits = replay_max_splits(n_hist);
+  const int64_t want = std::min<int64_t>(
+      ws_splits, std::max<int64_t>(1, n_cus / (nb * n_kv_heads)));
+  const int64_t tps = std::max<int64_t>(
+      hwkv::kReplayMinTilesPerSplit,
+      std::max<int64_t>((max_tiles + want - 1) / want, (max_tiles + ws_splits - 1) / ws_splits));
+  const int64_t n_splits = (max_tiles + tps - 1) / tps;
+  const size_t n_cols = (size_t)n_rows * n_q_heads;
+  const size_t set = n_cols * (size_t)(head_dim + 4);
+  float *win_ml = part + (size_t)(ws_splits + 1) * set;
+  hwkv::ReplayAttnArgs ra;
+  std::memset(&ra, 0, sizeof ra);
+  ra.q = static_cast<const uint16_t *>(q);
+  ra.k = static_cast<const uint16_t *>(k_src);
+  ra.v = static_cast<const uint16_t *>(v_src);
+  ra.rows = static_cast<const int32_t *>(ws);
+  ra.part = part;
+  ra.win_acc = static_cast<float *>(outs);       // candidate k's rows hold its edge acc
+  ra.win_ml = win_ml;
+  // a window reaching back past the history holds every key
+  for (int32_t c = 0; c < n_windows; ++c)
+    ra.windows[c] = (int32_t)std::min<int64_t>(windows[c], n_hist);
+  for (int32_t h = 0; h < n_kv_heads; ++h) ra.k_scale[h] = ks[h];
+  ra.n_windows = n_windows;
+  ra.n_splits = (int32_t)n_splits;
+  ra.tiles_per_split = (int32_t)tps;
+  ra.n_rows = (int32_t)n_rows;
+  ra.n_kv_heads = n_kv_heads;
+  ra.group = G;
+  ra.n_sinks = n_sinks;
+  ra.n_col_blocks = (int32_t)nb;
+  ra.scale_log2 = scale * 1.4426950408889634f;
+  rc = check_device(hwkv::launch_replay_attn(head_dim, ra, st), "calib replay launch");
+  if (rc != HWKV_OK) return rc;
+  hwkv::ReplayMergeArgs ma;
+  std::memset(&ma, 0, sizeof ma);
+  ma.part = part;
+  ma.win_ml = win_ml;
+  ma.outs = static_cast<float *>(outs);
+  ma.rows = ra.rows;
+  std::memcpy(ma.windows, ra.windows, sizeof ma.windows);
+  for (int32_t h = 0; h < n_kv_heads; ++h) {
+    ma.k_scale[h] = ks[h];
+    ma.v_scale[h] = vs[h];
+  }
+  ma.n_windows = n_windows;
+  ma.n_splits = (int32_t)n_splits;
+  ma.tiles_per_split = (int32_t)tps;
+  ma.n_cols = (int32_t)n_cols;
+  ma.n_q_heads = n_q_heads;
+  ma.group = G;
+  ma.n_sinks = n_sinks;
+  ma.scale_log2 = ra.scale_log2;
+  rc = check_device(hwkv::launch_replay_merge(head_dim, ma, st), "calib merge launch");
+  if (rc != HWKV_OK) return rc;
   hwkv::CalibArgs ca;
   ca.outs = static_cast<const float *>(outs);
   ca.ref = static_cast<const float *>(ref_full);

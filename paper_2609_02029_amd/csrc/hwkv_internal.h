@@ -137,11 +137,6 @@ struct PrefillAttnArgs {
   const uint16_t *k;             // [n_tokens][Hkv][D]
   const uint16_t *v;
   float *out;                    // [n_tokens][Hq][D]
-  const int32_t *rows;           // calibration replay: position of each query
-                                 // row (ascending); null for prefill (p0 + row)
-  float *part;                   // split-K partials (replay) or null: per split
-                                 // and column [m, l, -, -, acc[D]]
-  int32_t tiles_per_split;       // key tiles per split when part is set
   int32_t p0;
   int32_t n_tokens;
   int32_t n_kv_heads;
@@ -206,8 +201,7 @@ struct StageChunkArgs {
 };
 hipError_t launch_stage_chunk(int D, const StageChunkArgs &a, hipStream_t s);
 int prefill_attn_columns_per_block();   // (token, q head) columns
-hipError_t launch_prefill_attn(int D, const PrefillAttnArgs &a, hipStream_t s,
-                              int n_splits = 1);
+hipError_t launch_prefill_attn(int D, const PrefillAttnArgs &a, hipStream_t s);
 
 // Calibration scores: for every (row, q head), the stabilised cosine of each
 // candidate output against the full one (and of the full one against a
@@ -222,24 +216,51 @@ struct CalibArgs {
 };
 hipError_t launch_calib_scores(int D, const CalibArgs &a, hipStream_t s);
 
-// Merge of the replay's split-K partials into normalised outputs.
+// Calibration replay in one pass: for every sampled row, the keys of the
+// traced history are visited once, from the row's position down, and every
+// candidate window's partial is taken at the window's edge (the windows are
+// nested suffixes of the history, plus the common sink prefix).
+constexpr int kMaxWindows = 64;
+struct ReplayAttnArgs {
+  const uint16_t *q;             // [n_rows][Hq][D] queries of the sampled rows
+  const uint16_t *k, *v;         // [n_hist][Hkv][D] traced keys and values
+  const int32_t *rows;           // [n_rows] positions, strictly increasing
+  float *part;                   // [n_splits + 1][n_cols][D + 4]: the splits'
+                                 // partials [m, l, -, -, acc], then the sinks'
+  float *win_acc;                // [n_windows][n_cols][D]: a window's acc at its edge
+  float *win_ml;                 // [n_windows][n_cols][2]: its (m, l)
+  int32_t windows[kMaxWindows];  // finite candidate windows, strictly increasing
+  float k_scale[kMaxItems];      // per kv head: the keys' logit scale (fp8; else 1)
+  int32_t n_windows, n_splits, tiles_per_split;
+  int32_t n_rows, n_kv_heads, group, n_sinks, n_col_blocks;
+  float scale_log2;              // scale * log2(e)
+};
+hipError_t launch_replay_attn(int D, const ReplayAttnArgs &a, hipStream_t s);
+
+// Merge of the one-pass replay: candidate k of column c from the sinks'
+// partial, the partials of the splits that lie inside the window and the
+// edge partial of the split that holds the window's edge.
 struct ReplayMergeArgs {
-  const float *part;             // [n_splits][n_cols][D + 4]
-  float *out;                    // [n_cols][D]
-  int32_t n_splits, n_cols;
-  int32_t n_q_heads, group;      // column c is q head c % n_q_heads
+  const float *part;             // as in ReplayAttnArgs
+  const float *win_ml;
+  float *outs;                   // [n_windows + 1][n_cols][D], full last; on entry
+                                 // a window's rows hold its edge partial's acc
+  const int32_t *rows;
+  int32_t windows[kMaxWindows];
+  float k_scale[kMaxItems];      // per kv head: the keys' logit scale
+  float v_scale[kMaxItems];      //   and the values' scale (fp8; else 1)
+  int32_t n_windows, n_splits, tiles_per_split;
+  int32_t n_cols, n_q_heads, group, n_sinks;
   float scale_log2;
-  float k_scale[kMaxItems];      // per kv head: the stored keys' logit scale
-  float v_scale[kMaxItems];      //   and the stored values' scale (fp8)
 };
 hipError_t launch_replay_merge(int D, const ReplayMergeArgs &a, hipStream_t s);
 constexpr int kReplayTilesPerSplit = 128;   // 32-key tiles per split, at most
 #ifndef HWKV_REPLAY_MIN_TILES
 #define HWKV_REPLAY_MIN_TILES 8
 #endif
-// A candidate with fewer tiles takes smaller splits (as many as the
-// workspace holds, of at least this many tiles), so that its launch still
-// has workgroups for every CU.
+// A short trace takes smaller splits (as many as the workspace holds, of at
+// least this many tiles), so that the launch still has workgroups for every
+// CU.
 constexpr int kReplayMinTilesPerSplit = HWKV_REPLAY_MIN_TILES;
 hipError_t launch_calib_means(const CalibArgs &a, hipStream_t s);
 
@@ -253,3 +274,5 @@ static_assert(sizeof(hwkv::PageUpdateArgs) <= 4096, "page update kernarg too lar
 static_assert(sizeof(hwkv::StageArgs) <= 4096, "stage kernarg too large");
 static_assert(sizeof(hwkv::StageChunkArgs) <= 4096, "stage chunk kernarg too large");
 static_assert(sizeof(hwkv::PrefillAttnArgs) <= 4096, "prefill kernarg too large");
+static_assert(sizeof(hwkv::ReplayAttnArgs) <= 4096, "replay kernarg too large");
+static_assert(sizeof(hwkv::ReplayMergeArgs) <= 4096, "replay merge kernarg too large");

@@ -10,9 +10,8 @@
 // whose residency at length p0 covers every s >= p0 + 1 - w); keys in
 // [p0, t] come from the chunk's own K/V.
 //
-// Calibration replay runs the same kernel with a list of query positions
-// (ascending, one per query row), p0 = 0 and the layer's whole traced K/V as
-// the "chunk", once per candidate window.
+// The calibration replay (replay_attn, below) uses the same tiles, operand
+// layouts and softmax on a traced history, for every candidate in one pass.
 //
 // Formulation.  A workgroup owns one KV head and 32 * NW consecutive
 // (token, q-head) columns of that head (column c = token * G + g), one
@@ -131,10 +130,9 @@ void prefill_attn(const PrefillAttnArgs a) {
   const int c_first = cb * 32 * NW;
   const int c_last = min(c_first + 32 * NW, ncols) - 1;
   // positions and slots fit in 32 bits (max_ctx < 2^24).  Query row r sits
-  // at position p0 + r, or rows[r] in calibration replay (ascending).
+  // at position p0 + r.
   const int p0 = a.p0;
-  const int32_t *rows = a.rows;
-  auto pos = [&](int r) -> int { return rows ? rows[r] : p0 + r; };
+  auto pos = [&](int r) -> int { return p0 + r; };
   const int S = a.n_sinks;
   const int W = hd.window;                          // 0 = full
   const int ta = pos(c_first / G), tb = pos(c_last / G);
@@ -175,22 +173,6 @@ void prefill_attn(const PrefillAttnArgs a) {
   }
   const int na = (ra1 + kKeys - 1) / kKeys;
   const int ntiles = na + (rb1 - rb0 + kKeys - 1) / kKeys;
-  // split-K (calibration replay): this workgroup's share of the tiles
-  int i_begin = 0, i_end = ntiles;
-  if (a.part) {
-    i_begin = blockIdx.y * a.tiles_per_split;
-    i_end = min(ntiles, i_begin + a.tiles_per_split);
-  }
-  const size_t col_id = q_row / D;                  // row * Hq + h * G + g
-  float *pp = a.part ? a.part + ((size_t)blockIdx.y * (a.n_tokens * Hq) + col_id) * (D + 4)
-                     : nullptr;
-  if (i_begin >= i_end) {                           // uniform: an empty split
-    if (pp && col_ok && half == 0) {
-      pp[0] = -1e30f;
-      pp[1] = 0.0f;
-    }
-    return;
-  }
 
   const uint16_t *kc = a.cache + hd.k_off;
   const uint16_t *vc = a.cache + hd.v_off;
@@ -301,12 +283,12 @@ void prefill_attn(const PrefillAttnArgs a) {
   const int vkey0 = 4 * (gq >> 1) + (mq >> 2);
   const int vlane = (gq & 1) * P::VPAIR + vpar * 512 + (vkey0 ^ (4 * vpar)) * 16 + (mq & 1) * 8;
 
-  issue_loads(i_begin, i_begin & 1);
+  issue_loads(0, 0);
 
-  for (int i = i_begin; i < i_end; ++i) {
+  for (int i = 0; i < ntiles; ++i) {
     wait_loads();
     __syncthreads();
-    if (i + 1 < i_end) issue_loads(i + 1, (i + 1) & 1);
+    if (i + 1 < ntiles) issue_loads(i + 1, (i + 1) & 1);
     int s0, se;
     tile_range(i, &s0, &se);
     const int slast = min(s0 + kKeys, se) - 1;
@@ -391,20 +373,6 @@ void prefill_attn(const PrefillAttnArgs a) {
   halves(l, &l_lo, &l_hi);
   if (!col_ok) return;
   const float lt = l_lo + l_hi;
-  if (pp) {                                         // split-K partial, unnormalised
-    if (half == 0) {
-      pp[0] = m;
-      pp[1] = lt;
-    }
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-      for (int rq = 0; rq < 4; ++rq)
-        *reinterpret_cast<float4 *>(pp + 4 + 32 * db + 8 * rq + 4 * half) =
-            make_float4(o[db][4 * rq + 0], o[db][4 * rq + 1], o[db][4 * rq + 2],
-                        o[db][4 * rq + 3]);
-    return;
-  }
   const float inv = hd.v_scale / lt;     // the stored values' scale (fp8)
   // the output row, recomputed here rather than kept live through the loop
   int c_out = c;
@@ -424,18 +392,331 @@ void prefill_attn(const PrefillAttnArgs a) {
     }
 }
 
+
+// Calibration replay in one pass.  Workgroups and columns as in prefill_attn
+// (column c = row * G + g of one KV head, row r at position rows[r]); the
+// keys are the traced history, each candidate window w holds the sinks
+// [0, S) and the suffix [max(S, t + 1 - w), t] of row position t, and the
+// full candidate holds every s <= t.  The suffixes are nested, so a column
+// walks its keys once, from the top tile down: when the walk has added every
+// key at or above a window's edge t + 1 - w, the running (m, l, acc) is that
+// window's share of the split, written out there.  A tile holding an edge is
+// added in up to two passes of the V^T P^T product per edge: the keys at or
+// above the edge, then the rest.  Split y < n_splits covers key tiles
+// [y tps, (y + 1) tps) of [0, t_last] without the sinks; split n_splits adds
+// the sinks alone.  replay_merge assembles each candidate.
+template <int D, int NW>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
+void replay_attn(const ReplayAttnArgs a) {
+  using P = Prefill<D, NW>;
+  constexpr int KS = P::KS, DB = P::DB;
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * P::STAGE];
+  __shared__ int swin[kMaxWindows];
+
+  const int nb = a.n_col_blocks;
+  const int h = blockIdx.x / nb;
+  const int cb = nb - 1 - (int)(blockIdx.x % nb);   // later rows first
+  const int G = a.group;
+  const int Hq = a.n_kv_heads * G;
+  const int ncols = a.n_rows * G;
+  const int c_first = cb * 32 * NW;
+  const int c_last = min(c_first + 32 * NW, ncols) - 1;
+  const int32_t *rows = a.rows;
+  const int S = a.n_sinks;
+  const int K = a.n_windows;
+  const int tb = rows[c_last / G];                  // the block's last position
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int half = lane >> 5, cl = lane & 31;
+  const int wc0 = c_first + 32 * wave;
+  const bool wave_live = wc0 <= c_last;
+  const int wc_last = min(wc0 + 31, c_last);
+  const int t_lo = rows[min(wc0, c_last) / G], t_hi = rows[wc_last / G];
+  const int c = wc0 + cl;
+  const bool col_ok = c <= c_last;
+  const int cc = min(c, c_last);
+  const int tl = cc / G, g = cc - tl * G;
+  const int t = rows[tl];
+  const size_t q_row = ((size_t)tl * Hq + (size_t)h * G + g) * D;
+  const size_t n_cols = (size_t)a.n_rows * Hq;
+  // the lane's column id (row * Hq + h * G + g), recomputed where it is
+  // needed rather than kept live through the tile loop
+  auto column_id = [&]() -> size_t {
+    int cx = wc0 + (int)(threadIdx.x & 31);
+    asm volatile("" : "+v"(cx));
+    const int ccx = min(cx, c_last), tx = ccx / G;
+    return (size_t)tx * Hq + (size_t)h * G + (size_t)(ccx - tx * G);
+  };
+
+  // this workgroup's key tiles
+  const int ntiles = tb / kKeys + 1;
+  const bool sink_pass = (int)blockIdx.y == a.n_splits;
+  int i_lo, i_hi;
+  if (sink_pass) {
+    i_lo = 0;
+    i_hi = min(ntiles, (S + kKeys - 1) / kKeys);
+  } else {
+    i_lo = blockIdx.y * a.tiles_per_split;
+    i_hi = min(ntiles, i_lo + a.tiles_per_split);
+  }
+  if (i_lo >= i_hi) {                               // uniform: an empty split
+    if (col_ok && half == 0) {
+      float *pp = a.part + ((size_t)blockIdx.y * n_cols + q_row / D) * (D + 4);
+      pp[0] = -1e30f;
+      pp[1] = 0.0f;
+    }
+    return;
+  }
+  for (int i = tid; i < K; i += NW * 64) swin[i] = a.windows[i];
+
+  u32x4_t qv[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks)
+    qv[ks] = col_ok ? ld16(a.q + q_row + 16 * ks + 8 * half) : u32x4_t{0, 0, 0, 0};
+
+  const size_t in_stride = (size_t)a.n_kv_heads * D;
+  const uint16_t *kin = a.k + (size_t)h * D;
+  const uint16_t *vin = a.v + (size_t)h * D;
+  const uint16_t *zero = reinterpret_cast<const uint16_t *>(g_zero_row);
+  // the key this lane loads in every tile (see prefill_attn)
+  const int lkey = cl ^ (4 * half);
+  auto issue_loads = [&](int i, int buf) {
+    const int s = i * kKeys + lkey;
+    const uint16_t *kp = s <= tb ? kin + (size_t)s * in_stride : zero;
+    const uint16_t *vp = s <= tb ? vin + (size_t)s * in_stride : zero;
+    uint8_t *kl = smem + buf * P::STAGE;
+    uint8_t *vl = kl + P::KBYTES;
+#pragma unroll
+    for (int j = 0; j < P::IPW; ++j) {
+      const int n = wave + j * NW;
+      if (P::NINST % NW != 0 && n >= P::NINST) break;   // uniform per wave
+      const int ch = 2 * n + half;
+      g2lds(kp + ch * 8, kl + n * 1024);
+      g2lds(vp + ch * 8, vl + n * P::VPAIR);
+    }
+  };
+
+  // logit scale, base 2, with the keys' scale; uniform (scalar register)
+  const float c2 = __builtin_bit_cast(
+      float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, a.scale_log2 * a.k_scale[h])));
+  float m = -1e30f;                              // running shift (raw units)
+  float l = 0.0f;                                // this lane's partial sum
+  f32x16_t o[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[db][r] = 0.0f;
+
+  const int klane = half * 512 + lkey * 16;
+  const int gq = lane >> 4, mq = lane & 15;
+  const int vpar = (mq >> 1) & 1;
+  const int vkey0 = 4 * (gq >> 1) + (mq >> 2);
+  const int vlane = (gq & 1) * P::VPAIR + vpar * 512 + (vkey0 ^ (4 * vpar)) * 16 + (mq & 1) * 8;
+
+  issue_loads(i_hi - 1, 0);
+  __syncthreads();                               // swin
+  // The lane's next window: the first whose edge lies below this split's top
+  // (windows with an edge at or above it have no key here).  An edge at or
+  // below S means the window holds every key: it is the full candidate.
+  const int top = i_hi * kKeys;
+  int kn = 0;
+  int edge = INT_MIN;
+  if (!sink_pass) {
+    while (kn < K && t + 1 - swin[kn] >= top) ++kn;
+    edge = (kn < K && t + 1 - swin[kn] > S) ? t + 1 - swin[kn] : INT_MIN;
+  }
+
+  // V^T P^T over the keys of rows [lo, hi) of this lane's tile rows (key of
+  // row r: s0 + 4 half + 8 (r / 4) + r % 4), adding their weights to l
+  auto add_keys = [&](const float (&pr)[16], int s0, int lo, int hi, const uint8_t *vl) {
+    u32x4_t pb[2];
+    const int e = s0 + 4 * half;
+    float ls = 0.0f;
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r0 = 8 * s + 2 * j, r1 = r0 + 1;
+        const int k0 = e + (r0 >> 2) * 8 + (r0 & 3), k1 = e + (r1 >> 2) * 8 + (r1 & 3);
+        const float p0 = (k0 >= lo && k0 < hi) ? pr[r0] : 0.0f;
+        const float p1 = (k1 >= lo && k1 < hi) ? pr[r1] : 0.0f;
+        ls += p0 + p1;
+        pb[s][j] = pack_bf16(p0, p1);
+      }
+    l += ls;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        i16x4_t v2[2];
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh)
+          v2[hh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (lds_i16x4_t *)(vl + 2 * db * P::VPAIR + (16 * s + 8 * hh) * 16));
+        const bf16x8_t va = __builtin_bit_cast(
+            bf16x8_t, __builtin_shufflevector(v2[0], v2[1], 0, 1, 2, 3, 4, 5, 6, 7));
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            va, __builtin_bit_cast(bf16x8_t, pb[s]), o[db], 0, 0, 0);
+      }
+    }
+  };
+
+  const int n_it = i_hi - i_lo;
+  for (int it = 0; it < n_it; ++it) {
+    const int i = i_hi - 1 - it;                 // tiles from the top down
+    wait_loads();
+    __syncthreads();
+    if (it + 1 < n_it) issue_loads(i - 1, (it + 1) & 1);
+    const int s0 = i * kKeys;
+    const bool skip = !wave_live || s0 > t_hi ||
+                      (sink_pass ? s0 >= S : s0 + kKeys <= S);
+    if (skip) continue;
+    const uint8_t *kl = smem + (it & 1) * P::STAGE + klane;
+    const uint8_t *vl = smem + (it & 1) * P::STAGE + P::KBYTES + vlane;
+    // S^T of the tile, masked: visible keys are s <= t, and s < S in the
+    // sink pass, s >= S otherwise
+    const bool full_vis = s0 + kKeys - 1 <= t_lo && (sink_pass ? s0 + kKeys <= S : s0 >= S);
+    auto logits = [&]() -> f32x16_t {
+      f32x16_t st;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) st[r] = 0.0f;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const u32x4_t kx = *reinterpret_cast<const u32x4_t *>(kl + ks * 1024);
+        st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            __builtin_bit_cast(bf16x8_t, kx), __builtin_bit_cast(bf16x8_t, qv[ks]), st, 0, 0, 0);
+      }
+      if (!full_vis) {
+        int e = s0 + 4 * half, d = e - t;
+        asm volatile("" : "+v"(e), "+v"(d));
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int cr = (r >> 2) * 8 + (r & 3);
+          const bool vis = (d <= -cr) & (sink_pass ? (e < S - cr) : (e >= S - cr));
+          if (!vis) st[r] = -__builtin_inff();
+        }
+      }
+      return st;
+    };
+    // a window's partial at its edge, for the lanes whose edge lies in this
+    // tile; those lanes move to their next window
+    auto edge_partials = [&](bool act) {
+      float l_lo, l_hi;
+      halves(l, &l_lo, &l_hi);
+      if (act && wc0 + cl <= c_last) {
+        const size_t col_id = column_id();
+        float *wa = a.win_acc + ((size_t)kn * n_cols + col_id) * D;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int rq = 0; rq < 4; ++rq)
+            *reinterpret_cast<float4 *>(wa + 32 * db + 8 * rq + 4 * half) =
+                make_float4(o[db][4 * rq + 0], o[db][4 * rq + 1], o[db][4 * rq + 2],
+                            o[db][4 * rq + 3]);
+        if (half == 0)
+          *reinterpret_cast<float2 *>(a.win_ml + ((size_t)kn * n_cols + col_id) * 2) =
+              make_float2(m, l_lo + l_hi);
+      }
+      if (act) {
+        ++kn;
+        edge = (kn < K && t + 1 - swin[kn] > S) ? t + 1 - swin[kn] : INT_MIN;
+      }
+    };
+
+    float mc;
+    {
+      const f32x16_t st = logits();
+      float mx = st[0];
+#pragma unroll
+      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, st[r]);
+      {
+        float lo_half, hi_half;
+        halves(mx, &lo_half, &hi_half);
+        mx = fmaxf(lo_half, hi_half);
+      }
+      if (__any((mx - m) * c2 > 8.0f)) {        // lazy rescale: shift moves by > 8
+        const float mn = fmaxf(m, mx);
+        const float alpha = __builtin_amdgcn_exp2f((m - mn) * c2);
+        m = mn;
+        l *= alpha;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+      }
+      mc = m * c2;
+      float pr[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) pr[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(st[r], c2, -mc));
+      // First pass: a lane whose next window edge lies in this tile adds the
+      // keys at or above the edge; every other lane adds the whole tile.
+      const bool act = edge >= s0;
+      add_keys(pr, s0, act ? edge : s0, s0 + kKeys, vl);
+    }
+    if (__any(edge >= s0)) {                     // uniform; rare
+      // Further passes, each over the keys below the last edge taken: the
+      // logits and weights are recomputed from the tile (same shift, same
+      // values) rather than kept live through the passes.
+      bool act = edge >= s0;                     // the lanes of the first pass
+      int cut = act ? edge : s0;                 // keys [s0, cut) not added yet
+      while (true) {
+        edge_partials(act);
+        if (!__any(cut > s0)) break;
+        act = edge >= s0;                        // the lane's next edge, below cut
+        const int lo = act ? edge : s0;
+        const f32x16_t st = logits();
+        float pr[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) pr[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(st[r], c2, -mc));
+        add_keys(pr, s0, lo, cut, vl);
+        cut = lo;
+      }
+    }
+  }
+
+  float l_lo, l_hi;
+  halves(l, &l_lo, &l_hi);
+  if (wc0 + cl > c_last) return;
+  float *pp = a.part + ((size_t)blockIdx.y * n_cols + column_id()) * (D + 4);
+  if (half == 0) {
+    pp[0] = m;
+    pp[1] = l_lo + l_hi;
+  }
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int rq = 0; rq < 4; ++rq)
+      *reinterpret_cast<float4 *>(pp + 4 + 32 * db + 8 * rq + 4 * half) =
+          make_float4(o[db][4 * rq + 0], o[db][4 * rq + 1], o[db][4 * rq + 2],
+                      o[db][4 * rq + 3]);
+}
+
 }  // namespace
 
 int prefill_attn_columns_per_block() { return 32 * kPrefillWaves; }
 
-hipError_t launch_prefill_attn(int D, const PrefillAttnArgs &a, hipStream_t s,
-                              int n_splits) {
-  const dim3 grid((unsigned)(a.n_col_blocks * a.n_kv_heads), (unsigned)n_splits);
+hipError_t launch_prefill_attn(int D, const PrefillAttnArgs &a, hipStream_t s) {
+  const dim3 grid((unsigned)(a.n_col_blocks * a.n_kv_heads));
   const dim3 block(kPrefillWaves * 64);
   switch (D) {
     case 64: hipLaunchKernelGGL((prefill_attn<64, kPrefillWaves>), grid, block, 0, s, a); break;
     case 128: hipLaunchKernelGGL((prefill_attn<128, kPrefillWaves>), grid, block, 0, s, a); break;
     case 256: hipLaunchKernelGGL((prefill_attn<256, kPrefillWaves>), grid, block, 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_replay_attn(int D, const ReplayAttnArgs &a, hipStream_t s) {
+  const dim3 grid((unsigned)(a.n_col_blocks * a.n_kv_heads),
+                  (unsigned)(a.n_splits + (a.n_sinks > 0 ? 1 : 0)));
+  const dim3 block(kPrefillWaves * 64);
+  switch (D) {
+    case 64: hipLaunchKernelGGL((replay_attn<64, kPrefillWaves>), grid, block, 0, s, a); break;
+    case 128: hipLaunchKernelGGL((replay_attn<128, kPrefillWaves>), grid, block, 0, s, a); break;
+    case 256: hipLaunchKernelGGL((replay_attn<256, kPrefillWaves>), grid, block, 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -140,8 +140,8 @@ def test_replay_small(D, G):
 
 @pytest.mark.parametrize("D,G", [(128, 4), (256, 6)])
 def test_replay_split_keys(D, G):
-    """Histories long enough that the full and the 5000 candidates are split
-    over several workgroups (4,096 keys each) and merged."""
+    """A history long enough that its keys are split over several workgroups
+    and the candidates merged from the splits' and the edges' partials."""
     S, windows = 4, [100, 5000]
     kh, vh, qh, rows = small_case(34, 9000, 2, G, D, windows, S, extra_rows=24)
     scale = 1.0 / math.sqrt(D)
@@ -171,6 +171,70 @@ def test_replay_edges_and_full_check():
         for k, w in enumerate(windows):
             covered = [i for i, t in enumerate(rows) if S + w >= t + 1]
             assert np.array_equal(res["outs"][k, covered], res["outs"][-1, covered])
+
+
+def _split_keys(N, R, G, Hkv):
+    """Keys per split of the one-pass replay for this shape, by the library's
+    rule: about one workgroup per CU over the column blocks, at most the
+    workspace's split count (128 tiles each), at least 8 tiles per split."""
+    n_cus = torch.cuda.get_device_properties(0).multi_processor_count
+    nb = -(-R * G // 256)
+    tiles = -(-N // 32)
+    ws_splits = -(-tiles // 128)
+    want = min(ws_splits, max(1, n_cus // (nb * Hkv)))
+    max_tiles = (N - 1) // 32 + 1
+    tps = max(8, -(-max_tiles // want), -(-max_tiles // ws_splits))
+    return 32 * tps, -(-max_tiles // tps)
+
+
+def test_replay_one_pass_boundaries():
+    """The one-pass replay's edges: window edges exactly on, just below and
+    just above split boundaries and tile boundaries, several edges in one
+    tile, 40 sinks over two tiles, windows at and past the history."""
+    N, Hkv, G, D, S = 20000, 1, 4, 64, 40
+    windows = [1, 2, 31, 32, 33, 100, 4095, 19999, 25000]
+    R = 192
+    T, n_splits = _split_keys(N, R, G, Hkv)
+    assert n_splits >= 3, (T, n_splits)
+    want = {0, 1, S - 1, S, S + 1, 63, 64, N - 1}
+    for w in (1, 33, 100, 4095):
+        for j in range(1, n_splits):
+            for d in (-33, -1, 0, 1, 31, 32):
+                want.add(j * T + d + w - 1)          # edge t + 1 - w = j T + d
+        want |= {S + w - 2, S + w - 1, S + w}      # edges around the sinks
+    want = sorted(x for x in want if 0 <= x < N)
+    r = np.random.default_rng(41)
+    rest = np.setdiff1d(np.arange(N), want)
+    assert len(want) <= R
+    rows = sorted(set(want) | {int(x) for x in r.choice(rest, size=R - len(want), replace=False)})
+    kh = W.normal_bf16((N, Hkv, D), 41, 0, W.K, 0)
+    vh = W.normal_bf16((N, Hkv, D), 41, 0, W.V, 0)
+    qh = W.normal_bf16((R, Hkv * G, D), 41, 0, W.Q_PROMPT, 7)
+    scale = 1.0 / math.sqrt(D)
+    res = replay(up(kh, "cuda:0"), up(vh, "cuda:0"), up(qh, "cuda:0"), rows, windows, S, scale)
+    ref = oracle.replay_outputs(qh, kh, vh, rows, S, list(windows) + [0], scale, n_threads=16)
+    ratio, serr = check_all(res, ref, kh, vh, rows, windows, S, G, "one-pass boundaries")
+    # windows reaching back past the history equal the full candidate
+    for k, w in enumerate(windows):
+        covered = [i for i, t in enumerate(rows) if S + w >= t + 1]
+        assert np.array_equal(res["outs"][k, covered], res["outs"][-1, covered])
+    log(f"one-pass boundaries: {n_splits} splits of {T} keys, {R} rows, outputs "
+        f"{ratio:.3f} of the bound, score error {serr:.2e}")
+
+
+def test_replay_64_windows():
+    """The most candidate windows the replay takes (64), at head_dim 64,
+    without sinks, over a split history."""
+    N, Hkv, G, D, S = 9000, 2, 2, 64, 0
+    windows = list(range(1, 33)) + [40 + 37 * i for i in range(24)] + [5000, 8998, 8999, 9000,
+                                                                       9001, 12000, 20000, 40000]
+    assert len(windows) == 64 and all(b > a for a, b in zip(windows, windows[1:]))
+    kh, vh, qh, rows = small_case(43, N, Hkv, G, D, [1, 32, 100, 5000], S, extra_rows=24)
+    scale = 1.0 / math.sqrt(D)
+    res = replay(up(kh, "cuda:0"), up(vh, "cuda:0"), up(qh, "cuda:0"), rows, windows, S, scale)
+    ref = oracle.replay_outputs(qh, kh, vh, rows, S, list(windows) + [0], scale, n_threads=16)
+    ratio, serr = check_all(res, ref, kh, vh, rows, windows, S, G, "64 windows")
+    log(f"64 windows: {len(rows)} rows, outputs {ratio:.3f} of the bound, score error {serr:.2e}")
 
 
 def test_replay_zero_values_score_one():

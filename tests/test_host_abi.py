@@ -280,6 +280,18 @@ def test_calib_selection_matches_golden_and_oracle(hw, golden):
         assert hw.budget_select(rates, floors, 0.5) == oracle.budget_select(rates, floors, 0.5)
 
 
+def test_calib_workspace_formula(hw):
+    """The replay workspace: the row positions (256-byte aligned) and
+    ceil(n_hist / 4096) + 3 partial sets of rows x q heads x (d + 4) fp32,
+    whatever the number of windows."""
+    for hq, d, S, n_hist, nr in [(8, 64, 4, 50, 3), (24, 256, 4, 131072, 256),
+                                 (8, 128, 0, 4096, 7), (8, 128, 40, 4097, 7)]:
+        rows_b = -(-nr * 4 // 256) * 256
+        sets = -(-(-(-n_hist // 32)) // 128) + 3
+        assert hw.calib_workspace_bytes(hq, d, S, n_hist, nr) == \
+            rows_b + sets * nr * hq * (d + 4) * 4, (hq, d, S, n_hist, nr)
+
+
 def test_calib_host_errors(hw):
     L = hw._lib
     sc = ctypes.c_float(0.125)

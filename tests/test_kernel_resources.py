@@ -18,7 +18,10 @@ import pytest
 from paper_2609_02029_amd import build
 
 # kernels allowed a little scratch (bytes), each with its reason
-SCRATCH_ALLOWED = {}
+SCRATCH_ALLOWED = {
+    # one lane offset stored before the tile loop and read back after it
+    "replay_attn<256, 8>": 12,
+}
 
 
 def _demangle(name):
@@ -72,7 +75,8 @@ def kernel_table(tmp_path_factory):
 def test_every_hot_kernel_is_present(kernel_table):
     for name in ["decode_split<256, 6, 0>", "decode_split<256, 6, 2>", "decode_split<256, 6, 1>",
                  "prefill_attn<256, 8>", "prefill_attn<128, 8>", "prefill_attn<64, 8>",
-                 "replay_merge<256>", "prefill_write<256, 0>", "append_token<256, 2>"]:
+                 "replay_attn<256, 8>", "replay_merge<256>", "prefill_write<256, 0>",
+                 "append_token<256, 2>"]:
         assert name in kernel_table, sorted(kernel_table)
 
 
