@@ -57,6 +57,10 @@ def parse():
     ap.add_argument("--paged", action="store_true",
                     help="page the full units (pages of 256 rows from a pool sized to the "
                          "workload's final lengths) instead of reserving max_ctx rows")
+    ap.add_argument("--replicas", type=int, default=1,
+                    help="decode workloads: R independent caches of the workload (own seeded "
+                         "data), steps cycling through them, so that a cache smaller than the "
+                         "256 MB Infinity Cache is read cold from HBM (ctx32k: 16 replicas)")
     ap.add_argument("--unfused", action="store_true",
                     help="time hwkv_append + hwkv_decode_attn instead of the fused call")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -104,13 +108,16 @@ def main():
     Hq, Hkv, D, S = cfg["n_q_heads"], cfg["n_kv_heads"], cfg["head_dim"], cfg["n_sinks"]
     levels = W.levels(cfg)
     windows = W.windows_of(cfg, levels)
-    # warmup, the timed region, then the kernel-timing region (same length)
+    # warmup, the timed region, then the kernel-timing region (same length);
+    # with replicas, step s decodes replica s mod R, for its (s // R)-th time
+    R = max(1, args.replicas)
     total_steps = args.warmup + 2 * args.steps
+    rep_steps = (total_steps + R - 1) // R
     prompts = W.prompts(cfg)
     max_ctx = cfg["max_ctx"]
-    if total_steps > cfg["steps"]:
+    if rep_steps > cfg["steps"]:
         # keep the final context at max_ctx: start from a shorter prompt
-        extra = total_steps - cfg["steps"]
+        extra = rep_steps - cfg["steps"]
         prompts = [max(1, p - extra) for p in prompts]
     scale = 1.0 / math.sqrt(D)
 
@@ -121,13 +128,14 @@ def main():
     n_pages = None
     if args.paged:
         # every full unit of every layer holds ceil(n_b / 256) pages at the
-        # final length n_b = prompt_b + total_steps
+        # final length n_b = prompt_b + rep_steps
         full = sum(1 for l in range(L) for h in range(Hkv)
                    if windows[l][h] == 0 or S + windows[l][h] >= max_ctx)
-        n_pages = full * sum((p + total_steps + hwkv.PAGE_TOKENS - 1) // hwkv.PAGE_TOKENS
+        n_pages = full * sum((p + rep_steps + hwkv.PAGE_TOKENS - 1) // hwkv.PAGE_TOKENS
                              for p in prompts)
-    cache = hwkv.cache_alloc(pol, B, max_ctx, kv_format=fmt, k_scale=scales, v_scale=scales,
-                             n_pages=n_pages)
+    caches = [hwkv.cache_alloc(pol, B, max_ctx, kv_format=fmt, k_scale=scales, v_scale=scales,
+                               n_pages=n_pages) for _ in range(R)]
+    cache = caches[0]
     cache_bytes = hwkv.cache_bytes(pol, B, max_ctx, fmt, n_pages=n_pages)
     reserved_bytes = hwkv.cache_bytes(pol, B, max_ctx, fmt)
     ws = torch.zeros(hwkv.decode_workspace_bytes(cache), dtype=torch.uint8, device=dev)
@@ -136,14 +144,15 @@ def main():
     osc = cfg.get("outlier_scale", 1.0)
 
     t0 = time.time()
-    for l in range(L):
-        for b in range(B):
-            k = W.normal_bf16_device((prompts[b], Hkv, D), cfg["seed"], l, W.K, b, device=dev,
-                                     scale_channels=outl, scale=osc)
-            v = W.normal_bf16_device((prompts[b], Hkv, D), cfg["seed"], l, W.V, b, device=dev,
-                                     scale_channels=outl, scale=osc)
-            hwkv.prefill_write(cache, l, b, 0, k, v)
-            del k, v
+    for r, c in enumerate(caches):                # replica r: its own seeded streams
+        for l in range(L):
+            for b in range(B):
+                k = W.normal_bf16_device((prompts[b], Hkv, D), cfg["seed"], l, W.K, b + 4096 * r,
+                                         device=dev, scale_channels=outl, scale=osc)
+                v = W.normal_bf16_device((prompts[b], Hkv, D), cfg["seed"], l, W.V, b + 4096 * r,
+                                         device=dev, scale_channels=outl, scale=osc)
+                hwkv.prefill_write(c, l, b, 0, k, v)
+                del k, v
     torch.cuda.synchronize()
     prefill_s = time.time() - t0
 
@@ -166,19 +175,20 @@ def main():
         for l in range(L):
             tot = 0
             for b in range(B):
-                n = prompts[b] + step_idx + 1
+                n = prompts[b] + step_idx // R + 1
                 for h in range(Hkv):
                     tot += min(n, caps[l][h]) * D * 2 * eb
             per_layer.append(tot)
         return per_layer
 
     def run_step(s):
+        c = caches[s % R]
         for l in range(L):
             if args.unfused:
-                hwkv.append(cache, l, kn[s, l], vn[s, l])
-                hwkv.decode_attn(cache, l, qs[s, l], scale, out[l], ws)
+                hwkv.append(c, l, kn[s, l], vn[s, l])
+                hwkv.decode_attn(c, l, qs[s, l], scale, out[l], ws)
             else:
-                hwkv.append_decode_attn(cache, l, kn[s, l], vn[s, l], qs[s, l], scale, out[l], ws)
+                hwkv.append_decode_attn(c, l, kn[s, l], vn[s, l], qs[s, l], scale, out[l], ws)
 
     for s in range(args.warmup):
         run_step(s)
@@ -205,11 +215,16 @@ def main():
     # streams every resident K/V byte) and its merge kernel with start and
     # stop HIP events on the same stream, which take the kernels' own start
     # and end times.
-    hwkv.decode_timing(cache, True)
+    for c in caches:
+        hwkv.decode_timing(c, True)
     for i in range(args.steps):
         run_step(args.warmup + args.steps + i)
-    split_ms, merge_ms, launches = hwkv.decode_timing_read(cache)
-    hwkv.decode_timing(cache, False)
+    split_ms = merge_ms = 0.0
+    launches = 0
+    for c in caches:
+        sp, mg, n = hwkv.decode_timing_read(c)
+        hwkv.decode_timing(c, False)
+        split_ms, merge_ms, launches = split_ms + sp, merge_ms + mg, launches + n
     bytes_t = [sum(kv_bytes(args.warmup + args.steps + i)) for i in range(args.steps)]
     split_avg_ms = split_ms / launches
     merge_avg_ms = merge_ms / launches
@@ -238,6 +253,7 @@ def main():
         "config": {
             "kv_format": fmt,
             "paged": bool(args.paged),
+            "replicas": R,
             "cache_bytes": int(cache_bytes),
             "cache_bytes_reserved_layout": int(reserved_bytes),
             "workload": (f"{cfg['name']}: {L} residual global layers, batch {B}, "
@@ -268,7 +284,8 @@ def main():
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(args, cfg, prompts, windows, caps, scale, outl, osc,
                                               dev, ms_per_step, bytes_per_step, eb, scales)
-    cache.free()
+    for c in caches:
+        c.free()
     print(json.dumps(result), flush=True)
 
 
