@@ -336,6 +336,7 @@ def cpu_baseline(args, cfg, prompts, windows, caps, scale, outl, osc, dev, gpu_m
     Hq, Hkv, D = cfg["n_q_heads"], cfg["n_kv_heads"], cfg["head_dim"]
     threads = max(1, min(16, os.cpu_count() or 1))
     done_bytes, spent, layers = 0, 0.0, 0
+    first = None                   # layer 0's inputs, timed again on one core
     step = args.warmup  # the first timed step
     for l in range(L):
         kh, vh, t = [], [], []
@@ -363,6 +364,8 @@ def cpu_baseline(args, cfg, prompts, windows, caps, scale, outl, osc, dev, gpu_m
             t0 = time.perf_counter()
             oracle.decode_layer(q, kh, vh, t, cfg["n_sinks"], windows[l], scale,
                                 n_threads=threads)
+            if first is None:
+                first = (q, kh, vh, t, l)
         else:
             sc = scales[l] if scales is not None else np.ones(Hkv, dtype=np.float32)
             kv = [np.stack([KF.values(KF.store(x[:, h], fmt, sc[h]), fmt, sc[h])
@@ -381,6 +384,18 @@ def cpu_baseline(args, cfg, prompts, windows, caps, scale, outl, osc, dev, gpu_m
         if spent >= args.cpu_seconds:
             break
     us_per_step = spent / done_bytes * step_bytes * 1e6
+    one_core = None
+    if first is not None:
+        q, kh, vh, t, l = first
+        t0 = time.perf_counter()
+        oracle.decode_layer(q, kh, vh, t, cfg["n_sinks"], windows[l], scale, n_threads=1)
+        s1 = time.perf_counter() - t0
+        b1 = sum(min(prompts[b] + step + 1, caps[l][h]) * D * 2 * eb
+                 for b in range(B) for h in range(Hkv))
+        one_core = {"value": round(s1 / b1 * step_bytes * 1e6, 1), "unit": "us/step",
+                    "gbs": round(b1 / s1 / 1e9, 3), "sample": f"layer {l} of step {step}",
+                    "seconds": round(s1, 2)}
+        del first
     model = ""
     try:
         with open("/proc/cpuinfo") as f:
@@ -395,8 +410,10 @@ def cpu_baseline(args, cfg, prompts, windows, caps, scale, outl, osc, dev, gpu_m
         "unit": "us/step",
         "gbs": round(done_bytes / spent / 1e9, 3),
         "cores": threads,
+        "hardware_concurrency": os.cpu_count(),
         "cpu": model,
         "kind": "oracle",
+        "one_core": one_core,
         "sample": (f"decode step {step} (first timed step), layers 0..{layers - 1} of {L}, every "
                    f"sequence and query head; fp64 masked-full-history oracle"
                    f"{'' if fmt == 'bf16' else ' over the stored ' + fmt + ' values'}, "
