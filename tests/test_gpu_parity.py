@@ -217,6 +217,8 @@ def test_capacity_errors_leave_state():
 # ---------------------------------------------------------------------------
 @pytest.mark.timeout(900)
 def test_ctx32k_workload():
+    """Residency of every unit after prefill and after every one of the 256
+    steps; outputs at 34 seeded steps (the first and the last among them)."""
     cfg = W.CONFIGS["ctx32k"]
     r = Run(cfg)
     with timed("ctx32k prefill"):
@@ -225,12 +227,12 @@ def test_ctx32k_workload():
     check = set(W.rng(cfg["seed"], 0, W.SAMPLE, 0).choice(cfg["steps"], size=32, replace=False).tolist())
     check |= {0, cfg["steps"] - 1}
     worst = 0.0
-    with timed("ctx32k steps"):
+    with timed("ctx32k steps, residency of every unit after each"):
         for st in range(cfg["steps"]):
             qa, out = r.step(0)
             if st in check:
                 worst = max(worst, r.check_out(0, qa, out, f"ctx32k step {st}"))
-    r.check_layer(0)
+            r.check_layer(0)
     log(f"ctx32k: levels {r.levels} max rel err {worst:.3e}")
     r.free()
 
@@ -269,25 +271,26 @@ def test_ctx112k_workload_full_size():
 # ---------------------------------------------------------------------------
 @pytest.mark.timeout(1200)
 def test_batch16_workload_full_size():
+    """Residency of every (sequence, unit) after prefill and at the end;
+    outputs of every layer and sequence at the first and the last step."""
     cfg = W.CONFIGS["batch16"]
-    track = [0, 5]
-    r = Run(cfg, track=track, device_gen=True)
+    r = Run(cfg, device_gen=True)
     log(f"batch16 prompts {r.prompts}")
     with timed("batch16 prefill"):
         for l in range(cfg["n_layers"]):
             for b in range(cfg["batch"]):
                 r.prefill(l, b)
-            if l in track:
-                r.check_layer(l)
+            r.check_layer(l)
     worst = 0.0
     with timed("batch16 64 steps x 8 layers"):
         for st in range(cfg["steps"]):
             for l in range(cfg["n_layers"]):
                 qa, out = r.step(l)
-                if st in (0, cfg["steps"] - 1) and l in track:
+                if st in (0, cfg["steps"] - 1):
                     worst = max(worst, r.check_out(l, qa, out, f"batch16 layer {l} step {st}"))
-    for l in track:
-        r.check_layer(l)
+    with timed("batch16 final residency"):
+        for l in range(cfg["n_layers"]):
+            r.check_layer(l)
     log(f"batch16: max rel err {worst:.3e}")
     r.free()
 
