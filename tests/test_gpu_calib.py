@@ -237,6 +237,29 @@ def test_replay_64_windows():
     log(f"64 windows: {len(rows)} rows, outputs {ratio:.3f} of the bound, score error {serr:.2e}")
 
 
+def test_replay_full_only_and_single_rows():
+    """No finite window (the full candidate alone), and one sampled row at
+    the first, a middle and the last position, with and without sinks."""
+    N, Hkv, G, D = 5000, 2, 4, 128
+    kh = W.normal_bf16((N, Hkv, D), 45, 0, W.K, 0)
+    vh = W.normal_bf16((N, Hkv, D), 45, 0, W.V, 0)
+    scale = 1.0 / math.sqrt(D)
+    for S in (0, 4):
+        rows = [3, 777, 2048, 4999]
+        qh = W.normal_bf16((len(rows), Hkv * G, D), 45, S, W.Q_PROMPT, 0)
+        res = replay(up(kh, "cuda:0"), up(vh, "cuda:0"), up(qh, "cuda:0"), rows, [], S, scale)
+        ref = oracle.replay_outputs(qh, kh, vh, rows, S, [0], scale, n_threads=16)
+        vb = np.repeat(vmax_retained(vh, rows, [], S), G, axis=2)
+        ratio = float((np.abs(res["outs"] - ref) / (P_ROUND * vb)).max())
+        assert np.all(np.isfinite(res["outs"])) and ratio <= 1.0, (S, ratio)
+        for t in (0, 2500, N - 1):
+            q1 = W.normal_bf16((1, Hkv * G, D), 46, t, W.Q_PROMPT, 0)
+            res = replay(up(kh, "cuda:0"), up(vh, "cuda:0"), up(q1, "cuda:0"), [t], [1, 64, 3000],
+                         S, scale)
+            ref = oracle.replay_outputs(q1, kh, vh, [t], S, [1, 64, 3000, 0], scale)
+            check_all(res, ref, kh, vh, [t], [1, 64, 3000], S, G, f"one row at {t}, S={S}")
+
+
 def test_replay_zero_values_score_one():
     """V = 0 makes every output the zero vector: stabilised cosine 1."""
     kh = W.normal_bf16((100, 1, 64), 33, 0, W.K, 0)
