@@ -461,8 +461,14 @@ def prefill_main(args, dev):
     k = W.normal_bf16_device((N, Hkv, D), cfg["seed"], 0, W.K, 0, device=dev)
     v = W.normal_bf16_device((N, Hkv, D), cfg["seed"], 0, W.V, 0, device=dev)
     out = torch.empty((N, Hq, D), dtype=torch.float32, device=dev)
-    # one fresh cache per step (prefill fills it), allocated before timing
-    caches = [hwkv.cache_alloc(pol, 1, cfg["max_ctx"]) for _ in range(warmup + 2 * steps)]
+    # one fresh cache per step (prefill fills it), allocated before timing;
+    # --paged: the full units take pages of 256 rows as the prompt grows
+    n_pages = None
+    if args.paged:
+        full = sum(1 for w in windows if w == 0 or S + w >= cfg["max_ctx"])
+        n_pages = full * ((cfg["max_ctx"] + hwkv.PAGE_TOKENS - 1) // hwkv.PAGE_TOKENS)
+    caches = [hwkv.cache_alloc(pol, 1, cfg["max_ctx"], n_pages=n_pages)
+              for _ in range(warmup + 2 * steps)]
     torch.cuda.synchronize()
 
     def run_step(cache, events=None):
@@ -516,6 +522,7 @@ def prefill_main(args, dev):
             "workload": (f"prefill128k: {N}-token prompt in {C}-token chunks, 1 layer, batch 1, "
                          f"{Hq} q / {Hkv} kv heads, head_dim {D}, {S} sinks, kv head windows "
                          f"{windows} (0 = full); per chunk prefill_attn then prefill_write"),
+            "paged": bool(args.paged),
             "algorithmic_flop_per_step": step_flop,
         },
         "roofline": {
