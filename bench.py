@@ -50,7 +50,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=60)
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--workload", default="ctx112k",
-                    choices=["ctx112k", "ctx32k", "batch16", "pr1", "prefill128k", "calib128k"])
+                    choices=["ctx112k", "ctx32k", "batch16", "pr1", "prefill128k", "calib128k",
+                             "probe"])
     ap.add_argument("--kv-format", default="bf16", choices=["bf16", "f16", "fp8"],
                     help="cache format of the decode workloads (fp8: E4M3 with the "
                          "workload's per-unit scales)")
@@ -102,6 +103,9 @@ def main():
         return
     if args.workload == "calib128k":
         calib_main(args, dev)
+        return
+    if args.workload == "probe":
+        probe_main(args, dev)
         return
     cfg = W.CONFIGS[args.workload]
     L, B = cfg["n_layers"], cfg["batch"]
@@ -560,6 +564,64 @@ def prefill_traffic(n_chunks):
     if rec.get("kernel_source_sha256_16") != profiling.kernel_source_hash(rec["kernel"]):
         return None
     return round(rec["fetch_bytes"] + rec["write_bytes"])
+
+
+def probe_main(args, dev):
+    """The practical read ceiling beside the decode roofline: passes of 16
+    launches of the library's read probe, each over its own region of the
+    ctx112k mean layer size (213.5 MB), as the 16 decode_split launches of a
+    step read theirs; the flat grid-stride sweep at 2, 4 and 8 wavefronts per
+    SIMD, and the split kernel's own walk without its arithmetic."""
+    import torch
+
+    from paper_2609_02029_amd import hwkv
+
+    L, per = 16, 3416322048 // 16 // 65536 * 65536
+    buf = torch.empty(L * per, dtype=torch.uint8, device=dev)
+    buf.fill_(1)
+    sink = torch.zeros(1, dtype=torch.float32, device=dev)
+    reps = max(1, min(args.steps, 20))
+    out = {}
+    for name, pattern, wps in [("flat, 2 waves/SIMD, 4 loads in flight", 0, 2),
+                               ("flat, 4 waves/SIMD, 2 loads in flight", 0, 4),
+                               ("flat, 8 waves/SIMD, 1 load in flight", 0, 8),
+                               ("decode_split walk without arithmetic, 4 loads in flight "
+                                "(the kernel's)", 1, 4),
+                               ("decode_split walk, 2 loads in flight", 1, 2),
+                               ("decode_split walk, 8 loads in flight", 1, 8)]:
+        def one_pass():
+            for l in range(L):
+                hwkv.read_probe(buf[l * per:(l + 1) * per], pattern, wps, sink)
+        for _ in range(3):
+            one_pass()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            one_pass()
+        b.record()
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b)
+        out[name] = {"gbs": round(L * per * reps / (ms * 1e-3) / 1e9, 1),
+                     "us_per_launch": round(ms * 1e3 / (reps * L), 2)}
+    best = max(v["gbs"] for k, v in out.items() if k.startswith("flat"))
+    result = {
+        "metric": "read-probe GB/s (16 launches of 213.5 MB, the 112K decode step's reads)",
+        "value": best,
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": reps,
+        "warmup": 3,
+        "frac_of_hbm_peak": round(best / HBM_PEAK_GBS, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u8 (loads only)",
+        "data": "synthetic",
+        "config": {"workload": f"probe: {L} regions of {per} bytes, one launch each per pass",
+                   "patterns": out},
+    }
+    print(json.dumps(result), flush=True)
 
 
 def calib_main(args, dev):

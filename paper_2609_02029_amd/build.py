@@ -19,7 +19,7 @@ ARCH = "gfx950"
 
 SOURCES = ["hwkv_api.hip", "decode_kernels.hip", "decode_split_bf16.hip",
            "decode_split_f16.hip", "decode_split_fp8.hip", "write_kernels.hip",
-           "prefill_attn_kernels.hip", "calib_kernels.hip"]
+           "prefill_attn_kernels.hip", "calib_kernels.hip", "probe_kernels.hip"]
 
 CFLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",

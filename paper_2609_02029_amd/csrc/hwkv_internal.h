@@ -264,6 +264,17 @@ constexpr int kReplayTilesPerSplit = 128;   // 32-key tiles per split, at most
 constexpr int kReplayMinTilesPerSplit = HWKV_REPLAY_MIN_TILES;
 hipError_t launch_calib_means(const CalibArgs &a, hipStream_t s);
 
+// Read-bandwidth probes (loads only): pattern 0 flat grid-stride sweep,
+// pattern 1 the decode split kernel's tile walk.
+struct ProbeArgs {
+  const uint8_t *buf;
+  int64_t bytes;                 // a multiple of 64 KiB below 2^31
+  float *sink;                   // written only for an impossible fold
+  int32_t pattern;
+  int32_t waves_per_simd;        // pattern 0: 2, 4 or 8
+};
+hipError_t launch_probe(const ProbeArgs &a, int n_cus, hipStream_t s);
+
 }  // namespace hwkv
 
 // Kernel arguments travel by value; the kernarg segment is limited to 4 KiB.

@@ -330,3 +330,19 @@ def test_largest_capacity():
     pol = hwkv.policy_set(1, 1, 2, 256, 0, [0], [[0]])
     with pytest.raises(hwkv.HwkvError):
         hwkv.cache_bytes(pol, 1, cap + 64)
+
+
+# ---------------------------------------------------------------------------
+# the read probe of the decode roofline: every pattern runs over a buffer of
+# equal words (every fold is zero), and leaves the sink untouched
+# ---------------------------------------------------------------------------
+def test_read_probe_runs():
+    dev = torch.device("cuda:0")
+    buf = torch.full((64 << 20,), 7, dtype=torch.uint8, device=dev)
+    sink = torch.zeros(1, dtype=torch.float32, device=dev)
+    for pattern, wps in [(0, 2), (0, 4), (0, 8), (1, 2), (1, 4), (1, 8)]:
+        hwkv.read_probe(buf, pattern, wps, sink)
+        hwkv.read_probe(buf[: 3 << 16], pattern, wps, sink)   # fewer tiles than waves
+    torch.cuda.synchronize()
+    assert float(sink.cpu()[0]) == 0.0
+

@@ -554,3 +554,18 @@ def test_paged_pool_checks_before_device_work(hw):
     assert L.hwkv_cache_pages(h, ctypes.byref(t), ctypes.byref(f)) == hw.OK
     assert (t.value, f.value) == (0, 0)
     L.hwkv_cache_free(h)
+
+
+def test_read_probe_argument_errors(hw):
+    """The read probe validates everything before touching the device."""
+    L = hw._lib
+    f = ctypes.c_void_p(FAKE)
+    assert L.hwkv_read_probe(None, 65536, 0, 2, f, None) == hw.EINVAL
+    assert L.hwkv_read_probe(f, 65536, 0, 2, None, None) == hw.EINVAL
+    for bytes_ in (0, -65536, 65535, 65536 + 1024, 1 << 31):
+        assert L.hwkv_read_probe(f, bytes_, 0, 2, f, None) == hw.EINVAL, bytes_
+    assert L.hwkv_read_probe(f, 65536, 2, 2, f, None) == hw.EINVAL
+    for pattern in (0, 1):
+        for wps in (0, 1, 3, 16):
+            assert L.hwkv_read_probe(f, 65536, pattern, wps, f, None) == hw.EINVAL, wps
+
