@@ -480,7 +480,8 @@ int hwkv_decode_timing_read(hwkv_cache *cache, double *split_ms,
                             double *merge_ms, int64_t *launches);
 
 /* Read-bandwidth probe, for the decode roofline's practical ceiling: one
- * pass of 16-byte loads over bytes [0, bytes) of a device buffer, enqueued
+ * pass of 16-byte non-temporal loads (the decode split kernel's cache
+ * policy) over bytes [0, bytes) of a device buffer, enqueued
  * on `stream` (loads only: the data is folded into one value, written to
  * *sink only if it equals an impossible pattern).
  *   pattern 0  flat grid-stride sweep: consecutive wavefronts read

@@ -1,7 +1,8 @@
 // probe_kernels.hip -- read-bandwidth probes for the decode roofline (gfx950).
 //
-// Loads only: the loaded words are folded into one value, which is written
-// to *sink only if it equals an impossible pattern, so the loads stay.
+// Loads only, non-temporal (the split kernel's cache policy): the loaded
+// words are folded into one value, which is written to *sink only if it
+// equals an impossible pattern, so the loads stay.
 //  * flat: consecutive wavefronts read consecutive 1 KiB pieces (16 bytes a
 //    lane) and stride by the whole grid, PF loads in flight per lane.  At
 //    any moment the grid reads one compact window of the buffer: the
@@ -19,9 +20,10 @@ namespace {
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
 // a load in flight stays a whole 16-byte value until it is consumed (a fold
-// at issue would wait for it there)
+// at issue would wait for it there); non-temporal, as the split kernel's
+// streaming loads are
 __device__ __forceinline__ u32x4_t load16(__amdgpu_buffer_rsrc_t r, int off) {
-  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 2);
 }
 __device__ __forceinline__ uint32_t fold(u32x4_t v) { return v.x ^ v.y ^ v.z ^ v.w; }
 
