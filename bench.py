@@ -646,8 +646,15 @@ def calib_main(args, dev):
     outs = torch.empty((K + 1, R, Hq, D), dtype=torch.float32, device=dev)
     scores = torch.empty((K, R, Hq), dtype=torch.float32, device=dev)
     means = torch.empty((K, Hkv), dtype=torch.float32, device=dev)
-    ws = torch.zeros(hwkv.calib_workspace_bytes(Hq, D, S, k.shape[0], R), dtype=torch.uint8,
-                     device=dev)
+    fmt = args.kv_format
+    if fmt not in ("bf16", "fp8"):
+        raise SystemExit("calib128k replays bf16 or fp8 caches (binary16 values are not bf16)")
+    # fp8: every candidate over the trace as an fp8 cache stores it, with
+    # the decode workloads' scale recipe per kv head
+    scales = W.fp8_scales(cfg)[0] if fmt == "fp8" else None
+    ws = torch.zeros(hwkv.calib_workspace_bytes(Hq, D, S, k.shape[0], R, n_kv_heads=Hkv,
+                                                kv_format=fmt),
+                     dtype=torch.uint8, device=dev)
     # algorithmic FLOP: every candidate of every row and q head, 4d per
     # retained key
     pairs = 0
@@ -661,7 +668,8 @@ def calib_main(args, dev):
     steps, warmup = min(max(1, args.steps), 10), min(max(0, args.warmup), 3)
 
     def run():
-        hwkv.calib_replay(k, v, rows, q, windows, S, scale, outs, scores, means, ws)
+        hwkv.calib_replay(k, v, rows, q, windows, S, scale, outs, scores, means, ws,
+                          kv_format=fmt, k_scale=scales, v_scale=scales)
 
     for _ in range(warmup):
         run()
@@ -687,12 +695,14 @@ def calib_main(args, dev):
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16 (fp32 accumulate)",
+        "dtype": ("bf16 (fp32 accumulate)" if fmt == "bf16"
+                  else "fp8-e4m3 trace values, bf16 q (fp32 accumulate)"),
         "data": "synthetic",
         "config": {
             "workload": (f"calib128k: one traced layer of {N} tokens, {R} query rows from the "
                          f"final quarter, {Hq} q / {Hkv} kv heads, head_dim {D}, {S} sinks, "
                          f"candidates {windows} + full; outputs, scores and per-head means"),
+            "kv_format": fmt,
             "algorithmic_flop_per_step": flop,
             "computed_flop_per_step": flop_once,
             "means": [[round(float(x), 5) for x in row] for row in means.cpu().numpy()],
@@ -731,7 +741,9 @@ def calib_main(args, dev):
             "cores": threads,
             "kind": "oracle",
             "sample": (f"{done} of the {R} rows (all {Hq} q heads, every candidate), fp64 "
-                       f"masked-full-history oracle, {spent:.1f} s; scaled by retained pairs"),
+                       f"masked-full-history oracle, {spent:.1f} s; scaled by retained pairs"
+                       + ("" if fmt == "bf16" else "; over the bf16 trace (the C oracle's "
+                          "cost does not depend on the values)")),
         }
     print(json.dumps(result), flush=True)
 
