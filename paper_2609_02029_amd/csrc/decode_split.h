@@ -137,15 +137,19 @@ __device__ __forceinline__ uint4 bload(__amdgpu_buffer_rsrc_t r, int offset) {
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
-// One chunk (8 elements) of format F: a 16- or 8-byte buffer load.
+// One chunk (8 elements) of format F: a 16- or 8-byte buffer load at a
+// per-lane offset plus a wave-uniform one (soffset, an SGPR: no vector add);
+// the range check applies to their sum.
 template <int F>
 __device__ __forceinline__ typename KvFormat<F>::Chunk bload_chunk(
-    __amdgpu_buffer_rsrc_t r, int offset) {
+    __amdgpu_buffer_rsrc_t r, int offset, int soffset = 0) {
   if constexpr (KvFormat<F>::kBytes == 2) {
-    return bload(r, offset);
+    const u32x4_t v =
+        __builtin_amdgcn_raw_buffer_load_b128(r, offset, soffset, HWKV_DECODE_AUX);
+    return make_uint4(v.x, v.y, v.z, v.w);
   } else {
     const u32x2_t v =
-        __builtin_amdgcn_raw_buffer_load_b64(r, offset, 0, HWKV_DECODE_AUX);
+        __builtin_amdgcn_raw_buffer_load_b64(r, offset, soffset, HWKV_DECODE_AUX);
     return make_uint2(v.x, v.y);
   }
 }
@@ -374,7 +378,7 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
   int rk = rot_k(t), rv = rot_v(t);
   int kofs = (t * 64 - r0) * D * EB + lane * LB;
   if (t < n_tiles) static_for<PF>([&](auto jc) {
-    buf[jc.value] = bload_chunk<F>(krs, kofs + ((jc.value + rk) & (NC - 1)) * 64 * LB);
+    buf[jc.value] = bload_chunk<F>(krs, kofs, ((jc.value + rk) & (NC - 1)) * 64 * LB);
   });
   for (int k = 0; k < kTilesPerWave && t < n_tiles; ++k) {
     const int slot0 = t * 64;
@@ -386,12 +390,12 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
     int kofs_n = (tn * 64 - r0) * D * EB + lane * LB;
     uint64_t qaddr = (uint64_t)qc;
     // load j of this tile's stream: K chunk (j + rk) mod NC, or V step
-    // (j - NC + rv) mod NC; the row offset stays in the range-checked part
-    // of the buffer address, so V rows past n_valid still read as zero
+    // (j - NC + rv) mod NC; V's descriptor ends at row n_valid, so the
+    // rows past it read as zero
     auto ld = [&](auto jc) -> Chunk {
       constexpr int j = decltype(jc)::value;
-      if constexpr (j < NC)
-        return bload_chunk<F>(krs, kofs + ((j + rk) & (NC - 1)) * 64 * LB);
+      if constexpr (j < NC)   // K: the chunk step is uniform
+        return bload_chunk<F>(krs, kofs, ((j + rk) & (NC - 1)) * 64 * LB);
       else
         return bload_chunk<F>(vrs, vofs + ((j - NC + rv) & (NC - 1)) * RPS * D * EB);
     };
@@ -498,7 +502,7 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
         buf[j % PF] = ld(std::integral_constant<int, jn>{});
       } else {
         if (has_next)
-          buf[j % PF] = bload_chunk<F>(krs, kofs_n + ((jn - 2 * NC + rk_n) & (NC - 1)) * 64 * LB);
+          buf[j % PF] = bload_chunk<F>(krs, kofs_n, ((jn - 2 * NC + rk_n) & (NC - 1)) * 64 * LB);
       }
     };
     if constexpr (PAIR) {
