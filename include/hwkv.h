@@ -361,7 +361,9 @@ int hwkv_calib_workspace_bytes(int32_t n_q_heads, int32_t head_dim,
  *             the codebook in order; the full candidate is implicit
  *   k, v      device bf16 [n_hist][n_kv_heads][head_dim]: the layer's traced
  *             full-history keys (post-RoPE) and values
- *   rows      host int64 [n_rows], strictly increasing, in [0, n_hist)
+ *   rows      host int64 [n_rows], strictly increasing, in [0, n_hist);
+ *             read before the call returns (the library copies them into
+ *             pinned memory of its own and from there, on `stream`, into ws)
  *   q         device bf16 [n_rows][n_q_heads][head_dim]: traced queries
  *   outs      device fp32 [n_windows + 1][n_rows][n_q_heads][head_dim]:
  *             the candidate outputs in codebook order, the full one last

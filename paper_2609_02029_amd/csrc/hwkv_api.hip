@@ -13,6 +13,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <map>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -1025,6 +1026,51 @@ int64_t replay_max_splits(int64_t n_hist) {
   return (t + hwkv::kReplayTilesPerSplit - 1) / hwkv::kReplayTilesPerSplit;
 }
 
+// Row positions reach the device through a pinned host buffer per device,
+// so that their copy is asynchronous on the caller's stream.  A call reuses
+// the buffer once the previous call's copy from it (marked by an event) has
+// finished, which it has as soon as that call's first kernel ran.
+struct RowStage {
+  int32_t *host = nullptr;   // pinned, cap entries
+  int64_t cap = 0;
+  hipEvent_t copied = nullptr;
+};
+std::mutex g_row_stage_mu;
+std::map<int, RowStage> g_row_stage;
+
+// Enqueues the copy of rows[0, n) (as int32) to dst on st.
+int stage_rows(const int64_t *rows, int64_t n, void *dst, hipStream_t st) {
+  int dev = 0;
+  int rc = check_device(hipGetDevice(&dev), "hipGetDevice");
+  if (rc != HWKV_OK) return rc;
+  std::lock_guard<std::mutex> lock(g_row_stage_mu);
+  RowStage &rs = g_row_stage[dev];
+  if (!rs.copied) {
+    rc = check_device(hipEventCreateWithFlags(&rs.copied, hipEventDisableTiming),
+                      "hipEventCreateWithFlags");
+    if (rc != HWKV_OK) return rc;
+  } else {
+    rc = check_device(hipEventSynchronize(rs.copied), "hipEventSynchronize (rows)");
+    if (rc != HWKV_OK) return rc;
+  }
+  if (rs.cap < n) {
+    if (rs.host) (void)hipHostFree(rs.host);
+    rs.host = nullptr;
+    rs.cap = 0;
+    const int64_t cap = std::max<int64_t>(n, 1024);
+    rc = check_device(hipHostMalloc(reinterpret_cast<void **>(&rs.host), (size_t)cap * 4,
+                                    hipHostMallocDefault),
+                      "hipHostMalloc (rows)");
+    if (rc != HWKV_OK) return rc;
+    rs.cap = cap;
+  }
+  for (int64_t i = 0; i < n; ++i) rs.host[i] = (int32_t)rows[i];
+  rc = check_device(hipMemcpyAsync(dst, rs.host, (size_t)n * 4, hipMemcpyHostToDevice, st),
+                    "hipMemcpyAsync (rows)");
+  if (rc != HWKV_OK) return rc;
+  return check_device(hipEventRecord(rs.copied, st), "hipEventRecord (rows)");
+}
+
 // Partial sets of the workspace ([n_cols][D + 4] fp32 each): one per split,
 // one for the sinks, and two holding the windows' edge (m, l) pairs (at most
 // 64 windows x 2 floats <= 2 (D + 4) per column).
@@ -1138,13 +1184,8 @@ int hwkv_calib_replay_format(int32_t n_kv_heads, int32_t n_q_heads, int32_t head
     return fail(HWKV_EINVAL, "n_rows too large for one launch");
   hipStream_t st = (hipStream_t)stream;
 
-  // row positions to the device; the wait keeps the host buffer alive
-  std::vector<int32_t> r32(rows, rows + n_rows);
-  int rc = check_device(hipMemcpyAsync(ws, r32.data(), r32.size() * sizeof(int32_t),
-                                       hipMemcpyHostToDevice, st),
-                        "hipMemcpyAsync (rows)");
-  if (rc != HWKV_OK) return rc;
-  rc = check_device(hipStreamSynchronize(st), "hipStreamSynchronize");
+  // row positions to the device, asynchronously
+  int rc = stage_rows(rows, n_rows, ws, st);
   if (rc != HWKV_OK) return rc;
 
   int dev = 0, n_cus = 256;

@@ -373,3 +373,40 @@ def test_replay_format_errors():
     with pytest.raises(hwkv.HwkvError):
         hwkv.calib_replay(kh, kh, [10, 20], qh, [8], 0, 0.125, outs, sc, mn, ws[: need - 1],
                           kv_format="fp8")
+
+
+def test_replay_back_to_back_row_staging():
+    """Two replays enqueued on one stream without a wait between them, the
+    second with more rows than the library's initial row staging buffer (so
+    the buffer grows while the first call's copy may still be queued): each
+    equals the same replay run on its own."""
+    S, windows, D, G, Hkv, N = 4, [16, 64, 200], 64, 2, 1, 1500
+    kh = W.normal_bf16((N, Hkv, D), 41, 0, W.K, 0)
+    vh = W.normal_bf16((N, Hkv, D), 41, 0, W.V, 0)
+    rows_a = sorted({int(x) for x in np.random.default_rng(5).choice(N, size=40, replace=False)})
+    rows_b = list(range(N - 1100, N))
+    qa = W.normal_bf16((len(rows_a), Hkv * G, D), 41, 0, W.Q_PROMPT, 3)
+    qb = W.normal_bf16((len(rows_b), Hkv * G, D), 41, 0, W.Q_PROMPT, 4)
+    scale = 1.0 / math.sqrt(D)
+    k, v = up(kh, "cuda:0"), up(vh, "cuda:0")
+    alone_a = replay(k, v, up(qa, "cuda:0"), rows_a, windows, S, scale)
+    alone_b = replay(k, v, up(qb, "cuda:0"), rows_b, windows, S, scale)
+    K = len(windows)
+    bufs = []
+    for rows, q in ((rows_a, qa), (rows_b, qb)):
+        R = len(rows)
+        outs = torch.full((K + 1, R, G * Hkv, D), float("nan"), dtype=torch.float32, device="cuda:0")
+        scores = torch.full((K, R, G * Hkv), float("nan"), dtype=torch.float32, device="cuda:0")
+        means = torch.full((K, Hkv), float("nan"), dtype=torch.float32, device="cuda:0")
+        ws = torch.zeros(hwkv.calib_workspace_bytes(G * Hkv, D, S, N, R, n_kv_heads=Hkv),
+                         dtype=torch.uint8, device="cuda:0")
+        bufs.append((rows, up(q, "cuda:0"), outs, scores, means, ws))
+    torch.cuda.synchronize()
+    for rows, q, outs, scores, means, ws in bufs:        # no wait between the two
+        hwkv.calib_replay(k, v, rows, q, windows, S, scale, outs, scores, means, ws)
+    torch.cuda.synchronize()
+    for (rows, q, outs, scores, means, ws), alone in zip(bufs, (alone_a, alone_b)):
+        assert np.array_equal(outs.cpu().numpy().astype(np.float64), alone["outs"])
+        assert np.array_equal(scores.cpu().numpy().astype(np.float64), alone["scores"])
+        assert np.array_equal(means.cpu().numpy().astype(np.float64), alone["means"])
+    log(f"back-to-back replays of {len(rows_a)} and {len(rows_b)} rows equal the lone ones")
