@@ -18,6 +18,11 @@
 ``python -m paper_2609_02029_amd.profiling lds DB``
     LDS bank-conflict and LDS-active cycles per dispatch (SQ_LDS_BANK_CONFLICT,
     SQ_LDS_IDX_ACTIVE, GRBM_GUI_ACTIVE), as fractions of CU cycles
+``python -m paper_2609_02029_amd.profiling stalls DB``
+    per kernel, summed over its dispatches: where its wavefronts' cycles go
+    (SQ_WAIT_ANY, SQ_WAIT_INST_ANY, SQ_ACTIVE_INST_VALU / _VMEM / _LDS over
+    SQ_WAVE_CYCLES) and its VALU instructions per wavefront (SQ_INSTS_VALU
+    over SQ_WAVES)
 """
 import collections
 import hashlib
@@ -148,6 +153,29 @@ def traffic_record(db_fetch, db_write, mib, kernel="decode_split<256, 6, 0>"):
             "copy_mib": mib, "kernel_source_sha256_16": kernel_source_hash(kernel)}
 
 
+STALL_COUNTERS = ("SQ_WAIT_ANY", "SQ_WAIT_INST_ANY", "SQ_ACTIVE_INST_VALU",
+                  "SQ_ACTIVE_INST_VMEM", "SQ_ACTIVE_INST_LDS")
+
+
+def stalls(db):
+    """{kernel: (dispatches, {counter: fraction of SQ_WAVE_CYCLES}, VALU
+    instructions per wavefront)}."""
+    per = {}
+    for name in ("SQ_WAVE_CYCLES", "SQ_WAVES", "SQ_INSTS_VALU") + STALL_COUNTERS:
+        per[name] = counter(db, name)
+    out = {}
+    for k in sorted({v[0] for v in per["SQ_WAVE_CYCLES"].values()}):
+        ds = [d for d, (kk, _) in per["SQ_WAVE_CYCLES"].items() if kk == k]
+        tot = lambda name: sum(per[name].get(d, (k, 0.0))[1] for d in ds)
+        cyc = tot("SQ_WAVE_CYCLES")
+        if cyc <= 0:
+            continue
+        waves = tot("SQ_WAVES")
+        out[k] = (len(ds), {n: tot(n) / cyc for n in STALL_COUNTERS},
+                  tot("SQ_INSTS_VALU") / waves if waves else float("nan"))
+    return out
+
+
 def main(argv):
     if argv[0] == "kernels":
         print("| kernel | calls | mean us | median us | min us | max us | total us |")
@@ -191,6 +219,13 @@ def main(argv):
         print("|---|---|---|---|")
         for d, k, a, c in lds(argv[1]):
             print(f"| {d} | {k} | {a:.3f} | {c:.4f} |")
+    elif argv[0] == "stalls":
+        print("| kernel | dispatches | " + " | ".join(STALL_COUNTERS) +
+              " | VALU instructions per wavefront |")
+        print("|---|---|" + "---|" * len(STALL_COUNTERS) + "---|")
+        for k, (n, f, vpw) in stalls(argv[1]).items():
+            print(f"| {k} | {n} | " + " | ".join(f"{f[c]:.3f}" for c in STALL_COUNTERS) +
+                  f" | {vpw:.0f} |")
     else:
         raise SystemExit(__doc__)
 
