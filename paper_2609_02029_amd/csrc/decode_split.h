@@ -245,10 +245,10 @@ __device__ __forceinline__ float half_sum_pair(float x0, float x1) {
   return __builtin_bit_cast(float, (int)r[0]) + __builtin_bit_cast(float, (int)r[1]);
 }
 
-template <int D, int G, int F>
-__global__ __launch_bounds__(kWaves * 64)
-__attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
-    DecodeArgs a) {
+// The split phase with PFW chunk loads in flight per lane; instantiated by
+// decode_split (the default depth) and decode_split_deep (twice as deep).
+template <int D, int G, int F, int PFW>
+__device__ __forceinline__ void split_body(const DecodeArgs &a) {
   using Chunk = typename KvFormat<F>::Chunk;
   constexpr int EB = KvFormat<F>::kBytes;  // bytes per element
   constexpr int LB = 8 * EB;        // bytes per chunk
@@ -258,7 +258,6 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
   // loads in flight per lane (at most one tile's K chunks); the ring slot of
   // a load is its step number mod PF across tiles, so PF must divide 2 NC.
   // 8-byte loads keep twice as many in flight, for the same bytes.
-  constexpr int PFW = EB == 2 ? kPrefetch : kPrefetch8;
   constexpr int PF = PFW < NC ? PFW : NC;
   // fp8 values: p.v over token pairs with v_dot2_f32_f16 -- a lane's two
   // consecutive p.v steps read rows r and r + RPS of the same channels, whose
@@ -675,6 +674,40 @@ __attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(
 }
 
 
+template <int F>
+constexpr int kSplitDepth = KvFormat<F>::kBytes == 2 ? kPrefetch : kPrefetch8;
+
+template <int D, int G, int F>
+__global__ __launch_bounds__(kWaves * 64)
+__attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(DecodeArgs a) {
+  split_body<D, G, F, kSplitDepth<F>>(a);
+}
+
+// For launches with fewer split workgroups than CUs: the chip is not full,
+// so each wave keeps twice as many loads in flight.  (With the chip full the
+// default depth is faster: the arithmetic between loads is what the other
+// resident waves hide.)
+template <int D, int G, int F>
+__global__ __launch_bounds__(kWaves * 64)
+__attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split_deep(DecodeArgs a) {
+  split_body<D, G, F, 2 * kSplitDepth<F>>(a);
+}
+
+// Compute units of the current device (cached per device).
+inline int device_cus() {
+  static int cus[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cus[dev] <= 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        n < 1)
+      n = 256;
+    cus[dev] = n;
+  }
+  return cus[dev];
+}
+
 // Calls F<D, G>::run(args...) for the runtime (D, G) of a cache.
 template <template <int, int> class F, typename... Args>
 hipError_t dispatch_dg(int D, int G, Args &&...args) {
@@ -702,6 +735,14 @@ struct SplitLaunch {
   struct At {
     static hipError_t run(const DecodeArgs &a, int n, hipStream_t s, hipEvent_t e0,
                           hipEvent_t e1) {
+      // (8 q heads per kv head: the deeper ring does not fit the registers)
+      if constexpr (G < 8) {
+        if (n < device_cus()) {
+          hipExtLaunchKernelGGL((decode_split_deep<D, G, F>), dim3(n), dim3(kWaves * 64), 0,
+                                s, e0, e1, 0, a);
+          return hipGetLastError();
+        }
+      }
       hipExtLaunchKernelGGL((decode_split<D, G, F>), dim3(n), dim3(kWaves * 64), 0,
                             s, e0, e1, 0, a);
       return hipGetLastError();

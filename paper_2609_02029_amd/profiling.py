@@ -33,7 +33,7 @@ import sqlite3
 import statistics
 import sys
 
-KERNELS = (r"(decode_split<[^>]*>|decode_combine<[^>]*>|prefill_write<[^>]*>|append_token<[^>]*>"
+KERNELS = (r"(decode_split<[^>]*>|decode_split_deep<[^>]*>|decode_combine<[^>]*>|prefill_write<[^>]*>|append_token<[^>]*>"
            r"|prefill_attn<[^>]*>)")
 N_SIMD = 1024   # 256 CUs x 4 SIMDs
 N_CU = 256
@@ -45,7 +45,9 @@ N_XCD = 8
 def short(name):
     m = re.search(KERNELS, name or "")
     if m:
-        return m.group(1)
+        # the split phase at either load depth is one row: decode_split_deep
+        # serves the launches with fewer split workgroups than CUs
+        return m.group(1).replace("decode_split_deep<", "decode_split<")
     if "copyBuffer" in (name or ""):  # the runtime's blit kernel (torch copy_)
         return "copy:" + (name or "")[:60]
     return (name or "")[:60]

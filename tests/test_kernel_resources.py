@@ -74,6 +74,7 @@ def kernel_table(tmp_path_factory):
 
 def test_every_hot_kernel_is_present(kernel_table):
     for name in ["decode_split<256, 6, 0>", "decode_split<256, 6, 2>", "decode_split<256, 6, 1>",
+                 "decode_split_deep<256, 6, 0>", "decode_split_deep<256, 6, 2>",
                  "prefill_attn<256, 8>", "prefill_attn<128, 8>", "prefill_attn<64, 8>",
                  "replay_attn<256, 8>", "replay_merge<256>", "prefill_write<256, 0>",
                  "append_token<256, 2>"]:
@@ -93,6 +94,6 @@ def test_register_budgets(kernel_table):
     for n, (vg, _) in kernel_table.items():
         if n.startswith("prefill_attn<"):
             assert vg <= 256, (n, vg)
-        if n.startswith("decode_split<"):
+        if n.startswith("decode_split<") or n.startswith("decode_split_deep<"):
             d, g, _f = (int(x) for x in n[n.index("<") + 1:-1].split(","))
             assert vg <= (168 if (d, g) == (256, 8) else 128), (n, vg)
