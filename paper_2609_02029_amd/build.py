@@ -29,9 +29,18 @@ CFLAGS = [
 ]
 
 
+# Per-source hipcc flags beyond CFLAGS (none at present).
+SOURCE_FLAGS = {}
+
+
+def flags_for(src):
+    """hipcc flags of one source (the common flags and its own)."""
+    return [*CFLAGS, *SOURCE_FLAGS.get(src, [])]
+
+
 def _compile(src, verbose):
     obj = os.path.join(OBJDIR, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *CFLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *flags_for(src), "-c", os.path.join(CSRC, src), "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -3,6 +3,8 @@
 // once per cache format, in decode_split_<format>.hip.
 #include "decode_split.h"
 
+#include <algorithm>
+
 namespace hwkv {
 
 // Instantiated in the per-format sources.
@@ -48,10 +50,7 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine(
   constexpr int CH = D / CW;
   constexpr int LPR = CW / 4;                     // lanes per row
   constexpr int R = kCombineThreads / LPR;        // rows
-  constexpr int PS = G * (D + 2);
   constexpr int U = kCombineUnroll;
-  // 16-byte partial loads need the acc block 16-byte aligned: G even
-  constexpr bool VEC = (2 * G) % 4 == 0;
   constexpr int NWV = kCombineThreads / 64;      // wavefronts
   static_assert(R <= 64, "the row shifts are reduced by one wavefront");
   static_assert(64 % LPR == 0, "a row lies within one wavefront");
@@ -69,7 +68,10 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine(
   const int tid = threadIdx.x;
   const int r = tid / LPR, q = tid % LPR;
   const int c = ch * CW + 4 * q;
-  const float *base = a.ws + (size_t)(it.ws_split0 + sb) * PS;
+  // partial j of the item: acc row (j, h) is D floats (whole 128-byte lines
+  // per row of lanes), (m, l) of (j, h) two floats
+  const float *acc_base = a.part_acc + ((size_t)(it.ws_split0 + sb) * G + h) * D + c;
+  const float *ml_base = a.part_ml + ((size_t)(it.ws_split0 + sb) * G + h) * 2;
 
   float M = -INFINITY, L = 0.f;
   float4 A = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -79,14 +81,10 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine(
 #pragma unroll
     for (int u = 0; u < U; ++u) {  // every load of the round is in flight
       const int j = min(j0 + u * R, ns - 1);
-      const float *pj = base + (size_t)j * PS;
-      mj[u] = pj[h];
-      lj[u] = pj[G + h];
-      const float *pa = pj + 2 * G + h * D + c;
-      if constexpr (VEC)
-        aj[u] = *reinterpret_cast<const float4 *>(pa);
-      else
-        aj[u] = make_float4(pa[0], pa[1], pa[2], pa[3]);
+      const float2 ml = *reinterpret_cast<const float2 *>(ml_base + (size_t)j * G * 2);
+      mj[u] = ml.x;
+      lj[u] = ml.y;
+      aj[u] = *reinterpret_cast<const float4 *>(acc_base + (size_t)j * G * D);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u)
@@ -180,7 +178,11 @@ struct CombineLaunch {
 
 }  // namespace
 
-int decode_split_tokens() { return kWaves * kTilesPerWave * kTile; }
+int decode_workgroup_target(int fmt, int D, int G) {
+  // at most one workgroup per SIMD slot the register budget holds
+  const int per_cu4 = std::min(kDecodeWgPerCuX4, 4 * split_waves_per_eu(D, G, fmt));
+  return std::max(1, per_cu4 * device_cus() / 4);
+}
 int decode_combine_blocks_per_item(int D, int G) {
   return G * (D / (kCombineChan < D ? kCombineChan : D));
 }

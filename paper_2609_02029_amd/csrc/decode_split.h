@@ -10,16 +10,19 @@
 // Softmax is invariant to the order of the slots, so ring slots are read in
 // slot order and never unwrapped (keys are post-RoPE, positions are not used).
 //
-// Work decomposition.  One launch covers the (b, h) "items" of a layer; each
-// item's slots are cut into splits of kWaves * kTilesPerWave * 64 tokens and
-// every split is one workgroup, so the grid is balanced by bytes, not by unit
-// (full and windowed heads of one layer differ by up to ~56x in length).  The
-// G query heads of an item share every K/V byte read.  A split is one page
-// of a paged full unit, whose workgroup reads that page only.
+// Work decomposition.  One launch covers the (b, h) "items" of a layer.
+// Each item gets workgroups in proportion to its 64-slot tiles (the host
+// picks T tiles per workgroup for the whole launch, about four workgroups
+// per CU, and gives an item of n tiles ceil(n / T) workgroups), so the grid
+// is balanced by bytes, not by unit (full and windowed heads of one layer
+// differ by up to ~56x in length).  Workgroup j of an item takes its tiles
+// j, j + nwg, ... and walks them one after another with all four waves on
+// the same tile (split_body below).  The G query heads of an item share every
+// K/V byte read.
 //
-// Inside a wave, per 64-slot tile (one stream of chunk-sized buffer loads per
-// lane -- 16 bytes, or 8 for fp8 -- with kPrefetch, or kPrefetch8, loads
-// always in flight):
+// Inside a wave, per tile (one stream of chunk-sized buffer loads per lane
+// -- 16 bytes, or 8 for fp8 -- with PF loads always in flight, running on
+// into the next tile):
 //   q.k   one lane per slot: the K tile is stored slot-minor in 8-element
 //         channel chunks, so chunk g of the tile is contiguous and lane t
 //         reads its own slot's chunk; q is uniform and comes through scalar
@@ -27,26 +30,25 @@
 //         SGPR operand) with fp32 accumulate; fp8 keys are first widened to
 //         bf16 pairs (exact: every E4M3 value is a bf16 value) and take the
 //         same path, with the K scale folded into the logit scale; binary16
-//         keys meet the fp32-widened q in fp32 FMAs.  No cross-lane
-//         reduction is needed for the logits.
+//         keys meet the fp32-widened q in fp32 FMAs.  Each wave covers a
+//         quarter of the channels; the quarters are summed through LDS.
 //   softmax  online, base 2 (log2(e) folded into the scale); the tile max is
 //         one DPP row reduction plus four lane reads per head.
 //   p.v   lanes own 8 channels of one row (V row-major, a wave reads whole
 //         rows contiguously); p is broadcast through a per-wave LDS slice.
 //         bf16 and binary16 values are widened to fp32 (exactly) and take
 //         one fp32 FMA per (row, channel, head) with the fp32 weights; fp8
-//         values go over token pairs in binary16 (v_dot2_f32_f16, the
+//         values go over pairs of rows in binary16 (v_dot2_f32_f16, the
 //         weights rounded to binary16, the normaliser in fp32), and the fp8
 //         V scale multiplies the workgroup's result.
-//         The V buffer descriptor ends at row n_valid, so rows past it read
-//         as zero (and their p is zero).
+//         The V buffer descriptor of a tile ends at row n_valid, so rows
+//         past it read as zero (and their p is zero).
 // The fused append writes the new token, in the cache format, into its slot
-// at the start of the one workgroup whose split holds that slot, before any
+// at the start of the one workgroup whose tiles hold that slot, before any
 // of its waves read.
-// The waves of a workgroup are merged in LDS; a split either writes the final
-// output (single-split items) or a partial (m, l, acc) that the combine
-// kernel merges: m* = max m_j, l* = sum l_j 2^(m_j - m*),
-// out = sum acc_j 2^(m_j - m*) / l*.
+// A workgroup either writes the final output (an item with one workgroup) or
+// a partial (m, l, acc) that the combine kernel merges: m* = max m_j,
+// l* = sum l_j 2^(m_j - m*), out = sum acc_j 2^(m_j - m*) / l*.
 #pragma once
 
 #include <hip/hip_ext.h>
@@ -71,13 +73,7 @@ __device__ __forceinline__ void static_for(F &&f) {
   static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
-// Split geometry and load batching (compile-time; see decode_split_tokens).
-#ifndef HWKV_DECODE_WAVES
-#define HWKV_DECODE_WAVES 4
-#endif
-#ifndef HWKV_DECODE_TPW
-#define HWKV_DECODE_TPW 1
-#endif
+// Load batching (compile-time).
 #ifndef HWKV_DECODE_PREFETCH
 #define HWKV_DECODE_PREFETCH 4     // 16-byte chunk loads in flight
 #endif
@@ -90,17 +86,20 @@ __device__ __forceinline__ void static_for(F &&f) {
 #ifndef HWKV_DECODE_MINWAVES
 #define HWKV_DECODE_MINWAVES 4
 #endif
-#ifndef HWKV_DECODE_ROT
-#define HWKV_DECODE_ROT 7  // a tile's starting step: (ROT * tile) mod steps
-#endif
-constexpr int kWaves = HWKV_DECODE_WAVES;        // waves per workgroup
-constexpr int kTilesPerWave = HWKV_DECODE_TPW;   // 64-slot tiles per wave
+constexpr int kWaves = kDecodeWaves;             // waves per workgroup
 constexpr int kPrefetch = HWKV_DECODE_PREFETCH;  // 16-byte loads in flight
 constexpr int kPrefetch8 = HWKV_DECODE_PREFETCH8;  // 8-byte loads in flight
-constexpr int kMinWavesPerEU = HWKV_DECODE_MINWAVES;  // VGPR budget
-// A split is one page of a paged full unit: its workgroup reads one page.
-static_assert(kWaves * kTilesPerWave * kTile == kPageTokens && kTilesPerWave == 1,
-              "a decode split must be one page of 4 tiles, one per wave");
+// VGPR budget: four waves per SIMD (four workgroups per CU); eight q heads
+// per KV head (64 value accumulators per lane), and six with binary16 keys
+// at head_dim 128 and 256 (whose q.k widens the keys and q), need the
+// budget of three, and eight with binary16 keys at head_dim 128 and 256
+// the budget of two
+constexpr int split_waves_per_eu(int D, int G, int F) {
+  if (HWKV_DECODE_MINWAVES <= 2) return HWKV_DECODE_MINWAVES;
+  if (F == HWKV_KV_F16 && G == 8 && D >= 128) return HWKV_DECODE_MINWAVES - 2;
+  return (G == 8 || (F == HWKV_KV_F16 && G == 6 && D >= 128)) ? HWKV_DECODE_MINWAVES - 1
+                                                              : HWKV_DECODE_MINWAVES;
+}
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
@@ -229,12 +228,17 @@ __device__ __forceinline__ float wave_sum(float v) {
 
 template <int D, int G>
 struct SplitSmem {
-  static constexpr int NC = D / 8;
-  static constexpr int PST = (G + 3) & ~3;  // p stride per slot
-  float m[kWaves][G];
-  float l[kWaves][G];
-  float p[kWaves][64 * PST];                // per-wave p broadcast, tile loop
-  __attribute__((aligned(16))) float acc[kWaves][G][D];   // per-wave partials
+  static constexpr int PST = (G + 3) & ~3;  // weights per slot (fp32), 16-byte rows
+  struct Tile {
+    float lg[2][G][kWaves][64];     // partial logits (head, wave, slot), by tile parity
+    float p[64 * PST];              // the tile's weights (slot, head)
+  };
+  union {
+    Tile t;                                               // the tile walk
+    __attribute__((aligned(16))) float acc[kWaves][G][D];  // epilogue: wave sums
+  } u;
+  float alpha[G];                   // the tile's rescale of each head's sums
+  float m[G], l[G];                 // the workgroup's shift and normaliser
 };
 
 // x of lane l and x of lane l ^ 32 for two values at once (VALU lane swap):
@@ -245,27 +249,59 @@ __device__ __forceinline__ float half_sum_pair(float x0, float x1) {
   return __builtin_bit_cast(float, (int)r[0]) + __builtin_bit_cast(float, (int)r[1]);
 }
 
-// The split phase with PFW chunk loads in flight per lane; instantiated by
-// decode_split (the default depth) and decode_split_deep (twice as deep).
+// A wave-uniform 64-bit value in scalar registers.
+__device__ __forceinline__ int64_t uniform64(int64_t x) {
+  const uint64_t u = (uint64_t)x;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// One element of the page table read through the vector memory path: its
+// wait is ordered with the streaming loads (in issue order), so it does not
+// hold up the scalar loads of q the way a scalar load of the table would.
+// The value stays in a vector register until it is used (a read of it right
+// away would wait for every load in flight).
+__device__ __forceinline__ int page_entry(const int32_t *table, int idx) {
+  const __amdgpu_buffer_rsrc_t r = make_rsrc(table, (uint32_t)(idx + 1) * 4u);
+  return __builtin_amdgcn_raw_buffer_load_b32(r, 0, idx * 4, 0);
+}
+
+// The split phase with PFW chunk loads in flight per lane.
+//
+// A workgroup owns tiles j, j + nwg, j + 2 nwg, ... of its item (j is its
+// index among the item's nwg workgroups) and walks them one after another
+// with all four waves on the same tile: wave w takes the tile's K chunks
+// 4i + w and its V steps 4i + w (i = 0 .. NC/4 - 1), so at every step the
+// four waves read four adjacent chunk-rows of the tile, and at any moment the
+// launch's workgroups read a compact band of each unit (tile k of every
+// workgroup) rather than every tile of the layer at once.  Each wave forms
+// partial logits over its channels; the four partials of a slot meet in LDS,
+// where the owner of each head (wave h mod 4) adds them up and runs the
+// head's online softmax, and passes the weights and the rescale factor of
+// the running sums back through LDS; every wave accumulates p.v over its own
+// rows.  Two workgroup barriers per tile.
 template <int D, int G, int F, int PFW>
 __device__ __forceinline__ void split_body(const DecodeArgs &a) {
   using Chunk = typename KvFormat<F>::Chunk;
   constexpr int EB = KvFormat<F>::kBytes;  // bytes per element
   constexpr int LB = 8 * EB;        // bytes per chunk
   constexpr int NC = D / 8;         // chunks per row
-  constexpr int RPS = 64 / NC;      // rows per wave step in p.v
+  constexpr int RPS = 64 / NC;      // rows per V step
+  constexpr int NCW = NC / kWaves;  // a wave's K chunks, and V steps, per tile
+  constexpr int PIECES = 2 * NCW;   // a wave's loads per tile
+  // loads in flight per lane; the ring slot of a load is its piece number
+  // mod PF, the same in every tile
+  constexpr int PF = PFW < PIECES ? PFW : PIECES;
   constexpr int PST = SplitSmem<D, G>::PST;
-  // loads in flight per lane (at most one tile's K chunks); the ring slot of
-  // a load is its step number mod PF across tiles, so PF must divide 2 NC.
-  // 8-byte loads keep twice as many in flight, for the same bytes.
-  constexpr int PF = PFW < NC ? PFW : NC;
-  // fp8 values: p.v over token pairs with v_dot2_f32_f16 -- a lane's two
-  // consecutive p.v steps read rows r and r + RPS of the same channels, whose
-  // codes widen exactly to binary16 pairs; the weights enter the product
-  // rounded to binary16 (the normaliser keeps the fp32 weights)
+  // fp8 values: p.v over pairs of a wave's V steps with v_dot2_f32_f16 --
+  // steps 4(2i) + w and 4(2i + 1) + w read rows r and r + 4 RPS of the same
+  // channels, whose codes widen exactly to binary16 pairs; the weights enter
+  // the product rounded to binary16 (the normaliser keeps the fp32 weights)
   constexpr bool PAIR = F == HWKV_KV_FP8_E4M3;
-  static_assert(NC % 2 == 0, "p.v steps come in pairs");
-  static_assert((2 * NC) % PF == 0, "prefetch depth must divide 2 NC");
+  static_assert(NC % kWaves == 0, "the four waves share a tile's chunks");
+  static_assert(PIECES % PF == 0, "ring slots repeat from tile to tile");
+  static_assert(!PAIR || NCW % 2 == 0, "fp8 p.v takes a wave's V steps in pairs");
   __shared__ SplitSmem<D, G> sm;
 
   const DecodeItems &it = a.it;
@@ -279,70 +315,102 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
       hi = mid - 1;
   }
   const int item = lo;
-  const int split = blk - it.split_begin[item];
-  const int nsplit = it.split_begin[item + 1] - it.split_begin[item];
+  const int j = blk - it.split_begin[item];               // workgroup of the item
+  const int nwg = it.split_begin[item + 1] - it.split_begin[item];
   const int nv = it.n_valid[item];
   const int new_slot = it.new_slot[item];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int c8 = lane % NC;
   const int rsub = lane / NC;
-
-  // Region this workgroup reads: the item's rows, or for a paged unit the
-  // page of this split (rows r0 .. r0 + 255 of the unit); every address
-  // below is relative to the region's first row r0.
-  uint8_t *kbase, *vbase;
-  int r0 = 0, rows = nv;
-  if (it.pto[item] >= 0) {
-    const int64_t pg = a.page_table[it.pto[item] + split];
-    kbase = static_cast<uint8_t *>(a.cache) +
-            (a.pool_off + pg * 2 * kPageTokens * D) * EB;
-    vbase = kbase + kPageTokens * D * EB;
-    r0 = split * kPageTokens;
-    rows = min(nv - r0, kPageTokens);
-  } else {
-    kbase = static_cast<uint8_t *>(a.cache) + it.k_off[item] * EB;
-    vbase = static_cast<uint8_t *>(a.cache) + it.v_off[item] * EB;
-  }
-  // q is uniform across the workgroup: read it through the scalar path
-  // (constant address space), so v_dot2 takes it as an SGPR operand
-  const cu32x4_t *qc = (const cu32x4_t *)(a.q + (size_t)it.q_row[item] * D);
-  // Tiles of the item are dealt to its waves with a stride: wave wl of the
-  // item's nw waves takes tiles wl, wl + nw, ...  At any moment the item's
-  // waves then read a compact window of the cache instead of one far-apart
-  // region each, which keeps the DRAM traffic local.
   const int n_tiles = (nv + 63) / 64;
-  const int nw = nsplit * kWaves;
-  const int wl = split * kWaves + wave;
-  // fused append: the workgroup that reads new_slot stores the new token
-  // first; its waves then read it from the cache like any other slot
+  const int pto = it.pto[item];
+  // the item's K tiles and V rows, or the page pool of a paged unit (the
+  // offsets are uniform; said so, or the compiler may keep them in vector
+  // registers and then fail to feed them to the scalar operands below)
+  const int64_t koff = uniform64(pto >= 0 ? a.pool_off : it.k_off[item]);
+  const int64_t voff = uniform64(pto >= 0 ? a.pool_off + kPageTokens * D : it.v_off[item]);
+  uint8_t *const kbase = static_cast<uint8_t *>(a.cache) + koff * EB;
+  uint8_t *const vbase = static_cast<uint8_t *>(a.cache) + voff * EB;
+
+  // K tile t and the V rows of tile t (pg: its page, for a paged unit)
+  auto k_tile = [&](int t, int pg) -> uint8_t * {
+    if (pto >= 0)
+      return kbase + (size_t)pg * 2 * kPageTokens * D * EB +
+             (size_t)(t % (kPageTokens / 64)) * NC * 64 * LB;
+    return kbase + (size_t)t * NC * 64 * LB;
+  };
+  auto v_tile = [&](int t, int pg) -> uint8_t * {
+    if (pto >= 0)
+      return vbase + (size_t)pg * 2 * kPageTokens * D * EB +
+             (size_t)(t % (kPageTokens / 64)) * 64 * D * EB;
+    return vbase + (size_t)t * 64 * D * EB;
+  };
+  auto page_of = [&](int t) -> int {
+    return pto >= 0 ? page_entry(a.page_table, pto + t / (kPageTokens / 64)) : 0;
+  };
+  // K: the whole tile (slots past n_valid are masked); V: rows [0, n_valid)
+  // only, so that rows past it read as zero.  A tile that does not exist
+  // (has == false) gets empty descriptors: its loads return zero and touch
+  // no memory, so the loads of a tile's ring are issued the same way
+  // whether or not a next tile follows (a load behind a branch makes the
+  // compiler copy the ring's registers where the paths meet, and a copy of
+  // a register with a load in flight waits for every load in flight).
+  auto k_rsrc = [&](int t, int pg, bool has = true) {
+    return make_rsrc(k_tile(t, __builtin_amdgcn_readfirstlane(pg)),
+                     has ? (uint32_t)(NC * 64 * LB) : 0u);
+  };
+  auto v_rsrc = [&](int t, int pg, bool has = true) {
+    return make_rsrc(v_tile(t, __builtin_amdgcn_readfirstlane(pg)),
+                     has ? (uint32_t)(min(64, nv - 64 * t) * D * EB) : 0u);
+  };
+
+  // The walk visits logical tiles; logical tile 0 is the tile that holds
+  // new_slot (and that tile's logical number is 0), so that the new token's
+  // tile is always the first tile of workgroup 0, which stores the token
+  // before any of its waves read.  The order of the tiles does not change
+  // the softmax.
+  const int tile_new = new_slot >= 0 ? new_slot / 64 : 0;
+  auto phys = [&](int lt) {
+    return __builtin_amdgcn_readfirstlane(lt == 0 ? tile_new : (lt == tile_new ? 0 : lt));
+  };
+  // fused append: workgroup 0 stores the new token first; its waves then
+  // read it from the cache like any other slot
+  // (the same condition as new_slot >= 0 && j == 0, made explicitly uniform:
+  // written plainly, the compiler fails with an illegal VGPR to SGPR copy)
   const bool writes_new =
-      new_slot >= 0 && ((new_slot / 64) % nw) / kWaves == split;
+      __builtin_amdgcn_readfirstlane((int)(new_slot >= 0 && j == 0)) != 0;
   if (writes_new && threadIdx.x < 2 * NC) {
+    const int tn = new_slot / 64;
+    const int pg = pto >= 0 ? a.page_table[pto + tn / (kPageTokens / 64)] : 0;
     const size_t src = (size_t)it.kv_row[item] * D;
     if (threadIdx.x < NC) {
       const int g = threadIdx.x;
-      store_chunk<F>(
-          kbase + (((size_t)((new_slot - r0) / 64) * NC + g) * 64 + new_slot % 64) * LB,
-          encode8<F>(*reinterpret_cast<const uint4 *>(a.k_new + src + g * 8),
-                     it.k_scale[item]));
+      store_chunk<F>(k_tile(tn, pg) + ((size_t)g * 64 + new_slot % 64) * LB,
+                     encode8<F>(*reinterpret_cast<const uint4 *>(a.k_new + src + g * 8),
+                                it.k_scale[item]));
     } else {
       const int g = threadIdx.x - NC;
-      store_chunk<F>(vbase + (size_t)(new_slot - r0) * D * EB + g * LB,
+      store_chunk<F>(v_tile(tn, pg) + (size_t)(new_slot % 64) * D * EB + g * LB,
                      encode8<F>(*reinterpret_cast<const uint4 *>(a.v_new + src + g * 8),
                                 it.v_scale[item]));
     }
   }
 
-  float m[G], l[G], acc[G][8];
+  // The softmax of head h is run by wave h % 4 (its owner), which keeps the
+  // head's running shift m and lane sums l; every wave keeps acc over its
+  // own rows for every head and rescales it with the owner's factor.
+  constexpr int OWN = (G + kWaves - 1) / kWaves;   // heads a wave owns, at most
+  float m[OWN], l[OWN], acc[G][8];
 #pragma unroll
-  for (int h = 0; h < G; ++h) {
-    m[h] = -INFINITY;
-    l[h] = 0.f;
+  for (int o = 0; o < OWN; ++o) {
+    m[o] = -INFINITY;
+    l[o] = 0.f;
+  }
+#pragma unroll
+  for (int h = 0; h < G; ++h)
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
-  }
-  float *pl = sm.p[wave];
   // Only this workgroup reads the new slot in this launch: a workgroup-scope
   // release/acquire around the barrier orders the store before its loads
   // (agent scope would write back and invalidate the whole L2).
@@ -350,84 +418,97 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
   __syncthreads();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 
-  // K: every tile up to the last occupied one; V: rows [0, nv) only
-  const __amdgpu_buffer_rsrc_t krs =
-      make_rsrc(kbase, (uint32_t)(((rows + 63) / 64) * 64 * D * EB));
-  const __amdgpu_buffer_rsrc_t vrs = make_rsrc(vbase, (uint32_t)(rows * D * EB));
   // logit scale (base 2), with the fp8 K scale folded in
   const float zscale =
       F == HWKV_KV_FP8_E4M3 ? a.scale_log2 * it.k_scale[item] : a.scale_log2;
+  // per-lane parts of the piece addresses (the step is in soffset)
+  const int kl = lane * LB;                    // K: lane = slot
+  const int vl = rsub * D * EB + c8 * LB;      // V: row rsub of the step, 8 channels
+  // piece q of a tile: K chunk 4q + w, or V step 4(q - NCW) + w.  Both are
+  // 64 LB bytes long (a K chunk of 64 slots; RPS rows of D elements), so the
+  // offset of piece q is (4 (q mod NCW) + w) 64 LB: the wave's part is in
+  // wso (an SGPR), the step's part an immediate added to it.
+  static_assert(RPS * D * EB == 64 * LB, "K chunks and V steps are equally long");
+  const int wso = wave * 64 * LB;
+  auto ld = [&](__amdgpu_buffer_rsrc_t kr, __amdgpu_buffer_rsrc_t vr, auto qc) -> Chunk {
+    constexpr int q = decltype(qc)::value;
+    constexpr int step = kWaves * (q % NCW) * 64 * LB;
+    int so = wso;
+    asm volatile("" : "+s"(so));   // one SGPR add per load, not one SGPR per piece
+    if constexpr (q < NCW)
+      return bload_chunk<F>(kr, kl, so + step);
+    else
+      return bload_chunk<F>(vr, vl, so + step);
+  };
+  // q chunk c of head h is qw[h NC + c - wave] (the wave's chunks are
+  // c = 4i + wave)
+  const cu32x4_t *const qw = (const cu32x4_t *)(a.q + (size_t)it.q_row[item] * D) + wave;
+  float *const pl = sm.u.t.p;
 
-  // Each tile is a stream of 2 NC chunk loads per lane: NC K chunks (one
-  // lane per slot), then NC steps of V rows (lanes own channel slices).  It
-  // is consumed with PF loads always in flight: the V loads of a tile are on
-  // their way while its last K chunks and the softmax are computed, and the
-  // first K loads of the wave's next tile while its last V rows are.
-  //
-  // The wave walks its tile's K chunks, and its V rows, from a tile-dependent
-  // starting step and wraps round (the q chunks and the weights follow).
-  // Every wave starts at the same moment; without the rotation all of them
-  // would read the same offset of tiles a whole tile apart at each step,
-  // which crowds their requests onto a few HBM channels.  The V steps keep
-  // the fp8 token pairs (steps 2s, 2s + 1) together.
-  auto rot_k = [](int tile) { return (HWKV_DECODE_ROT * tile) & (NC - 1); };
-  auto rot_v = [](int tile) { return (HWKV_DECODE_ROT * tile) & (NC - 1) & (PAIR ? ~1 : ~0); };
+  int t = j;                     // logical tile
+  int tp = phys(t);              // its place in the unit
+  int pg = page_of(tp);
+  __amdgpu_buffer_rsrc_t krs = k_rsrc(tp, pg), vrs = v_rsrc(tp, pg);
   Chunk buf[PF];
-  int t = wl;
-  int rk = rot_k(t), rv = rot_v(t);
-  int kofs = (t * 64 - r0) * D * EB + lane * LB;
-  if (t < n_tiles) static_for<PF>([&](auto jc) {
-    buf[jc.value] = bload_chunk<F>(krs, kofs, ((jc.value + rk) & (NC - 1)) * 64 * LB);
-  });
-  for (int k = 0; k < kTilesPerWave && t < n_tiles; ++k) {
-    const int slot0 = t * 64;
-    const int slot = slot0 + lane;
-    const int tn = t + nw;
-    const bool has_next = k + 1 < kTilesPerWave && tn < n_tiles;
-    int rk_n = rot_k(tn);
-    int vofs = (slot0 - r0 + rsub) * D * EB + c8 * LB;
-    int kofs_n = (tn * 64 - r0) * D * EB + lane * LB;
-    uint64_t qaddr = (uint64_t)qc;
-    // load j of this tile's stream: K chunk (j + rk) mod NC, or V step
-    // (j - NC + rv) mod NC; V's descriptor ends at row n_valid, so the
-    // rows past it read as zero
-    auto ld = [&](auto jc) -> Chunk {
-      constexpr int j = decltype(jc)::value;
-      if constexpr (j < NC)   // K: the chunk step is uniform
-        return bload_chunk<F>(krs, kofs, ((j + rk) & (NC - 1)) * 64 * LB);
-      else
-        return bload_chunk<F>(vrs, vofs + ((j - NC + rv) & (NC - 1)) * RPS * D * EB);
+  static_for<PF>([&](auto jc) { buf[jc.value] = ld(krs, vrs, jc); });
+  for (int k = 0;; ++k) {
+    const bool has_next = t + nwg < n_tiles;
+    // the next tile and its page: its first PF loads are issued during the
+    // last PF pieces of this tile, with descriptors built at those loads
+    // (so that they are not live, beside q, through the whole tile)
+    const int tn = has_next ? t + nwg : -1;
+    const int tnp = has_next ? phys(tn) : 0;
+    const int pgn = has_next ? page_of(tnp) : 0;
+    // after consuming piece q, issue the load PF pieces later in the stream
+    auto issue = [&](auto qc) {
+      constexpr int q = decltype(qc)::value;
+      constexpr int qn = q + PF;
+      if constexpr (qn < PIECES) {
+        buf[q % PF] = ld(krs, vrs, std::integral_constant<int, qn>{});
+      } else {
+        int tt = tnp;
+        asm volatile("" : "+s"(tt));   // descriptors built here, not kept live
+        buf[q % PF] = ld(k_rsrc(tt, pgn, has_next), v_rsrc(tt, pgn, has_next),
+                         std::integral_constant<int, qn - PIECES>{});
+      }
     };
+    uint64_t qaddr = (uint64_t)qw;
     float s[G];
 #pragma unroll
     for (int h = 0; h < G; ++h) s[h] = 0.f;
 
-    // ---- q.k, one K chunk per step.  The empty asm statements make the
-    // accumulators, the offsets and the q address opaque at each step
-    // boundary, so that every step issues its own loads (one load PF steps
-    // ahead, the step's q chunk) and does its own arithmetic, instead of the
-    // compiler hoisting the loads of the whole tile and spilling.
-    // q chunks are read one step ahead of their use (qc: this step's chunk,
-    // qn: the next one), so the scalar-load latency overlaps a step of work.
+    // ---- partial q.k over the wave's chunks.  The empty asm statements make
+    // the accumulators and the q address opaque at each step boundary, so
+    // that every step issues its own loads and does its own arithmetic,
+    // instead of the compiler hoisting a tile's loads and spilling.  q chunks
+    // are read one step ahead of their use (scalar loads; q is uniform).
+    // (8 q heads, or binary16 keys, whose q is widened to fp32 SGPRs: no
+    // double buffer, its SGPRs do not fit beside the rest)
+#ifndef HWKV_DECODE_QAHEAD
+#define HWKV_DECODE_QAHEAD 0
+#endif
+    constexpr bool QAHEAD = HWKV_DECODE_QAHEAD && G < 8 && F != HWKV_KV_F16;
     u32x4_t qc[G];
-    {
-      const cu32x4_t *q0 = (const cu32x4_t *)qaddr;
+    if constexpr (QAHEAD) {
 #pragma unroll
-      for (int h = 0; h < G; ++h) qc[h] = q0[h * NC + rk];
+      for (int h = 0; h < G; ++h) qc[h] = qw[h * NC];
     }
-    static_for<NC>([&](auto jc) {
-      constexpr int j = decltype(jc)::value;
+    static_for<NCW>([&](auto jc) {
+      constexpr int q = decltype(jc)::value;
 #pragma unroll
       for (int h = 0; h < G; ++h) asm volatile("" : "+v"(s[h]));
-      asm volatile("" : "+v"(kofs), "+v"(vofs), "+s"(qaddr), "+s"(rk), "+s"(rv));
-      const Chunk x = buf[j % PF];
-      buf[j % PF] = ld(std::integral_constant<int, j + PF>{});
-      u32x4_t qn[G];
-      if constexpr (j + 1 < NC) {
-        const cu32x4_t *qj = (const cu32x4_t *)qaddr;
-        const int qi = (j + 1 + rk) & (NC - 1);
+      asm volatile("" : "+s"(qaddr));
+      const Chunk x = buf[q % PF];
+      issue(jc);
+      const cu32x4_t *qj = (const cu32x4_t *)qaddr;
+      if constexpr (!QAHEAD) {
 #pragma unroll
-        for (int h = 0; h < G; ++h) qn[h] = qj[h * NC + qi];
+        for (int h = 0; h < G; ++h) qc[h] = qj[h * NC + kWaves * q];
+      }
+      u32x4_t qn[G];
+      if constexpr (QAHEAD && q + 1 < NCW) {
+#pragma unroll
+        for (int h = 0; h < G; ++h) qn[h] = qj[h * NC + kWaves * (q + 1)];
       }
       if constexpr (F == HWKV_KV_BF16) {
 #pragma unroll
@@ -462,73 +543,84 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
           s[h] = fmaf(bf_hi(qc[h].w), kf[7], s[h]);
         }
       }
-      if constexpr (j + 1 < NC) {
+      if constexpr (QAHEAD && q + 1 < NCW) {
 #pragma unroll
         for (int h = 0; h < G; ++h) qc[h] = qn[h];
       }
     });
 
-    // ---- online softmax, base 2 (the first V loads are already in flight)
-    const bool valid = slot < nv;
-    // token-pair order of the binary16 weights: token t is half (t / RPS) % 2
-    // of pair (t / 2 RPS) RPS + t % RPS, whose G weights are G dwords
-    const int ppid = (lane / (2 * RPS)) * RPS + lane % RPS;
-    const int phalf = (lane / RPS) & 1;
+    // ---- the four partial logits of each slot meet in LDS (buffers
+    // alternate with the tile, so one barrier per tile suffices for them: a
+    // wave can only reach this tile's buffer again after every wave has
+    // passed the next tile's barrier, i.e. after every owner has read it)
+#pragma unroll
+    for (int h = 0; h < G; ++h) sm.u.t.lg[k & 1][h][wave][lane] = s[h];
+    __syncthreads();
+
+    // ---- online softmax, base 2, of the heads this wave owns
+    const bool valid = 64 * tp + lane < nv;
+    // fp8: the binary16 weights go in pair order: slot t is row t % RPS of
+    // V step st = t / RPS, which is step i = st / 4 of wave st % 4 -- half
+    // i % 2 of that wave's pair i / 2
+    const int st = lane / RPS;
+    const int ppid = ((st % kWaves) * (NCW / 2) + st / (2 * kWaves)) * RPS + lane % RPS;
+    const int phalf = (st / kWaves) & 1;
+#pragma unroll
+    for (int o = 0; o < OWN; ++o) {
+      const int h = wave + kWaves * o;
+      if (h < G) {  // uniform
+        float z = 0.f;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) z += sm.u.t.lg[k & 1][h][w][lane];  // fixed order
+        z = valid ? z * zscale : -INFINITY;
+        const float mnew = fmaxf(m[o], wave_max(z));
+        float alpha = 1.0f;
+        if (mnew > m[o]) {  // uniform
+          alpha = exp2f(m[o] - mnew);
+          l[o] *= alpha;
+          m[o] = mnew;
+        }
+        const float p = exp2f(z - mnew);
+        l[o] += p;
+        if constexpr (PAIR)
+          reinterpret_cast<_Float16 *>(pl)[2 * (ppid * G + h) + phalf] = (_Float16)p;
+        else
+          pl[lane * PST + h] = p;
+        if (lane == 0) sm.alpha[h] = alpha;
+      }
+    }
+    __syncthreads();
+    // every wave rescales its sums of the heads whose shift moved
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-      const float z = valid ? s[h] * zscale : -INFINITY;
-      const float mnew = fmaxf(m[h], wave_max(z));
-      if (mnew > m[h]) {  // uniform
-        const float alpha = exp2f(m[h] - mnew);
-        l[h] *= alpha;
+      const float alpha = __builtin_bit_cast(
+          float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, sm.alpha[h])));
+      if (alpha != 1.0f) {  // uniform
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc[h][e] *= alpha;
-        m[h] = mnew;
       }
-      const float p = exp2f(z - mnew);
-      l[h] += p;
-      if constexpr (PAIR)
-        reinterpret_cast<_Float16 *>(pl)[2 * (ppid * G + h) + phalf] = (_Float16)p;
-      else
-        pl[lane * PST + h] = p;
     }
 
-    // ---- p.v, one step of RPS rows per step; lanes own channels 8 c8 ..
-    auto issue = [&](auto jc) {  // the load PF steps after step j
-      constexpr int j = decltype(jc)::value;
-      constexpr int jn = j + PF;
-      if constexpr (jn < 2 * NC) {
-        buf[j % PF] = ld(std::integral_constant<int, jn>{});
-      } else {
-        if (has_next)
-          buf[j % PF] = bload_chunk<F>(krs, kofs_n, ((jn - 2 * NC + rk_n) & (NC - 1)) * 64 * LB);
-      }
-    };
+    // ---- p.v over the wave's V steps (rows (4i + w) RPS + rsub)
     if constexpr (PAIR) {
-      // steps 2s and 2s + 1 read rows r = rsub + 2s RPS and r + RPS: the
-      // first step keeps its chunk and reads the pair's weights (so the LDS
-      // latency overlaps a step), the second builds the binary16 pairs
-      // (v_r[c], v_r+RPS[c]) and takes one v_dot2 per (head, channel)
       const uint32_t *pp = reinterpret_cast<const uint32_t *>(pl);
-      int pofs = rsub * G;
       uint32_t pw[G];
       Chunk xp;
-      static_for<NC>([&](auto jc) {
-        constexpr int js = decltype(jc)::value;
-        constexpr int j = NC + js;
+      static_for<NCW>([&](auto jc) {
+        constexpr int i = decltype(jc)::value;
+        constexpr int q = NCW + i;
 #pragma unroll
         for (int h = 0; h < G; ++h)
 #pragma unroll
           for (int e = 0; e < 8; e += 2)
             asm volatile("" : "+v"(acc[h][e]), "+v"(acc[h][e + 1]));
-        asm volatile("" : "+v"(vofs), "+v"(kofs_n), "+v"(pofs), "+s"(rv), "+s"(rk_n));
-        const Chunk x = buf[j % PF];
-        issue(std::integral_constant<int, j>{});
-        if constexpr (js % 2 == 0) {
+        const Chunk x = buf[q % PF];
+        issue(std::integral_constant<int, q>{});
+        if constexpr (i % 2 == 0) {
           xp = x;
-          const int pi = ((js + rv) & (NC - 1)) / 2;   // the step pair's weights
 #pragma unroll
-          for (int h = 0; h < G; ++h) pw[h] = pp[pofs + pi * RPS * G + h];
+          for (int h = 0; h < G; ++h)
+            pw[h] = pp[((wave * (NCW / 2) + i / 2) * RPS + rsub) * G + h];
         } else {
           const uint32_t w0 = __builtin_amdgcn_perm(x.x, xp.x, 0x05010400u);
           const uint32_t w1 = __builtin_amdgcn_perm(x.x, xp.x, 0x07030602u);
@@ -548,54 +640,67 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
         }
       });
     } else {
-    // p of a step's rows is read from LDS one step ahead (pc: this step,
-    // pn: the next), so the LDS latency overlaps a step of work.
-    int pofs = rsub * PST;
-    float pc[G];
+      // p of a step's row is read from LDS one step ahead (pc: this step,
+      // pn: the next), so the LDS latency overlaps a step of work
+      float pc[G];
 #pragma unroll
-    for (int h = 0; h < G; ++h) pc[h] = pl[pofs + (rv & (NC - 1)) * RPS * PST + h];
-    static_for<NC>([&](auto jc) {
-      constexpr int js = decltype(jc)::value;
-      constexpr int j = NC + js;
+      for (int h = 0; h < G; ++h) pc[h] = pl[(wave * RPS + rsub) * PST + h];
+      static_for<NCW>([&](auto jc) {
+        constexpr int i = decltype(jc)::value;
+        constexpr int q = NCW + i;
 #pragma unroll
-      for (int h = 0; h < G; ++h)
+        for (int h = 0; h < G; ++h)
 #pragma unroll
-        for (int e = 0; e < 8; e += 2)
-          asm volatile("" : "+v"(acc[h][e]), "+v"(acc[h][e + 1]));
-      asm volatile("" : "+v"(vofs), "+v"(kofs_n), "+v"(pofs), "+s"(rv), "+s"(rk_n));
-      const Chunk x = buf[j % PF];
-      issue(std::integral_constant<int, j>{});
-      float pn[G];
-      if constexpr (js + 1 < NC) {
-        const int pi = (js + 1 + rv) & (NC - 1);
+          for (int e = 0; e < 8; e += 2)
+            asm volatile("" : "+v"(acc[h][e]), "+v"(acc[h][e + 1]));
+        const Chunk x = buf[q % PF];
+        issue(std::integral_constant<int, q>{});
+        float pn[G];
+        if constexpr (i + 1 < NCW) {
 #pragma unroll
-        for (int h = 0; h < G; ++h) pn[h] = pl[pofs + pi * RPS * PST + h];
-      }
-      float vf[8];
-      widen8<F>(x, vf);
+          for (int h = 0; h < G; ++h)
+            pn[h] = pl[((kWaves * (i + 1) + wave) * RPS + rsub) * PST + h];
+        }
+        float vf[8];
+        widen8<F>(x, vf);
 #pragma unroll
-      for (int h = 0; h < G; ++h)
+        for (int h = 0; h < G; ++h)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pc[h], vf[e], acc[h][e]);
-      if constexpr (js + 1 < NC) {
+          for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pc[h], vf[e], acc[h][e]);
+        if constexpr (i + 1 < NCW) {
 #pragma unroll
-        for (int h = 0; h < G; ++h) pc[h] = pn[h];
-      }
-    });
+          for (int h = 0; h < G; ++h) pc[h] = pn[h];
+        }
+      });
     }
+    if (!has_next) break;
     t = tn;
-    kofs = kofs_n;
-    rk = rk_n;
-    rv = rot_v(tn);
+    tp = tnp;
+    pg = pgn;
+    krs = k_rsrc(tp, pg);
+    vrs = v_rsrc(tp, pg);
   }
 
-  // ---- wave partials: l over all lanes; acc over the lanes that share a
-  // channel chunk (lane, lane ^ NC, ..., lane ^ 32).  The last step pairs
-  // channel e with e + 4 in one lane swap, so lanes 0..31 end with channels
-  // 0..3 and lanes 32..63 with channels 4..7 of their chunk.
+  // ---- the workgroup's partial.  Each head's owner gives its shift m and
+  // normaliser l (the lane sums added up); every wave applied the owners'
+  // rescale factors to its sums, so acc, which holds each wave's own rows,
+  // is summed as it is: over the lanes that share a channel chunk (lane,
+  // lane ^ NC, ..., lane ^ 32 -- the last step pairs channel e with e + 4 in
+  // one lane swap, so lanes 0..31 end with channels 0..3 and lanes 32..63
+  // with channels 4..7 of their chunk), then over the waves in LDS.
+#pragma unroll
+  for (int o = 0; o < OWN; ++o) {
+    const int h = wave + kWaves * o;
+    if (h < G) {  // uniform
+      const float lh = wave_sum(l[o]);
+      if (lane == 0) {
+        sm.m[h] = m[o];
+        sm.l[h] = lh;
+      }
+    }
+  }
 #pragma unroll
   for (int h = 0; h < G; ++h) {
-    l[h] = wave_sum(l[h]);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
 #pragma unroll
@@ -609,41 +714,27 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
   for (int h = 0; h < G; ++h)
 #pragma unroll
     for (int e = 0; e < 4; ++e) red[h][e] = half_sum_pair(acc[h][e], acc[h][e + 4]);
+  __syncthreads();  // every wave is done with the tile buffers that acc reuses
   if ((lane & 31) < NC) {
 #pragma unroll
     for (int h = 0; h < G; ++h)
-      *reinterpret_cast<float4 *>(&sm.acc[wave][h][c8 * 8 + 4 * half]) =
+      *reinterpret_cast<float4 *>(&sm.u.acc[wave][h][c8 * 8 + 4 * half]) =
           make_float4(red[h][0], red[h][1], red[h][2], red[h][3]);
-  }
-  if (lane == 0) {
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      sm.m[wave][h] = m[h];
-      sm.l[wave][h] = l[h];
-    }
   }
   __syncthreads();
 
-  // ---- merge the waves (wave 0 of every split has at least one tile), 4
-  // channels per thread and step
-  float *part = a.ws + (size_t)(it.ws_split0 + blk) * (G * (D + 2));
+  const int pidx = it.ws_split0 + blk;   // this workgroup's partial
   const float vsc = F == HWKV_KV_FP8_E4M3 ? it.v_scale[item] : 1.0f;
   for (int idx = threadIdx.x; idx < G * D / 4; idx += kWaves * 64) {
     const int h = idx / (D / 4), c = (idx % (D / 4)) * 4;
-    float M = sm.m[0][h];
-#pragma unroll
-    for (int w = 1; w < kWaves; ++w) M = fmaxf(M, sm.m[w][h]);
-    float L = 0.f;
     float4 A = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) {
-      const float f = exp2f(sm.m[w][h] - M);
-      L += sm.l[w][h] * f;
-      const float4 x = *reinterpret_cast<const float4 *>(&sm.acc[w][h][c]);
-      A.x += x.x * f;
-      A.y += x.y * f;
-      A.z += x.z * f;
-      A.w += x.w * f;
+      const float4 x = *reinterpret_cast<const float4 *>(&sm.u.acc[w][h][c]);
+      A.x += x.x;
+      A.y += x.y;
+      A.z += x.z;
+      A.w += x.w;
     }
     if constexpr (F == HWKV_KV_FP8_E4M3) {  // the V scale of the codes
       A.x *= vsc;
@@ -651,24 +742,16 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
       A.z *= vsc;
       A.w *= vsc;
     }
-    if (nsplit == 1) {
+    const float L = sm.l[h];
+    if (nwg == 1) {
       const float inv = 1.0f / L;
       *reinterpret_cast<float4 *>(&a.out[((size_t)it.q_row[item] + h) * D + c]) =
           make_float4(A.x * inv, A.y * inv, A.z * inv, A.w * inv);
     } else {
-      float *dst = &part[2 * G + h * D + c];
-      if constexpr ((2 * G) % 4 == 0) {     // partial records 16-byte aligned
-        *reinterpret_cast<float4 *>(dst) = A;
-      } else {
-        dst[0] = A.x;
-        dst[1] = A.y;
-        dst[2] = A.z;
-        dst[3] = A.w;
-      }
-      if (c == 0) {
-        part[h] = M;
-        part[G + h] = L;
-      }
+      *reinterpret_cast<float4 *>(&a.part_acc[((size_t)pidx * G + h) * D + c]) = A;
+      if (c == 0)
+        *reinterpret_cast<float2 *>(&a.part_ml[((size_t)pidx * G + h) * 2]) =
+            make_float2(sm.m[h], L);
     }
   }
 }
@@ -679,18 +762,8 @@ constexpr int kSplitDepth = KvFormat<F>::kBytes == 2 ? kPrefetch : kPrefetch8;
 
 template <int D, int G, int F>
 __global__ __launch_bounds__(kWaves * 64)
-__attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split(DecodeArgs a) {
+__attribute__((amdgpu_waves_per_eu(split_waves_per_eu(D, G, F)))) void decode_split(DecodeArgs a) {
   split_body<D, G, F, kSplitDepth<F>>(a);
-}
-
-// For launches with fewer split workgroups than CUs: the chip is not full,
-// so each wave keeps twice as many loads in flight.  (With the chip full the
-// default depth is faster: the arithmetic between loads is what the other
-// resident waves hide.)
-template <int D, int G, int F>
-__global__ __launch_bounds__(kWaves * 64)
-__attribute__((amdgpu_waves_per_eu(kMinWavesPerEU))) void decode_split_deep(DecodeArgs a) {
-  split_body<D, G, F, 2 * kSplitDepth<F>>(a);
 }
 
 // Compute units of the current device (cached per device).
@@ -735,14 +808,6 @@ struct SplitLaunch {
   struct At {
     static hipError_t run(const DecodeArgs &a, int n, hipStream_t s, hipEvent_t e0,
                           hipEvent_t e1) {
-      // (8 q heads per kv head: the deeper ring does not fit the registers)
-      if constexpr (G < 8) {
-        if (n < device_cus()) {
-          hipExtLaunchKernelGGL((decode_split_deep<D, G, F>), dim3(n), dim3(kWaves * 64), 0,
-                                s, e0, e1, 0, a);
-          return hipGetLastError();
-        }
-      }
       hipExtLaunchKernelGGL((decode_split<D, G, F>), dim3(n), dim3(kWaves * 64), 0,
                             s, e0, e1, 0, a);
       return hipGetLastError();

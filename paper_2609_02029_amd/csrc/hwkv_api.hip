@@ -227,10 +227,18 @@ int alloc_impl(hwkv_cache **out, const hwkv_policy *p, int32_t batch, int64_t ma
 
 int64_t group_size(const hwkv_policy &p) { return p.n_q_heads / p.n_kv_heads; }
 
-// Splits needed by one (unit, seq) item with n_valid rows.
-int64_t splits_for(int64_t n_valid) {
-  const int64_t t = hwkv::decode_split_tokens();
-  return (n_valid + t - 1) / t;
+// 64-slot tiles of an item with n_valid rows.
+int64_t tiles_for(int64_t n_valid) { return (n_valid + hwkv::kTile - 1) / hwkv::kTile; }
+
+// Decode split workgroups of the items of one launch, given their tile
+// counts: T = max(1, ceil(total tiles / target)) tiles per workgroup, and an
+// item of n tiles gets ceil(n / T) workgroups.  The launch then has at most
+// target + (number of items) workgroups, and never more than it has tiles.
+void plan_workgroups(const int64_t *tiles, int cnt, int64_t target, int32_t *nwg) {
+  int64_t total = 0;
+  for (int j = 0; j < cnt; ++j) total += tiles[j];
+  const int64_t T = std::max<int64_t>(1, (total + target - 1) / target);
+  for (int j = 0; j < cnt; ++j) nwg[j] = (int32_t)((tiles[j] + T - 1) / T);
 }
 
 size_t partial_bytes(const hwkv_policy &p) {
@@ -494,8 +502,8 @@ int decode_impl(hwkv_cache *c, int32_t layer, const void *k_new,
   const int G = (int)group_size(p);
   // item lengths
   const int n_items_total = B * H;
-  std::vector<int32_t> nv(n_items_total), ns(n_items_total), nslot(n_items_total);
-  int64_t total_splits = 0;
+  std::vector<int32_t> nv(n_items_total), nwg(n_items_total), nslot(n_items_total);
+  std::vector<int64_t> tiles(n_items_total);
   for (int32_t b = 0; b < B; ++b) {
     const int64_t n = seq_len(c, layer, b);
     for (int32_t h = 0; h < H; ++h) {
@@ -512,10 +520,17 @@ int decode_impl(hwkv_cache *c, int32_t layer, const void *k_new,
       }
       const int i = b * H + h;
       nv[i] = (int32_t)std::min(len, c->cap[u]);
-      ns[i] = (int32_t)splits_for(nv[i]);
+      tiles[i] = tiles_for(nv[i]);
       nslot[i] = s_new;
-      total_splits += ns[i];
     }
+  }
+  // split workgroups per item, per launch of at most kMaxItems items
+  const int64_t target = hwkv::decode_workgroup_target(c->fmt, p.head_dim, G);
+  int64_t total_splits = 0;
+  for (int i0 = 0; i0 < n_items_total; i0 += hwkv::kMaxItems) {
+    const int cnt = std::min(hwkv::kMaxItems, n_items_total - i0);
+    plan_workgroups(&tiles[i0], cnt, target, &nwg[i0]);
+    for (int j = 0; j < cnt; ++j) total_splits += nwg[i0 + j];
   }
   const size_t need = (size_t)total_splits * partial_bytes(p);
   if (!ws || ws_bytes < need)
@@ -550,7 +565,7 @@ int decode_impl(hwkv_cache *c, int32_t layer, const void *k_new,
       a.it.v_scale[j] = c->v_scale[u];
       a.it.pto[j] = page_tab_off(c, u, b);
       a.it.split_begin[j] = splits;
-      splits += ns[i];
+      splits += nwg[i];
     }
     a.it.split_begin[cnt] = splits;
     a.it.n_items = cnt;
@@ -562,7 +577,9 @@ int decode_impl(hwkv_cache *c, int32_t layer, const void *k_new,
     a.k_new = static_cast<const uint16_t *>(k_new);
     a.v_new = static_cast<const uint16_t *>(v_new);
     a.out = static_cast<float *>(out);
-    a.ws = static_cast<float *>(ws);
+    // the call's partials: acc rows of all its launches, then their (m, l)
+    a.part_acc = static_cast<float *>(ws);
+    a.part_ml = static_cast<float *>(ws) + (size_t)total_splits * G * p.head_dim;
     a.scale_log2 = scale * 1.4426950408889634f;
     const int n_combine =
         cnt * hwkv::decode_combine_blocks_per_item(p.head_dim, G);
@@ -772,13 +789,23 @@ int alloc_impl(hwkv_cache **out, const hwkv_policy *p, int32_t batch, int64_t ma
     }
     c->bytes = bytes;
     c->n.assign((size_t)p->n_layers * batch, 0);
-    // workspace: worst layer at full capacity
+    // workspace: the most partials any call on a layer can take.  A launch
+    // of cnt items has at most min(target + cnt, its tiles at capacity)
+    // workgroups (plan_workgroups), whatever the lengths.
     size_t ws = 0;
+    const int64_t target = hwkv::decode_workgroup_target(
+        kv_format, p->head_dim, (int)(p->n_q_heads / p->n_kv_heads));
+    const int64_t n_items = (int64_t)batch * p->n_kv_heads;
     for (int32_t l = 0; l < p->n_layers; ++l) {
-      int64_t sp = 0;
-      for (int32_t h = 0; h < p->n_kv_heads; ++h)
-        sp += splits_for(c->cap[l * p->n_kv_heads + h]);
-      ws = std::max(ws, (size_t)(sp * batch) * partial_bytes(*p));
+      int64_t parts = 0;
+      for (int64_t i0 = 0; i0 < n_items; i0 += hwkv::kMaxItems) {
+        const int64_t cnt = std::min<int64_t>(hwkv::kMaxItems, n_items - i0);
+        int64_t tiles = 0;
+        for (int64_t i = i0; i < i0 + cnt; ++i)
+          tiles += tiles_for(c->cap[l * p->n_kv_heads + i % p->n_kv_heads]);
+        parts += std::min(target + cnt, tiles);
+      }
+      ws = std::max(ws, (size_t)parts * partial_bytes(*p));
     }
     c->ws_bytes = ws;
     if (dev_buf) {

@@ -19,8 +19,7 @@
 // ([4 tiles][head_dim / 8][64][8]), then its V rows ([256][head_dim]) -- in
 // a pool after the finite units' regions; page j of (unit, sequence) is
 // page_table[pto + j], where pto = (full unit index * batch + sequence) *
-// pages per max_ctx.  One page is one decode split and holds whole prefill
-// key tiles.
+// pages per max_ctx.  A page holds whole decode and prefill key tiles.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -32,10 +31,19 @@ namespace hwkv {
 constexpr int kTile = 64;        // token slots per K tile (= wavefront width)
 constexpr int kMaxItems = 64;    // (sequence, kv-head) items per launch
 constexpr int kPageTokens = 256; // rows per page of a paged full unit
+constexpr int kDecodeWaves = 4;  // waves of a decode split workgroup
+#ifndef HWKV_DECODE_WG_PER_CU_X4
+#define HWKV_DECODE_WG_PER_CU_X4 8
+#endif
+// Decode split workgroups a launch aims at, in quarters per CU: the host
+// picks the tiles per workgroup so that the launch has about this many
+// workgroups (at most as many as the kernel's register budget holds at once).
+constexpr int kDecodeWgPerCuX4 = HWKV_DECODE_WG_PER_CU_X4;
 
 // Decode work of one launch: items are (sequence b, kv head h) pairs of one
-// layer; item i owns splits [split_begin[i], split_begin[i + 1]) of the
-// launch and rows [0, n_valid[i]) of its unit.
+// layer; item i owns rows [0, n_valid[i]) of its unit and the launch's split
+// workgroups [split_begin[i], split_begin[i + 1]); workgroup j of the item's
+// nwg walks the item's 64-slot tiles j, j + nwg, ...
 struct DecodeItems {
   int64_t k_off[kMaxItems];      // element offset of the item's K tiles
   int64_t v_off[kMaxItems];      // element offset of the item's V rows
@@ -48,7 +56,8 @@ struct DecodeItems {
   int32_t pto[kMaxItems];        // page-table offset of a paged unit, or -1
   int32_t split_begin[kMaxItems + 1];
   int32_t n_items;
-  int32_t ws_split0;             // first partial slot of this launch in ws
+  int32_t ws_split0;             // first partial of this launch in the call's
+                                 // partial arrays
 };
 
 struct DecodeArgs {
@@ -58,7 +67,8 @@ struct DecodeArgs {
   const uint16_t *k_new;         // [B][Hkv][D] or null
   const uint16_t *v_new;
   float *out;                    // [B][Hq][D]
-  float *ws;                     // partials [split][G][2 + D]
+  float *part_acc;               // partials: acc [partial][G][D]
+  float *part_ml;                //   and (m, l) [partial][G][2]
   const int32_t *page_table;     // paged caches (else null)
   int64_t pool_off;              // element offset of page 0
   float scale_log2;              // scale * log2(e)
@@ -165,7 +175,8 @@ hipError_t launch_decode_split_fmt(int D, int G, const DecodeArgs &a,
 hipError_t launch_decode_combine(int D, int G, const DecodeArgs &a,
                                  int n_combine_blocks, hipStream_t s,
                                  hipEvent_t e0 = nullptr, hipEvent_t e1 = nullptr);
-int decode_split_tokens();       // tokens per split (a multiple of 64)
+// split workgroups a launch aims at on the current device
+int decode_workgroup_target(int fmt, int D, int G);
 int decode_combine_blocks_per_item(int D, int G);  // merge workgroups
 hipError_t launch_prefill_write(int fmt, int D, const WriteArgs &a,
                                 int max_tiles, hipStream_t s);
