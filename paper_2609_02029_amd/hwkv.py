@@ -399,6 +399,14 @@ def append_decode_attn(cache, layer, k_new, v_new, q, scale, out, ws, stream=Non
         _stream(stream)))
 
 
+def append_decode_attn_ptr(cache, layer, k_new, v_new, q, scale, out, ws, ws_bytes, stream):
+    """``append_decode_attn`` on raw device addresses (ints) and a raw stream
+    handle: no Python-side checks (the library still validates what it can),
+    for callers that issue many calls on tensors they have already checked."""
+    _check(_lib.hwkv_append_decode_attn(cache.handle, layer, k_new, v_new, q, scale, out, ws,
+                                        ws_bytes, stream))
+
+
 def decode_timing(cache, enable):
     _check(_lib.hwkv_decode_timing(cache.handle, 1 if enable else 0))
 
