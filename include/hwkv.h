@@ -334,6 +334,23 @@ int hwkv_append_decode_attn(hwkv_cache *cache, int32_t layer,
                             const void *q, float scale, void *out, void *ws,
                             size_t ws_bytes, void *stream);
 
+/* hwkv_append_decode_attn for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): no workspace argument; the split partials go to a static
+ * device array of the library, 16 MiB per device, held until the process
+ * ends.  The call itself allocates nothing (no hipMalloc, hipFree or
+ * allocating library routine); its first call on a device looks up the
+ * array's device address.  Same arguments, kernels, errors and result as
+ * hwkv_append_decode_attn, plus EINVAL, with nothing changed, if the call
+ * would need more than the 16 MiB of partials (hwkv_decode_workspace_bytes
+ * bounds the need of any call on a cache).  Every call on a device shares
+ * that device's array: calls that overlap on one device (concurrent
+ * streams, several host threads) race on it and must not be issued. */
+int hwkv_append_decode_attn_noalloc(hwkv_cache *cache, int32_t layer,
+                                    const void *k_new, const void *v_new,
+                                    const void *q, float scale, void *out,
+                                    void *stream);
+
 /* ------------------------------------------------------------------------ */
 /* Calibration (Method, "Sequential Prefix-Conditioned Calibration";         */
 /* Appendix, "Calibration Score and Fixed-Prefix Selection" and             */

@@ -486,10 +486,45 @@ int prefill_attn_impl(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0,
              : HWKV_EDEVICE;
 }
 
-// Shared validation of a decode call; fills per-item lengths.
+// The split partials of hwkv_append_decode_attn_noalloc: a file-scope
+// device array (one copy per device, held until the process ends), so that
+// the call allocates nothing.  Host code never passes the array's name to a
+// kernel or a copy: in host code it stands for the array, not for its device
+// address, which scratch_ptr() takes once per device.
+constexpr size_t kScratchBytes = (size_t)16 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[64] = {};
+
+// The device address of `scratch` on the current device (looked up on the
+// first call on each device).
+int scratch_ptr(void **out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(HWKV_EDEVICE, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  if (dev < 0 || dev >= 64) return fail(HWKV_EDEVICE, "device index beyond 63");
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) {
+      (void)hipGetLastError();
+      return fail(HWKV_EDEVICE, std::string("hipGetSymbolAddress(scratch): ") +
+                                    hipGetErrorString(e));
+    }
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return HWKV_OK;
+}
+
+// Shared validation of a decode call; fills per-item lengths.  static_ws:
+// ws is the static scratch (an over-size call is refused with its limit).
 int decode_impl(hwkv_cache *c, int32_t layer, const void *k_new,
                 const void *v_new, const void *q, float scale, void *out,
-                void *ws, size_t ws_bytes, void *stream, bool fused) {
+                void *ws, size_t ws_bytes, void *stream, bool fused,
+                bool static_ws = false) {
   if (!c) return fail(HWKV_EINVAL, "cache is null");
   const hwkv_policy &p = c->pol;
   if (layer < 0 || layer >= p.n_layers)
@@ -533,6 +568,10 @@ int decode_impl(hwkv_cache *c, int32_t layer, const void *k_new,
     for (int j = 0; j < cnt; ++j) total_splits += nwg[i0 + j];
   }
   const size_t need = (size_t)total_splits * partial_bytes(p);
+  if (static_ws && need > ws_bytes)
+    return fail(HWKV_EINVAL, "the call needs " + std::to_string(need) +
+                                 " bytes of split partials, more than the " +
+                                 std::to_string(ws_bytes) + "-byte static scratch");
   if (!ws || ws_bytes < need)
     return fail(HWKV_EINVAL, "workspace missing or too small (need " +
                                  std::to_string(need) + " bytes)");
@@ -1672,6 +1711,18 @@ int hwkv_append_decode_attn(hwkv_cache *c, int32_t layer, const void *k_new,
                             void *stream) {
   return decode_impl(c, layer, k_new, v_new, q, scale, out, ws, ws_bytes,
                      stream, true);
+}
+
+int hwkv_append_decode_attn_noalloc(hwkv_cache *c, int32_t layer,
+                                    const void *k_new, const void *v_new,
+                                    const void *q, float scale, void *out,
+                                    void *stream) {
+  if (!c) return fail(HWKV_EINVAL, "cache is null");
+  void *ws = nullptr;
+  const int rc = scratch_ptr(&ws);
+  if (rc != HWKV_OK) return rc;
+  return decode_impl(c, layer, k_new, v_new, q, scale, out, ws, kScratchBytes, stream, true,
+                     true);
 }
 
 int hwkv_decode_timing(hwkv_cache *c, int32_t enable) {

@@ -66,6 +66,7 @@ SYMBOLS = {
     "hwkv_decode_workspace_bytes": ([_vp, _P(_sz)], ctypes.c_int),
     "hwkv_decode_attn": ([_vp, _i32, _vp, _flt, _vp, _vp, _sz, _vp], ctypes.c_int),
     "hwkv_append_decode_attn": ([_vp, _i32, _vp, _vp, _vp, _flt, _vp, _vp, _sz, _vp], ctypes.c_int),
+    "hwkv_append_decode_attn_noalloc": ([_vp, _i32, _vp, _vp, _vp, _flt, _vp, _vp], ctypes.c_int),
     "hwkv_cache_read_unit": ([_vp, _i32, _i32, _i32, _vp, _vp, _P(_i64)], ctypes.c_int),
     "hwkv_decode_timing": ([_vp, _i32], ctypes.c_int),
     "hwkv_decode_timing_read": ([_vp, _P(_dbl), _P(_dbl), _P(_i64)], ctypes.c_int),
@@ -397,6 +398,20 @@ def append_decode_attn(cache, layer, k_new, v_new, q, scale, out, ws, stream=Non
         cache.handle, layer, _dev(k_new, "bfloat16", "k_new"), _dev(v_new, "bfloat16", "v_new"),
         _dev(q, "bfloat16", "q"), float(scale), _dev(out, "float32", "out"), wp, wn,
         _stream(stream)))
+
+
+def append_decode_attn_noalloc(cache, layer, k_new, v_new, q, scale, out, stream=None):
+    """``append_decode_attn`` without a workspace: the split partials go to
+    the library's static scratch (``hwkv_append_decode_attn_noalloc``)."""
+    shp = (cache.batch, cache.n_kv_heads, cache.head_dim)
+    if tuple(k_new.shape) != shp or tuple(v_new.shape) != shp:
+        raise ValueError("k_new and v_new must be [batch, n_kv_heads, head_dim]")
+    qshp = (cache.batch, cache.n_q_heads, cache.head_dim)
+    if tuple(q.shape) != qshp or tuple(out.shape) != qshp:
+        raise ValueError("q and out must be [batch, n_q_heads, head_dim]")
+    _check(_lib.hwkv_append_decode_attn_noalloc(
+        cache.handle, layer, _dev(k_new, "bfloat16", "k_new"), _dev(v_new, "bfloat16", "v_new"),
+        _dev(q, "bfloat16", "q"), float(scale), _dev(out, "float32", "out"), _stream(stream)))
 
 
 def append_decode_attn_ptr(cache, layer, k_new, v_new, q, scale, out, ws, ws_bytes, stream):
