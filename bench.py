@@ -49,9 +49,14 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=60)
     ap.add_argument("--warmup", type=int, default=8)
-    ap.add_argument("--workload", default="ctx112k",
-                    choices=["ctx112k", "ctx32k", "batch16", "pr1", "prefill128k", "calib128k",
-                             "probe"])
+    ap.add_argument("--workload", default="suite",
+                    choices=["suite", "ctx112k", "ctx32k", "batch16", "pr1", "prefill128k",
+                             "calib128k", "probe"],
+                    help="suite (default): the 112K headline (--steps/--warmup) plus every "
+                         "other configuration in one line; or one workload alone")
+    ap.add_argument("--intervals", type=int, default=3,
+                    help="decode workloads: the timed steps are cut into this many consecutive "
+                         "intervals; us/step is their median")
     ap.add_argument("--kv-format", default="bf16", choices=["bf16", "f16", "fp8"],
                     help="cache format of the decode workloads (fp8: E4M3 with the "
                          "workload's per-unit scales)")
@@ -99,7 +104,7 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     if args.workload == "prefill128k":
-        prefill_main(args, dev)
+        print(json.dumps(prefill_run(args, dev)), flush=True)
         return
     if args.workload == "calib128k":
         calib_main(args, dev)
@@ -107,6 +112,21 @@ def main():
     if args.workload == "probe":
         probe_main(args, dev)
         return
+    if args.workload == "suite":
+        print(json.dumps(suite(args, dev)), flush=True)
+        return
+    print(json.dumps(decode_run(args, dev)), flush=True)
+
+
+def decode_run(args, dev, one_core=True):
+    """One decode workload (``args.workload``, ``kv_format``, ``paged``,
+    ``replicas``, ``steps``, ``warmup``, ...): the result dict of its line."""
+    import numpy as np
+    import torch
+
+    import workloads as W
+    from paper_2609_02029_amd import hwkv
+
     cfg = W.CONFIGS[args.workload]
     L, B = cfg["n_layers"], cfg["batch"]
     Hq, Hkv, D, S = cfg["n_q_heads"], cfg["n_kv_heads"], cfg["head_dim"], cfg["n_sinks"]
@@ -215,16 +235,21 @@ def main():
     torch.cuda.synchronize()
 
     # the timed region: K steps, bracketed by events on the stream the
-    # kernels are launched on (torch's current stream)
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # kernels are launched on (torch's current stream), cut into consecutive
+    # intervals by events between them; us/step is the median interval's
+    n_int = max(1, min(args.intervals, args.steps))
+    cuts = [args.steps * i // n_int for i in range(n_int + 1)]
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(n_int + 1)]
     torch.cuda.synchronize()
-    start.record()
-    for i in range(args.steps):
-        run_step(args.warmup + i)
-    end.record()
+    evs[0].record()
+    for k in range(n_int):
+        for i in range(cuts[k], cuts[k + 1]):
+            run_step(args.warmup + i)
+        evs[k + 1].record()
     torch.cuda.synchronize()
-    total_ms = start.elapsed_time(end)
-    ms_per_step = total_ms / args.steps
+    total_ms = evs[0].elapsed_time(evs[-1])
+    int_ms = [evs[k].elapsed_time(evs[k + 1]) / (cuts[k + 1] - cuts[k]) for k in range(n_int)]
+    ms_per_step = float(np.median(int_ms))
 
     bytes_steps = [sum(kv_bytes(args.warmup + i)) for i in range(args.steps)]
     bytes_per_step = sum(bytes_steps) / args.steps
@@ -262,6 +287,18 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4),
         "us_per_step": round(ms_per_step * 1e3, 1),
+        "us_per_step_intervals": [round(x * 1e3, 1) for x in int_ms],
+        "us_per_step_mean": round(total_ms / args.steps * 1e3, 1),
+        "step_decomposition_us": {
+            "decode_split": round(split_avg_ms * 1e3 * launches / args.steps, 1),
+            "decode_combine": round(merge_avg_ms * 1e3 * launches / args.steps, 1),
+            "between_kernels": round(ms_per_step * 1e3 - (split_avg_ms + merge_avg_ms) * 1e3
+                                     * launches / args.steps, 1),
+            "launches_per_step": launches // args.steps,
+            "note": ("kernel times from start/stop events the library passes to each launch "
+                     "(a separate run of the same steps); between_kernels = median us/step "
+                     "minus both"),
+        },
         "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
         "higher_is_better": True,
         "scaling": "weak",
@@ -303,10 +340,65 @@ def main():
 
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(args, cfg, prompts, windows, caps, scale, outl, osc,
-                                              dev, ms_per_step, bytes_per_step, eb, scales)
+                                              dev, ms_per_step, bytes_per_step, eb, scales,
+                                              one_core=one_core)
     for c in caches:
         c.free()
-    print(json.dumps(result), flush=True)
+    del ws
+    return result
+
+
+def suite(args, dev):
+    """The default run: the 112K-context headline (``--steps``, ``--warmup``,
+    ``--cpu-seconds``) and, under ``configs``, every other configuration of
+    the workload set -- the PR1 reference, 32K warm and cold (16 replicas),
+    the batch-16 serving mix reserved and paged, the 112K workload in the
+    fp8 and binary16 cache formats, and the 128K prefill -- each with its own
+    roofline and, where noted, its own oracle baseline on a bounded sample."""
+    import copy
+
+    def opts(**kw):
+        o = copy.copy(args)
+        o.kv_format, o.paged, o.replicas, o.unfused = "bf16", False, 1, False
+        for k, v in kw.items():
+            setattr(o, k, v)
+        return o
+
+    head = decode_run(opts(workload="ctx112k"), dev)
+    keep = ("metric", "value", "unit", "steps", "warmup", "ms_per_step", "us_per_step",
+            "us_per_step_intervals", "frac_of_hbm_peak", "step_decomposition_us", "dtype",
+            "roofline", "cpu_baseline", "config")
+    configs = {}
+
+    def add(name, fn):
+        t0 = time.time()
+        try:
+            r = fn()
+        except Exception as e:          # a refused call is reported, not fatal
+            r = {"error": f"{type(e).__name__}: {e}"}
+        r = {k: v for k, v in r.items() if k in keep or k == "error"}
+        r["bench_seconds"] = round(time.time() - t0, 1)
+        configs[name] = r
+        print(f"[bench] {name}: {r.get('us_per_step', r.get('ms_per_step'))} "
+              f"({r['bench_seconds']} s)", file=sys.stderr, flush=True)
+
+    add("pr1", lambda: decode_run(opts(workload="pr1", steps=6, warmup=2, cpu_seconds=2.0), dev))
+    add("ctx32k", lambda: decode_run(opts(workload="ctx32k", steps=60, warmup=8,
+                                          cpu_seconds=2.0), dev, one_core=False))
+    add("ctx32k_cold16", lambda: decode_run(opts(workload="ctx32k", steps=60, warmup=8,
+                                                 replicas=16, no_cpu_baseline=True), dev))
+    add("batch16", lambda: decode_run(opts(workload="batch16", steps=30, warmup=2,
+                                           cpu_seconds=2.0), dev, one_core=False))
+    add("batch16_paged", lambda: decode_run(opts(workload="batch16", steps=30, warmup=2,
+                                                 paged=True, no_cpu_baseline=True), dev))
+    add("ctx112k_fp8", lambda: decode_run(opts(workload="ctx112k", kv_format="fp8", steps=30,
+                                               warmup=4, no_cpu_baseline=True), dev))
+    add("ctx112k_f16", lambda: decode_run(opts(workload="ctx112k", kv_format="f16", steps=30,
+                                               warmup=4, no_cpu_baseline=True), dev))
+    add("prefill128k", lambda: prefill_run(opts(workload="prefill128k", steps=3, warmup=1,
+                                                cpu_seconds=8.0), dev))
+    head["configs"] = configs
+    return head
 
 
 def measured_traffic(args):
@@ -337,7 +429,7 @@ def measured_traffic(args):
 
 
 def cpu_baseline(args, cfg, prompts, windows, caps, scale, outl, osc, dev, gpu_ms, step_bytes,
-                 eb=2, scales=None):
+                 eb=2, scales=None, one_core=True):
     """The fp64 oracle timed on the host cores on a bounded sample of the same
     step: whole layers of decode step 0 (every sequence and query head),
     regenerated from the same seeds, until about ``--cpu-seconds`` of oracle
@@ -404,15 +496,15 @@ def cpu_baseline(args, cfg, prompts, windows, caps, scale, outl, osc, dev, gpu_m
         if spent >= args.cpu_seconds:
             break
     us_per_step = spent / done_bytes * step_bytes * 1e6
-    one_core = None
-    if first is not None:
+    one_core_rec = None
+    if first is not None and one_core:
         q, kh, vh, t, l = first
         t0 = time.perf_counter()
         oracle.decode_layer(q, kh, vh, t, cfg["n_sinks"], windows[l], scale, n_threads=1)
         s1 = time.perf_counter() - t0
         b1 = sum(min(prompts[b] + step + 1, caps[l][h]) * D * 2 * eb
                  for b in range(B) for h in range(Hkv))
-        one_core = {"value": round(s1 / b1 * step_bytes * 1e6, 1), "unit": "us/step",
+        one_core_rec = {"value": round(s1 / b1 * step_bytes * 1e6, 1), "unit": "us/step",
                     "gbs": round(b1 / s1 / 1e9, 3), "sample": f"layer {l} of step {step}",
                     "seconds": round(s1, 2)}
         del first
@@ -433,7 +525,7 @@ def cpu_baseline(args, cfg, prompts, windows, caps, scale, outl, osc, dev, gpu_m
         "hardware_concurrency": os.cpu_count(),
         "cpu": model,
         "kind": "oracle",
-        "one_core": one_core,
+        "one_core": one_core_rec,
         "sample": (f"decode step {step} (first timed step), layers 0..{layers - 1} of {L}, every "
                    f"sequence and query head; fp64 masked-full-history oracle"
                    f"{'' if fmt == 'bf16' else ' over the stored ' + fmt + ' values'}, "
@@ -453,7 +545,7 @@ def prefill_pairs(N, p0, p1, S, w):
     return upto(p1) - upto(p0)
 
 
-def prefill_main(args, dev):
+def prefill_run(args, dev):
     import numpy as np
     import torch
 
@@ -564,7 +656,7 @@ def prefill_main(args, dev):
                                                       step_flop, ms_per_step)
     for c in caches:
         c.free()
-    print(json.dumps(result), flush=True)
+    return result
 
 
 def prefill_traffic(n_chunks):

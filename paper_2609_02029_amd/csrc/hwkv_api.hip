@@ -234,6 +234,12 @@ int64_t tiles_for(int64_t n_valid) { return (n_valid + hwkv::kTile - 1) / hwkv::
 // counts: T = max(1, ceil(total tiles / target)) tiles per workgroup, and an
 // item of n tiles gets ceil(n / T) workgroups.  The launch then has at most
 // target + (number of items) workgroups, and never more than it has tiles.
+// The most workgroups plan_workgroups gives a launch of cnt items whose
+// tiles add up to at most `tiles`, whatever their lengths.
+int64_t max_workgroups(int64_t target, int64_t cnt, int64_t tiles) {
+  return std::min(tiles, target + cnt);
+}
+
 void plan_workgroups(const int64_t *tiles, int cnt, int64_t target, int32_t *nwg) {
   int64_t total = 0;
   for (int j = 0; j < cnt; ++j) total += tiles[j];
@@ -842,7 +848,7 @@ int alloc_impl(hwkv_cache **out, const hwkv_policy *p, int32_t batch, int64_t ma
         int64_t tiles = 0;
         for (int64_t i = i0; i < i0 + cnt; ++i)
           tiles += tiles_for(c->cap[l * p->n_kv_heads + i % p->n_kv_heads]);
-        parts += std::min(target + cnt, tiles);
+        parts += max_workgroups(target, cnt, tiles);
       }
       ws = std::max(ws, (size_t)parts * partial_bytes(*p));
     }
