@@ -676,13 +676,22 @@ def prefill_traffic(n_chunks):
 
 def probe_main(args, dev):
     """The practical read ceiling beside the decode roofline: passes of 16
-    launches of the library's read probe, each over its own region of the
-    ctx112k mean layer size (213.5 MB), as the 16 decode_split launches of a
-    step read theirs; the flat grid-stride sweep at 2, 4 and 8 wavefronts per
+    launches of the read probe (``_lib/libhwkv_probe.so``, measurement
+    tooling beside the library), each over its own region of the ctx112k
+    mean layer size (213.5 MB), as the 16 decode_split launches of a step
+    read theirs; the flat grid-stride sweep at 2, 4 and 8 wavefronts per
     SIMD, and the split kernel's own walk without its arithmetic."""
+    import ctypes
+
     import torch
 
-    from paper_2609_02029_amd import hwkv
+    from paper_2609_02029_amd import build
+
+    lib = ctypes.CDLL(build.PROBE_LIB)
+    lib.hwkv_read_probe.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
+                                    ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    lib.hwkv_read_probe.restype = ctypes.c_int
+    stream = torch.cuda.current_stream().cuda_stream
 
     L, per = 16, 3416322048 // 16 // 65536 * 65536
     buf = torch.empty(L * per, dtype=torch.uint8, device=dev)
@@ -699,7 +708,10 @@ def probe_main(args, dev):
                                ("decode_split walk, 8 loads in flight", 1, 8)]:
         def one_pass():
             for l in range(L):
-                hwkv.read_probe(buf[l * per:(l + 1) * per], pattern, wps, sink)
+                rc = lib.hwkv_read_probe(buf.data_ptr() + l * per, per, pattern, wps,
+                                         sink.data_ptr(), stream)
+                if rc != 0:
+                    raise RuntimeError(f"hwkv_read_probe returned {rc}")
         for _ in range(3):
             one_pass()
         torch.cuda.synchronize()

@@ -296,8 +296,12 @@ int hwkv_prefill_attn_ws(hwkv_cache *cache, int32_t layer, int32_t seq,
 
 /* Append one token to every sequence of `layer`: token n_b of sequence b
  * goes to slot(n_b) of each unit (once n_b >= S + w this overwrites token
- * n_b - w, the one leaving the window), then n_b += 1.  ENOMEM if a paged
- * cache's pool has too few pages for the tokens.
+ * n_b - w, the one leaving the window), then n_b += 1.  The window is J_t(w)
+ * of Method, Eq. conditional-attention (the last w positions up to the
+ * query's own), with the S sinks kept in front; a token is evicted when it
+ * leaves that set, as the sink-plus-recent cache of the Appendix evicts once
+ * it holds S + w tokens.  ENOMEM if a paged cache's pool has too few pages
+ * for the tokens.
  *   k_new, v_new   device bf16 [batch][n_kv_heads][head_dim], stored in
  *                  the cache's format.
  * ECAPACITY if a full unit of the layer already holds max_ctx tokens. */
@@ -497,25 +501,6 @@ int hwkv_decode_timing(hwkv_cache *cache, int32_t enable);
  * of kernel launch groups recorded, then clears the record. */
 int hwkv_decode_timing_read(hwkv_cache *cache, double *split_ms,
                             double *merge_ms, int64_t *launches);
-
-/* Read-bandwidth probe, for the decode roofline's practical ceiling: one
- * pass of 16-byte non-temporal loads (the decode split kernel's cache
- * policy) over bytes [0, bytes) of a device buffer, enqueued
- * on `stream` (loads only: the data is folded into one value, written to
- * *sink only if it equals an impossible pattern).
- *   pattern 0  flat grid-stride sweep: consecutive wavefronts read
- *              consecutive 1 KiB pieces and stride by the grid;
- *              waves_per_simd (2, 4 or 8) wavefronts per SIMD of the
- *              device, 8 / waves_per_simd loads in flight per lane
- *   pattern 1  the decode split kernel's walk without its arithmetic: one
- *              64 KiB tile (32 KiB of K, then 32 KiB of V) per wavefront,
- *              each half's 32 loads from step 7t mod 32 on; waves_per_simd
- *              (2, 4 or 8) is here the loads in flight per lane (the split
- *              kernel keeps 4)
- * buf and sink are device pointers; bytes a positive multiple of 65,536
- * below 2^31.  EINVAL otherwise; EDEVICE on a launch error. */
-int hwkv_read_probe(const void *buf, int64_t bytes, int32_t pattern,
-                    int32_t waves_per_simd, float *sink, void *stream);
 
 /* Test hook: synchronously copy unit (layer, kv_head) of sequence `seq` to
  * the host after all device work completes.  host_k, host_v receive

@@ -1,4 +1,6 @@
-"""Build ``_lib/libhwkv.so`` (the C-ABI library) for gfx950 with hipcc.
+"""Build ``_lib/libhwkv.so`` (the C-ABI library) for gfx950 with hipcc, and
+``_lib/libhwkv_probe.so``, the read-bandwidth probe the benchmark loads
+beside the decode roofline (measurement tooling, not part of the ABI).
 
 Every call recompiles all sources (in parallel), then links.  HIP code is
 compiled with packed fp32 instructions disabled.
@@ -19,7 +21,9 @@ ARCH = "gfx950"
 
 SOURCES = ["hwkv_api.hip", "decode_kernels.hip", "decode_split_bf16.hip",
            "decode_split_f16.hip", "decode_split_fp8.hip", "write_kernels.hip",
-           "prefill_attn_kernels.hip", "calib_kernels.hip", "probe_kernels.hip"]
+           "prefill_attn_kernels.hip", "calib_kernels.hip"]
+PROBE_SOURCE = os.path.join("probe", "read_probe.hip")
+PROBE_LIB = os.path.join(LIBDIR, "libhwkv_probe.so")
 
 CFLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
@@ -40,6 +44,7 @@ def flags_for(src):
 
 def _compile(src, verbose):
     obj = os.path.join(OBJDIR, os.path.splitext(src)[0] + ".o")
+    os.makedirs(os.path.dirname(obj), exist_ok=True)
     cmd = [HIPCC, *flags_for(src), "-c", os.path.join(CSRC, src), "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
@@ -49,19 +54,26 @@ def _compile(src, verbose):
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(OBJDIR, exist_ok=True)
-    os.makedirs(LIBDIR, exist_ok=True)
-    with cf.ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
-    tmp = LIB + ".tmp"
+def _link(objs, lib, verbose):
+    tmp = lib + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+
+
+def build(verbose: bool = False) -> str:
+    """Builds both libraries; returns the path of libhwkv.so."""
+    os.makedirs(OBJDIR, exist_ok=True)
+    os.makedirs(LIBDIR, exist_ok=True)
+    srcs = SOURCES + [PROBE_SOURCE]
+    with cf.ThreadPoolExecutor(max_workers=len(srcs)) as ex:
+        objs = list(ex.map(lambda s: _compile(s, verbose), srcs))
+    _link(objs[:-1], LIB, verbose)
+    _link(objs[-1:], PROBE_LIB, verbose)
     return LIB
 
 

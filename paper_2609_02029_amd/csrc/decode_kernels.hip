@@ -180,7 +180,8 @@ struct CombineLaunch {
 
 int decode_workgroup_target(int fmt, int D, int G) {
   // at most one workgroup per SIMD slot the register budget holds
-  const int per_cu4 = std::min(kDecodeWgPerCuX4, 4 * split_waves_per_eu(D, G, fmt));
+  const int want = fmt == HWKV_KV_FP8_E4M3 ? kDecodeWgPerCuX4Fp8 : kDecodeWgPerCuX4;
+  const int per_cu4 = std::min(want, 4 * split_waves_per_eu(D, G, fmt));
   return std::max(1, per_cu4 * device_cus() / 4);
 }
 int decode_combine_blocks_per_item(int D, int G) {

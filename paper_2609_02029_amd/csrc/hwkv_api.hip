@@ -1768,29 +1768,6 @@ int hwkv_decode_timing_read(hwkv_cache *c, double *split_ms, double *merge_ms,
   return ok();
 }
 
-int hwkv_read_probe(const void *buf, int64_t bytes, int32_t pattern,
-                    int32_t waves_per_simd, float *sink, void *stream) {
-  if (!buf || !sink) return fail(HWKV_EINVAL, "buf and sink must be non-null");
-  if (bytes <= 0 || bytes % 65536 != 0 || bytes > (int64_t)INT32_MAX)
-    return fail(HWKV_EINVAL, "bytes must be a positive multiple of 65536 below 2^31");
-  if (pattern != 0 && pattern != 1) return fail(HWKV_EINVAL, "pattern must be 0 or 1");
-  if (waves_per_simd != 2 && waves_per_simd != 4 && waves_per_simd != 8)
-    return fail(HWKV_EINVAL, "waves_per_simd (pattern 1: loads in flight) must be 2, 4 or 8");
-  int dev = 0, n_cus = 0;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&n_cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-      n_cus < 1)
-    return fail(HWKV_EDEVICE, "no device");
-  hwkv::ProbeArgs a;
-  a.buf = static_cast<const uint8_t *>(buf);
-  a.bytes = bytes;
-  a.sink = sink;
-  a.pattern = pattern;
-  a.waves_per_simd = waves_per_simd;
-  const int rc = check_device(hwkv::launch_probe(a, n_cus, (hipStream_t)stream), "probe launch");
-  return rc == HWKV_OK ? ok() : rc;
-}
-
 int hwkv_cache_read_unit(const hwkv_cache *c, int32_t layer, int32_t kv_head,
                          int32_t seq, void *host_k, void *host_v,
                          int64_t *n_valid) {

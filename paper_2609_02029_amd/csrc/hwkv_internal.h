@@ -35,10 +35,16 @@ constexpr int kDecodeWaves = 4;  // waves of a decode split workgroup
 #ifndef HWKV_DECODE_WG_PER_CU_X4
 #define HWKV_DECODE_WG_PER_CU_X4 8
 #endif
+#ifndef HWKV_DECODE_WG_PER_CU_X4_FP8
+#define HWKV_DECODE_WG_PER_CU_X4_FP8 12
+#endif
 // Decode split workgroups a launch aims at, in quarters per CU: the host
 // picks the tiles per workgroup so that the launch has about this many
 // workgroups (at most as many as the kernel's register budget holds at once).
+// Two per CU for the 16-bit formats; three for fp8, whose split kernel spends
+// more VALU work per byte and hides it better with a third wave per SIMD.
 constexpr int kDecodeWgPerCuX4 = HWKV_DECODE_WG_PER_CU_X4;
+constexpr int kDecodeWgPerCuX4Fp8 = HWKV_DECODE_WG_PER_CU_X4_FP8;
 
 // Decode work of one launch: items are (sequence b, kv head h) pairs of one
 // layer; item i owns rows [0, n_valid[i]) of its unit and the launch's split
@@ -274,17 +280,6 @@ constexpr int kReplayTilesPerSplit = 128;   // 32-key tiles per split, at most
 // CU.
 constexpr int kReplayMinTilesPerSplit = HWKV_REPLAY_MIN_TILES;
 hipError_t launch_calib_means(const CalibArgs &a, hipStream_t s);
-
-// Read-bandwidth probes (loads only): pattern 0 flat grid-stride sweep,
-// pattern 1 the decode split kernel's tile walk.
-struct ProbeArgs {
-  const uint8_t *buf;
-  int64_t bytes;                 // a multiple of 64 KiB below 2^31
-  float *sink;                   // written only for an impossible fold
-  int32_t pattern;
-  int32_t waves_per_simd;        // pattern 0: 2, 4 or 8
-};
-hipError_t launch_probe(const ProbeArgs &a, int n_cus, hipStream_t s);
 
 }  // namespace hwkv
 

@@ -70,7 +70,6 @@ SYMBOLS = {
     "hwkv_cache_read_unit": ([_vp, _i32, _i32, _i32, _vp, _vp, _P(_i64)], ctypes.c_int),
     "hwkv_decode_timing": ([_vp, _i32], ctypes.c_int),
     "hwkv_decode_timing_read": ([_vp, _P(_dbl), _P(_dbl), _P(_i64)], ctypes.c_int),
-    "hwkv_read_probe": ([_vp, _i64, _i32, _i32, _vp, _vp], ctypes.c_int),
     "hwkv_calib_workspace_bytes": ([_i32, _i32, _i32, _i64, _i64, _P(_sz)], ctypes.c_int),
     "hwkv_calib_replay": ([_i32, _i32, _i32, _i32, _i32, _vp, _i64, _vp, _vp, _i64, _vp, _vp,
                            _flt, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp], ctypes.c_int),
@@ -432,20 +431,6 @@ def decode_timing_read(cache):
     _check(_lib.hwkv_decode_timing_read(cache.handle, ctypes.byref(sp), ctypes.byref(mg),
                                         ctypes.byref(n)))
     return sp.value, mg.value, n.value
-
-
-def read_probe(buf, pattern, waves_per_simd=2, sink=None, stream=None):
-    """One read pass over the device uint8 tensor ``buf`` (see
-    ``hwkv_read_probe``): pattern 0 the flat grid-stride sweep, 1 the decode
-    split kernel's walk.  ``sink``: a device float32 tensor (a fresh one if
-    None)."""
-    import torch
-    if sink is None:
-        sink = torch.zeros(1, dtype=torch.float32, device=buf.device)
-    _check(_lib.hwkv_read_probe(_dev(buf, "uint8", "buf"), buf.numel(),
-                                int(pattern), int(waves_per_simd),
-                                _dev(sink, "float32", "sink"), _stream(stream)))
-    return sink
 
 
 def calib_workspace_bytes(n_q_heads, head_dim, n_sinks, n_hist, n_rows, n_kv_heads=None,

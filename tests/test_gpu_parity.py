@@ -337,12 +337,20 @@ def test_largest_capacity():
 # equal words (every fold is zero), and leaves the sink untouched
 # ---------------------------------------------------------------------------
 def test_read_probe_runs():
+    import ctypes
+
+    from paper_2609_02029_amd import build
+    lib = ctypes.CDLL(build.PROBE_LIB)
+    lib.hwkv_read_probe.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
+                                    ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
     dev = torch.device("cuda:0")
     buf = torch.full((64 << 20,), 7, dtype=torch.uint8, device=dev)
     sink = torch.zeros(1, dtype=torch.float32, device=dev)
+    s = torch.cuda.current_stream().cuda_stream
     for pattern, wps in [(0, 2), (0, 4), (0, 8), (1, 2), (1, 4), (1, 8)]:
-        hwkv.read_probe(buf, pattern, wps, sink)
-        hwkv.read_probe(buf[: 3 << 16], pattern, wps, sink)   # fewer tiles than waves
+        assert lib.hwkv_read_probe(buf.data_ptr(), buf.numel(), pattern, wps, sink.data_ptr(), s) == 0
+        # fewer tiles than workgroups
+        assert lib.hwkv_read_probe(buf.data_ptr(), 3 << 16, pattern, wps, sink.data_ptr(), s) == 0
     torch.cuda.synchronize()
     assert float(sink.cpu()[0]) == 0.0
 

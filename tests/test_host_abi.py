@@ -556,16 +556,23 @@ def test_paged_pool_checks_before_device_work(hw):
     L.hwkv_cache_free(h)
 
 
-def test_read_probe_argument_errors(hw):
-    """The read probe validates everything before touching the device."""
-    L = hw._lib
+def test_read_probe_argument_errors():
+    """The read probe (its own library, measurement tooling beside the
+    runtime) validates everything before touching the device, and the
+    runtime's library does not export it."""
+    from paper_2609_02029_amd import build
+    L = ctypes.CDLL(build.PROBE_LIB)
+    L.hwkv_read_probe.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
+                                  ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
     f = ctypes.c_void_p(FAKE)
-    assert L.hwkv_read_probe(None, 65536, 0, 2, f, None) == hw.EINVAL
-    assert L.hwkv_read_probe(f, 65536, 0, 2, None, None) == hw.EINVAL
+    assert L.hwkv_read_probe(None, 65536, 0, 2, f, None) == 1
+    assert L.hwkv_read_probe(f, 65536, 0, 2, None, None) == 1
     for bytes_ in (0, -65536, 65535, 65536 + 1024, 1 << 31):
-        assert L.hwkv_read_probe(f, bytes_, 0, 2, f, None) == hw.EINVAL, bytes_
-    assert L.hwkv_read_probe(f, 65536, 2, 2, f, None) == hw.EINVAL
+        assert L.hwkv_read_probe(f, bytes_, 0, 2, f, None) == 1, bytes_
+    assert L.hwkv_read_probe(f, 65536, 2, 2, f, None) == 1
     for pattern in (0, 1):
         for wps in (0, 1, 3, 16):
-            assert L.hwkv_read_probe(f, 65536, pattern, wps, f, None) == hw.EINVAL, wps
+            assert L.hwkv_read_probe(f, 65536, pattern, wps, f, None) == 1, wps
+    runtime = ctypes.CDLL(build.LIB)
+    assert not hasattr(runtime, "hwkv_read_probe")
 
