@@ -481,7 +481,8 @@ int hwkv_policy_serialize(const hwkv_policy *policy, const char *artifact_id,
  * (validated as by hwkv_policy_set) and the recorded fields (each output
  * pointer may be NULL; artifact_id receives at most id_cap - 1 characters
  * and a NUL).  EINVAL on any other text: unknown, missing or repeated keys,
- * malformed values, trailing characters. */
+ * malformed values, strings with escapes or characters outside printable
+ * ASCII, trailing characters. */
 int hwkv_policy_deserialize(const char *buf, size_t len, hwkv_policy **out,
                             char *artifact_id, size_t id_cap, uint64_t *seed,
                             int32_t *grid_index, double *tau, double *rate,

@@ -29,7 +29,8 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# HWKV_ORACLE_LIBRARY may name the sanitizer build of the same source.
+_LIB_PATH = os.environ.get("HWKV_ORACLE_LIBRARY") or os.path.join(_HERE, "liboracle.so")
 _lib = None
 
 _i64 = ctypes.c_int64

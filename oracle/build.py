@@ -25,5 +25,24 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+def build_sanitized(out_dir: str, verbose: bool = False) -> str:
+    """The same source with AddressSanitizer and UndefinedBehaviorSanitizer,
+    built by clang against its shared sanitizer runtime (the one the
+    library's sanitizer build uses, so both load into one process); returns
+    the path of ``out_dir``/liboracle_san.so."""
+    os.makedirs(out_dir, exist_ok=True)
+    lib = os.path.join(out_dir, "liboracle_san.so")
+    cmd = [
+        "/opt/rocm/llvm/bin/clang", "-std=c11", "-O1", "-g", "-ffp-contract=off",
+        "-fno-fast-math", "-fPIC", "-shared", "-D_POSIX_C_SOURCE=200809L",
+        "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+        "-fno-omit-frame-pointer", "-shared-libsan", SRC, "-o", lib, "-lm", "-lpthread",
+    ]
+    if verbose:
+        print(" ".join(cmd))
+    subprocess.run(cmd, check=True)
+    return lib
+
+
 if __name__ == "__main__":
     print(build(verbose=True))

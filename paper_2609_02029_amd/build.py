@@ -77,5 +77,50 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+# The CPU tests' sanitizer build: the same sources with AddressSanitizer and
+# UndefinedBehaviorSanitizer on the host code only (device code is compiled
+# as usual and never runs on the CPU), linked against clang's shared
+# sanitizer runtime, which the loading process must preload.
+CLANGXX = "/opt/rocm/llvm/bin/clang++"
+SAN_HOST_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined", "-Xarch_host", "-fno-sanitize-recover=all", "-Xarch_host", "-fno-omit-frame-pointer"]
+SAN_LINK_FLAGS = ["-fsanitize=address,undefined", "-shared-libsan"]
+
+
+def sanitizer_runtime() -> str:
+    """Path of the shared sanitizer runtime the sanitizer build needs."""
+    r = subprocess.run([CLANGXX, "-print-file-name=libclang_rt.asan-x86_64.so"],
+                       capture_output=True, text=True, check=True)
+    return r.stdout.strip()
+
+
+def build_host_sanitized(out_dir: str, verbose: bool = False) -> str:
+    """Builds libhwkv.so's sources into ``out_dir``/libhwkv_san.so with the
+    host sanitizers on; returns its path."""
+    os.makedirs(out_dir, exist_ok=True)
+
+    def one(src):
+        obj = os.path.join(out_dir, os.path.splitext(src)[0] + ".o")
+        flags = [f for f in flags_for(src) if f != "-O3"]
+        cmd = [HIPCC, *flags, "-O1", "-g", *SAN_HOST_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")
+        return obj
+
+    with cf.ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
+        objs = list(ex.map(one, SOURCES))
+    lib = os.path.join(out_dir, "libhwkv_san.so")
+    cmd = [CLANGXX, "-shared", "-fPIC", *SAN_LINK_FLAGS, *objs, "-L/opt/rocm/lib",
+           "-Wl,-rpath,/opt/rocm/lib", "-lamdhip64", "-o", lib]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
+    return lib
+
+
 if __name__ == "__main__":
     print(build(verbose=True))

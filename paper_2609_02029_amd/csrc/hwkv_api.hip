@@ -1087,6 +1087,8 @@ int hwkv_prefill_attn_ws(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0
                            ws_bytes, stream);
 }
 
+}  // extern "C"
+
 namespace {
 
 size_t replay_rows_bytes(int64_t n_rows) { return (size_t)((n_rows * 4 + 255) / 256 * 256); }
@@ -1149,6 +1151,7 @@ int stage_rows(const int64_t *rows, int64_t n, void *dst, hipStream_t st) {
 int64_t replay_partial_sets(int64_t n_hist) { return replay_max_splits(n_hist) + 3; }
 
 }  // namespace
+extern "C" {
 
 int hwkv_calib_workspace_bytes(int32_t n_q_heads, int32_t head_dim, int32_t n_sinks,
                                int64_t n_hist, int64_t n_rows, size_t *bytes) {
@@ -1426,6 +1429,8 @@ int hwkv_budget_select(int32_t n_records, const double *rates,
   return ok();
 }
 
+}  // extern "C"
+
 namespace {
 
 const char kArtifactFormat[] = "hwkv-policy/1";
@@ -1437,8 +1442,8 @@ std::string fmt_double(double x) {
 }
 
 // A strict reader for the artifact's JSON subset: one object whose values
-// are strings without escapes, numbers, arrays of integers or arrays of
-// arrays of integers.
+// are strings of printable ASCII without escapes, numbers, arrays of
+// integers or arrays of arrays of integers.
 struct ArtifactReader {
   const char *p, *end;
   bool ok = true;
@@ -1458,7 +1463,8 @@ struct ArtifactReader {
     if (p >= end || *p != '"') return false;
     const char *q = ++p;
     while (p < end && *p != '"') {
-      if (*p == '\\' || (unsigned char)*p < 0x20) return false;
+      // printable ASCII without escapes: what the writer emits
+      if (*p == '\\' || (unsigned char)*p < 0x20 || (unsigned char)*p > 0x7e) return false;
       ++p;
     }
     if (p >= end) return false;
@@ -1518,6 +1524,7 @@ struct ArtifactReader {
 };
 
 }  // namespace
+extern "C" {
 
 int hwkv_policy_serialize(const hwkv_policy *p, const char *artifact_id, uint64_t seed,
                           int32_t grid_index, double tau, double rate, double floor,

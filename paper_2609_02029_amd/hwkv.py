@@ -10,7 +10,9 @@ import ctypes
 import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "_lib", "libhwkv.so")
+# HWKV_LIBRARY may name another build of the same library (the CPU tests'
+# host-sanitizer build); by default the in-tree one is loaded.
+LIB_PATH = os.environ.get("HWKV_LIBRARY") or os.path.join(_HERE, "_lib", "libhwkv.so")
 
 OK, EINVAL, ENOMEM, ECAPACITY, ESTATE, EDEVICE = 0, 1, 2, 3, 4, 5
 # cache formats (HWKV_KV_*): name -> (code, bytes per element)

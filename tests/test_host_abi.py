@@ -400,6 +400,71 @@ def test_policy_artifact_rejects_malformed_text(hw, golden):
                                          n.value, ctypes.byref(n)) == hw.ENOMEM
 
 
+def _deserialize_exact(hw, raw):
+    """hwkv_policy_deserialize over a malloc'd block of exactly len(raw)
+    bytes with no NUL after it: a read past the stated length is then a heap
+    overflow that the address-sanitizer build of the library reports.
+    Returns (status, policy handle or None)."""
+    libc = ctypes.CDLL(None)
+    libc.malloc.restype = ctypes.c_void_p
+    libc.malloc.argtypes = [ctypes.c_size_t]
+    libc.free.argtypes = [ctypes.c_void_p]
+    buf = libc.malloc(max(1, len(raw)))
+    try:
+        ctypes.memmove(buf, raw, len(raw))
+        h = ctypes.c_void_p()
+        aid = ctypes.create_string_buffer(256)
+        seed, gi = ctypes.c_uint64(), ctypes.c_int32()
+        tau, rate, fl = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+        rc = hw._lib.hwkv_policy_deserialize(ctypes.cast(buf, ctypes.c_char_p), len(raw),
+                                             ctypes.byref(h), aid, 256, ctypes.byref(seed),
+                                             ctypes.byref(gi), ctypes.byref(tau),
+                                             ctypes.byref(rate), ctypes.byref(fl))
+    finally:
+        libc.free(buf)
+    return rc, h.value
+
+
+def test_policy_artifact_every_prefix_and_seeded_mutations(hw, golden):
+    """Every prefix of a valid artifact that cuts into its text is refused;
+    seeded one-byte
+    mutations are refused with EINVAL or, where the text stays well formed,
+    parse to a policy whose artifact parses back to itself.  Run under the
+    sanitizer tier, this is where an unchecked read or length shows."""
+    good = golden("policy_artifact.json")["text"].encode("ascii")
+    rc, h = _deserialize_exact(hw, good)
+    assert rc == hw.OK and h
+    hw._lib.hwkv_policy_free(ctypes.c_void_p(h))
+    body = len(good.rstrip())          # trailing white space is optional
+    for n in range(len(good)):
+        rc, h = _deserialize_exact(hw, good[:n])
+        if n >= body:
+            assert rc == hw.OK, n
+            hw._lib.hwkv_policy_free(ctypes.c_void_p(h))
+        else:
+            assert (rc, h) == (hw.EINVAL, None), n
+    r = np.random.default_rng(17)
+    alphabet = b'"{}[],:-+.eE0129 \\\n\x00\xff'
+    accepted = 0
+    for _ in range(600):
+        raw = bytearray(good)
+        for _k in range(int(r.integers(1, 4))):
+            i = int(r.integers(0, len(raw)))
+            raw[i] = alphabet[int(r.integers(0, len(alphabet)))]
+        rc, h = _deserialize_exact(hw, bytes(raw))
+        assert rc in (hw.OK, hw.EINVAL)
+        if rc == hw.OK:
+            accepted += 1
+            hw._lib.hwkv_policy_free(ctypes.c_void_p(h))
+            q, meta = hw.policy_deserialize(bytes(raw))
+            text = hw.policy_serialize(q, **meta)
+            q2, meta2 = hw.policy_deserialize(text)
+            assert meta2 == meta and hw.policy_serialize(q2, **meta2) == text
+        else:
+            assert h is None
+    assert accepted < 600
+
+
 # --------------------------------------------------------------------------
 # cache formats
 # --------------------------------------------------------------------------
