@@ -264,31 +264,42 @@ int hwkv_prefill_write(hwkv_cache *cache, int32_t layer, int32_t seq,
  * value product rounded to bf16.  ESTATE if pos0 != n(layer, seq);
  * ECAPACITY if pos0 + n_tokens > max_ctx; EINVAL on bad indices, null
  * pointers, a non-finite or non-positive scale, or a cache whose format is
- * not bf16 (see hwkv_prefill_attn_ws); n_tokens == 0 is a no-op. */
+ * not bf16 (hwkv_prefill_attn_ws takes every format); n_tokens == 0 is a
+ * no-op. */
 int hwkv_prefill_attn(hwkv_cache *cache, int32_t layer, int32_t seq,
                       int64_t pos0, int64_t n_tokens, const void *q,
                       const void *k, const void *v, float scale, void *out,
                       void *stream);
 
 /* Device workspace bytes hwkv_prefill_attn_ws needs on this cache for chunks
- * of up to n_tokens tokens: 0 for a bf16 cache; for an fp8 cache, a bf16
- * image of one sequence's units of the largest layer (K tiles and V rows,
- * the layout of a bf16 cache) plus the chunk's K and V. */
+ * of up to n_tokens tokens: 0 for a bf16 cache; for a binary16 cache, the
+ * chunk's K and V as stored (2 * n_tokens * n_kv_heads * head_dim * 2
+ * bytes); for an fp8 cache, a bf16 image of one sequence's units of the
+ * largest layer (K tiles and V rows, the layout of a bf16 cache) plus the
+ * chunk's K and V. */
 int hwkv_prefill_attn_workspace_bytes(const hwkv_cache *cache, int64_t n_tokens,
                                       size_t *bytes);
 
-/* hwkv_prefill_attn for bf16 and fp8 caches.  With an fp8 cache the keys and
- * values enter with their stored values -- the cached ones as stored, the
- * chunk's own as the cache will store them (code(x / s)) -- because a format
+/* hwkv_prefill_attn for every cache format.  With an fp8 or binary16 cache
+ * the keys and values enter with their stored values -- the cached ones as
+ * stored, the chunk's own as the cache will store them -- because a format
  * that changes numerical execution is used by every consumer of the cache
- * (Method, Eq. nominal-storage and the paragraph after it): q.k is taken
- * over the decoded codes and multiplied by the K scale, the output by the V
- * scale.  Every E4M3 value is a bf16 value, so the codes are staged into ws
- * as bf16 (exactly) and the bf16 MFMA kernel runs on them.
+ * (Method, Eq. nominal-storage and the paragraph after it).
+ *   fp8: q.k is taken over the decoded codes and multiplied by the K scale,
+ *        the output by the V scale.  Every E4M3 value is a bf16 value, so
+ *        the codes are staged into ws as bf16 (exactly) and the bf16 MFMA
+ *        kernel runs on them.
+ *   binary16: the cached rows are read in place and the chunk's rows are
+ *        staged into ws as binary16; binary16 MFMA products.  q enters as
+ *        binary16 after scaling by a power of two per group of 32
+ *        consecutive (token, q head) columns, exact for every component
+ *        within a factor 2^31 of the group's largest |q|; the softmax
+ *        weights enter the value product rounded to binary16 (with a 2^7
+ *        bias that keeps them out of its subnormal range).
  *   ws, ws_bytes  device workspace of >= hwkv_prefill_attn_workspace_bytes
  *                 for n_tokens (may be NULL for a bf16 cache)
  * Other arguments, results and errors as hwkv_prefill_attn; EINVAL for a
- * binary16 cache (its values are not bf16 values) or a short workspace. */
+ * short or missing workspace. */
 int hwkv_prefill_attn_ws(hwkv_cache *cache, int32_t layer, int32_t seq,
                          int64_t pos0, int64_t n_tokens, const void *q,
                          const void *k, const void *v, float scale, void *out,

@@ -326,10 +326,11 @@ int take_pages(hwkv_cache *c, int32_t layer,
   return HWKV_OK;
 }
 
-// Element offsets (bf16) of the prefill-attention staging image of an fp8
-// cache: per kv head of the layer its K tiles and V rows in the bf16 cache
-// layout (cap_pad rows each), then the chunk's K and V ([n_tokens][Hkv][D]);
-// returns the bytes.
+// Element offsets (2-byte elements) of the prefill-attention staging area:
+// for an fp8 cache, per kv head of the layer its K tiles and V rows widened
+// to bf16 in the bf16 cache layout (cap_pad rows each); then, for fp8 and
+// binary16 caches, the chunk's K and V ([n_tokens][Hkv][D]) as the cache will
+// store them.  Returns the bytes (0 for a bf16 cache).
 struct StageLayout {
   std::vector<int64_t> k_img, v_img;
   int64_t k_in = 0, v_in = 0;
@@ -339,7 +340,11 @@ size_t stage_layout(const hwkv_cache *c, int32_t layer, int64_t n_tokens, StageL
   const int64_t D = p.head_dim;
   int64_t off = 0;
   StageLayout L;
-  for (int32_t h = 0; h < p.n_kv_heads; ++h) {
+  if (c->fmt == HWKV_KV_BF16) {
+    if (out) *out = L;
+    return 0;
+  }
+  for (int32_t h = 0; h < p.n_kv_heads && c->fmt == HWKV_KV_FP8_E4M3; ++h) {
     const int32_t u = layer * p.n_kv_heads + h;
     L.k_img.push_back(off);
     off += c->cap_pad[u] * D;
@@ -359,10 +364,10 @@ int prefill_attn_impl(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0,
                       int64_t n_tokens, const void *q, const void *k, const void *v,
                       float scale, void *out, void *ws, size_t ws_bytes, void *stream) {
   if (!c) return fail(HWKV_EINVAL, "cache is null");
-  if (c->fmt == HWKV_KV_F16)
-    return fail(HWKV_EINVAL, "prefill attention reads bf16 or fp8 caches (binary16 "
-                             "values are not bf16 values)");
+  // fp8: the units are staged as bf16 code values; fp8 and binary16: the
+  // chunk's own keys and values are staged as the cache will store them
   const bool staged = c->fmt == HWKV_KV_FP8_E4M3;
+  const bool chunk_staged = c->fmt != HWKV_KV_BF16;
   const hwkv_policy &p = c->pol;
   if (layer < 0 || layer >= p.n_layers || seq < 0 || seq >= c->batch)
     return fail(HWKV_EINVAL, "layer or seq out of range");
@@ -379,7 +384,7 @@ int prefill_attn_impl(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0,
   if (!q || !k || !v || !out)
     return fail(HWKV_EINVAL, "q, k, v and out must be non-null");
   StageLayout SL;
-  if (staged) {
+  if (chunk_staged) {
     const size_t need = stage_layout(c, layer, n_tokens, &SL);
     if (!ws || ws_bytes < need)
       return fail(HWKV_EINVAL, "workspace missing or too small (need " +
@@ -424,8 +429,8 @@ int prefill_attn_impl(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0,
   const int64_t nb = (cols + per - 1) / per;
   if (nb * H > (int64_t)INT32_MAX)
     return fail(HWKV_EINVAL, "n_tokens too large for one launch");
+  uint16_t *img = static_cast<uint16_t *>(ws);
   if (staged) {
-    uint16_t *img = static_cast<uint16_t *>(ws);
     // the occupied rows of every unit (the keys below pos0), widened
     hwkv::StageArgs sa;
     std::memset(&sa, 0, sizeof sa);
@@ -452,9 +457,17 @@ int prefill_attn_impl(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0,
     if (max_chunks > 0 &&
         (rc = check_device(hwkv::launch_stage_units((int)D, sa, st), "stage launch")) != HWKV_OK)
       return rc;
+    a.cache = img;
+  } else {
+    a.cache = reinterpret_cast<const uint16_t *>(c->base);
+    a.page_table = device_page_table(c);
+    a.pool_off = c->pool_off;
+  }
+  if (chunk_staged) {
     // the chunk's own keys and values as the cache will store them
     hwkv::StageChunkArgs ca;
     std::memset(&ca, 0, sizeof ca);
+    ca.fmt = c->fmt;
     ca.k = static_cast<const uint16_t *>(k);
     ca.v = static_cast<const uint16_t *>(v);
     ca.k_out = img + SL.k_in;
@@ -465,15 +478,11 @@ int prefill_attn_impl(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0,
     }
     ca.n_chunks = n_tokens * H * (D / 8);
     ca.n_kv_heads = H;
-    if ((rc = check_device(hwkv::launch_stage_chunk((int)D, ca, st), "stage launch")) != HWKV_OK)
-      return rc;
-    a.cache = img;
+    const int rc = check_device(hwkv::launch_stage_chunk((int)D, ca, st), "stage launch");
+    if (rc != HWKV_OK) return rc;
     a.k = img + SL.k_in;
     a.v = img + SL.v_in;
   } else {
-    a.cache = reinterpret_cast<const uint16_t *>(c->base);
-    a.page_table = device_page_table(c);
-    a.pool_off = c->pool_off;
     a.k = static_cast<const uint16_t *>(k);
     a.v = static_cast<const uint16_t *>(v);
   }
@@ -486,7 +495,8 @@ int prefill_attn_impl(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0,
   a.n_sinks = p.n_sinks;
   a.n_col_blocks = (int32_t)nb;
   a.scale_log2 = scale * 1.4426950408889634f;
-  return check_device(hwkv::launch_prefill_attn(p.head_dim, a, st), "prefill_attn launch") ==
+  return check_device(hwkv::launch_prefill_attn(p.head_dim, c->fmt == HWKV_KV_F16, a, st),
+                      "prefill_attn launch") ==
                  HWKV_OK
              ? ok()
              : HWKV_EDEVICE;
@@ -1062,7 +1072,7 @@ int hwkv_prefill_attn(hwkv_cache *c, int32_t layer, int32_t seq, int64_t pos0,
                       const void *v, float scale, void *out, void *stream) {
   if (c && c->fmt != HWKV_KV_BF16)
     return fail(HWKV_EINVAL, "prefill attention needs a bf16 cache here "
-                             "(hwkv_prefill_attn_ws takes fp8 caches)");
+                             "(hwkv_prefill_attn_ws takes fp8 and binary16 caches)");
   return prefill_attn_impl(c, layer, seq, pos0, n_tokens, q, k, v, scale, out,
                            nullptr, 0, stream);
 }
@@ -1072,9 +1082,8 @@ int hwkv_prefill_attn_workspace_bytes(const hwkv_cache *c, int64_t n_tokens,
   if (!c || !bytes) return fail(HWKV_EINVAL, "null argument");
   if (n_tokens < 0) return fail(HWKV_EINVAL, "n_tokens must be >= 0");
   size_t best = 0;
-  if (c->fmt == HWKV_KV_FP8_E4M3)
-    for (int32_t l = 0; l < c->pol.n_layers; ++l)
-      best = std::max(best, stage_layout(c, l, n_tokens, nullptr));
+  for (int32_t l = 0; l < c->pol.n_layers; ++l)
+    best = std::max(best, stage_layout(c, l, n_tokens, nullptr));
   *bytes = best;
   return ok();
 }
@@ -1283,6 +1292,7 @@ int hwkv_calib_replay_format(int32_t n_kv_heads, int32_t n_q_heads, int32_t head
     uint16_t *vst = kst + (size_t)n_hist * n_kv_heads * head_dim;
     hwkv::StageChunkArgs ca;
     std::memset(&ca, 0, sizeof ca);
+    ca.fmt = HWKV_KV_FP8_E4M3;
     ca.k = static_cast<const uint16_t *>(k);
     ca.v = static_cast<const uint16_t *>(v);
     ca.k_out = kst;

@@ -146,7 +146,7 @@ struct PrefillAttnHead {
 struct PrefillAttnArgs {
   PrefillAttnHead head[kMaxItems];
   int32_t head_order[kMaxItems];
-  const uint16_t *cache;         // bf16 caches only
+  const uint16_t *cache;         // 2-byte elements: bf16 or binary16
   const int32_t *page_table;     // paged caches (else null)
   int64_t pool_off;              // element offset of page 0
   const uint16_t *q;             // [n_tokens][Hq][D]
@@ -209,8 +209,10 @@ struct StageArgs {
 };
 hipError_t launch_stage_units(int D, const StageArgs &a, hipStream_t s);
 struct StageChunkArgs {
+  int32_t fmt;                   // HWKV_KV_FP8_E4M3 or HWKV_KV_F16
   const uint16_t *k, *v;         // [n_tokens][Hkv][D] bf16 inputs
-  uint16_t *k_out, *v_out;       // the same layout, bf16 code values
+  uint16_t *k_out, *v_out;       // the same layout: the stored values, as bf16
+                                 // code values (fp8) or binary16 (f16)
   float k_scale[kMaxItems];      // per kv head of the layer
   float v_scale[kMaxItems];
   int64_t n_chunks;              // n_tokens * Hkv * D / 8
@@ -218,7 +220,8 @@ struct StageChunkArgs {
 };
 hipError_t launch_stage_chunk(int D, const StageChunkArgs &a, hipStream_t s);
 int prefill_attn_columns_per_block();   // (token, q head) columns
-hipError_t launch_prefill_attn(int D, const PrefillAttnArgs &a, hipStream_t s);
+// f16: the cache, k and v hold binary16 values (else bf16); q is bf16.
+hipError_t launch_prefill_attn(int D, bool f16, const PrefillAttnArgs &a, hipStream_t s);
 
 // Calibration scores: for every (row, q head), the stabilised cosine of each
 // candidate output against the full one (and of the full one against a

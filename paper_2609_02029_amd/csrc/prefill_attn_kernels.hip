@@ -1,5 +1,5 @@
 // prefill_attn_kernels.hip -- sink + window causal attention of one prefill
-// chunk on bf16 MFMA (gfx950).
+// chunk on bf16 or binary16 MFMA (gfx950).
 //
 // Query token t of the chunk [p0, p1), query head q of KV head h = q / G,
 // attends over R(t + 1) restricted to [0, t]: positions s <= t with s < S or
@@ -48,6 +48,17 @@
 // Keys past the tile's range read a zero row, so they are exact zeros (and
 // masked).
 //
+// Binary16 caches (prefill_attn<.., true>): the same tiles, loads and
+// layouts (both formats are 2-byte elements), on v_mfma_f32_32x32x16_f16.
+// The keys and values enter as stored; q (bf16) is converted to binary16
+// after scaling by a power of two 2^sh common to the wavefront that puts the
+// wavefront's largest |q| in [2^14, 2^15), which is exact for every
+// component within a factor 2^31 of it, and the logit scale takes 2^-sh back.
+// The softmax weights enter the value product as binary16 with a 2^7 bias
+// (they are at most 2^8 before it, so at most 2^15 after), which keeps the
+// small ones clear of binary16's subnormal range; the running sum carries the
+// same bias, so the quotient is unchanged.
+//
 // Online softmax in base 2 with a lazy rescale: the running shift m only
 // moves when a tile's maximum exceeds it by more than 8 (log2 units), so the
 // O^T accumulators are rescaled rarely; any shift gives the same quotient
@@ -63,6 +74,8 @@ __device__ __attribute__((aligned(16))) uint32_t g_zero_row[128] = {};
 namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
@@ -80,6 +93,22 @@ __device__ __forceinline__ u32x4_t ld16(const uint16_t *p) {
 __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
   const f32x2_t f = {lo, hi};
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
+}
+
+__device__ __forceinline__ uint32_t pack_f16(float lo, float hi) {
+  const f32x2_t f = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, f16x2_t));
+}
+
+// 32x32x16 MFMA on 2-byte operands: binary16 (F16) or bf16
+template <bool F16>
+__device__ __forceinline__ f32x16_t mfma16(u32x4_t a, u32x4_t b, f32x16_t c) {
+  if constexpr (F16)
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8_t, a),
+                                                  __builtin_bit_cast(f16x8_t, b), c, 0, 0, 0);
+  else
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                   __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
 }
 
 // 16 bytes from global memory into the LDS block of the issuing instruction
@@ -113,7 +142,7 @@ struct Prefill {
   static constexpr int IPW = (NINST + NW - 1) / NW;   // per wave and tile, each of K, V
 };
 
-template <int D, int NW>
+template <int D, int NW, bool F16>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void prefill_attn(const PrefillAttnArgs a) {
   using P = Prefill<D, NW>;
@@ -261,9 +290,41 @@ void prefill_attn(const PrefillAttnArgs a) {
   // logit scale, base 2, with the stored keys' scale (1 but for fp8 caches);
   // uniform, so kept in a scalar register (the 256-channel kernel has no
   // vector register to spare for it)
-  const float c2 = __builtin_bit_cast(
+  float c2 = __builtin_bit_cast(
       float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, a.scale_log2 * hd.k_scale)));
+  if constexpr (F16) {
+    // q to binary16 under the wavefront's power of two 2^sh; c2 takes 2^-sh
+    // (sh is capped so that c2 stays a normal number)
+    float mx = 0.0f;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float x0 = __builtin_bit_cast(float, qv[ks][j] << 16);
+        const float x1 = __builtin_bit_cast(float, qv[ks][j] & 0xffff0000u);
+        mx = fmaxf(mx, fmaxf(fabsf(x0), fabsf(x1)));
+      }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+    mx = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, mx)));
+    int ex, ec;
+    (void)frexpf(mx, &ex);                      // mx in [2^(ex-1), 2^ex)
+    (void)frexpf(c2, &ec);
+    int sh = mx > 0.0f ? 15 - ex : 0;
+    sh = min(sh, ec + 120);
+    sh = __builtin_amdgcn_readfirstlane(sh);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float x0 = __builtin_bit_cast(float, qv[ks][j] << 16);
+        const float x1 = __builtin_bit_cast(float, qv[ks][j] & 0xffff0000u);
+        qv[ks][j] = pack_f16(ldexpf(x0, sh), ldexpf(x1, sh));
+      }
+    c2 = ldexpf(c2, -sh);
+  }
   const float tau = 8.0f / c2;                  // lazy-rescale slack (raw units)
+  constexpr float pbias = F16 ? 7.0f : 0.0f;    // log2 of the weights' bias
   float m = -1e30f;                              // running shift (raw units)
   float l = 0.0f;                                // this lane's partial sum
   f32x16_t o[DB];
@@ -303,8 +364,7 @@ void prefill_attn(const PrefillAttnArgs a) {
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       const u32x4_t kx = *reinterpret_cast<const u32x4_t *>(kl + ks * 1024);
-      st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-          __builtin_bit_cast(bf16x8_t, kx), __builtin_bit_cast(bf16x8_t, qv[ks]), st, 0, 0, 0);
+      st = mfma16<F16>(kx, qv[ks], st);
     }
     const bool full_vis = s0 + kKeys <= se && slast <= t_lo &&
                           (W == 0 || slast < S || s0 >= t_hi + 1 - W);
@@ -340,7 +400,7 @@ void prefill_attn(const PrefillAttnArgs a) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
     }
-    const float mc = m * c2;
+    const float mc = m * c2 - pbias;
     float pr[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
@@ -351,7 +411,9 @@ void prefill_attn(const PrefillAttnArgs a) {
 #pragma unroll
     for (int s = 0; s < 2; ++s)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) pb[s][j] = pack_bf16(pr[8 * s + 2 * j], pr[8 * s + 2 * j + 1]);
+      for (int j = 0; j < 4; ++j)
+        pb[s][j] = F16 ? pack_f16(pr[8 * s + 2 * j], pr[8 * s + 2 * j + 1])
+                       : pack_bf16(pr[8 * s + 2 * j], pr[8 * s + 2 * j + 1]);
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
 #pragma unroll
@@ -361,10 +423,9 @@ void prefill_attn(const PrefillAttnArgs a) {
         for (int hh = 0; hh < 2; ++hh)
           v2[hh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
               (lds_i16x4_t *)(vl + 2 * db * P::VPAIR + (16 * s + 8 * hh) * 16));
-        const bf16x8_t va = __builtin_bit_cast(
-            bf16x8_t, __builtin_shufflevector(v2[0], v2[1], 0, 1, 2, 3, 4, 5, 6, 7));
-        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            va, __builtin_bit_cast(bf16x8_t, pb[s]), o[db], 0, 0, 0);
+        const u32x4_t va = __builtin_bit_cast(
+            u32x4_t, __builtin_shufflevector(v2[0], v2[1], 0, 1, 2, 3, 4, 5, 6, 7));
+        o[db] = mfma16<F16>(va, pb[s], o[db]);
       }
     }
   }
@@ -697,15 +758,18 @@ void replay_attn(const ReplayAttnArgs a) {
 
 int prefill_attn_columns_per_block() { return 32 * kPrefillWaves; }
 
-hipError_t launch_prefill_attn(int D, const PrefillAttnArgs &a, hipStream_t s) {
+hipError_t launch_prefill_attn(int D, bool f16, const PrefillAttnArgs &a, hipStream_t s) {
   const dim3 grid((unsigned)(a.n_col_blocks * a.n_kv_heads));
   const dim3 block(kPrefillWaves * 64);
+#define HWKV_PA(DD, FF) \
+  hipLaunchKernelGGL((prefill_attn<DD, kPrefillWaves, FF>), grid, block, 0, s, a)
   switch (D) {
-    case 64: hipLaunchKernelGGL((prefill_attn<64, kPrefillWaves>), grid, block, 0, s, a); break;
-    case 128: hipLaunchKernelGGL((prefill_attn<128, kPrefillWaves>), grid, block, 0, s, a); break;
-    case 256: hipLaunchKernelGGL((prefill_attn<256, kPrefillWaves>), grid, block, 0, s, a); break;
+    case 64: if (f16) HWKV_PA(64, true); else HWKV_PA(64, false); break;
+    case 128: if (f16) HWKV_PA(128, true); else HWKV_PA(128, false); break;
+    case 256: if (f16) HWKV_PA(256, true); else HWKV_PA(256, false); break;
     default: return hipErrorInvalidValue;
   }
+#undef HWKV_PA
   return hipGetLastError();
 }
 

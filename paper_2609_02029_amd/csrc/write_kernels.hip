@@ -178,9 +178,9 @@ __global__ __launch_bounds__(256) void stage_units(StageArgs a) {
   }
 }
 
-// The chunk's own K and V as the fp8 cache will store them (code(x / s) of
-// the unit's scale), widened to bf16 code values.
-template <int D>
+// The chunk's own K and V as the cache will store them: fp8 codes (code(x /
+// s) of the unit's scale) widened to bf16 code values, or binary16 values.
+template <int D, int F>
 __global__ __launch_bounds__(256) void stage_chunk(StageChunkArgs a) {
   constexpr int NC = D / 8;
   for (int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x; c < a.n_chunks;
@@ -188,10 +188,15 @@ __global__ __launch_bounds__(256) void stage_chunk(StageChunkArgs a) {
     const int h = (int)((c / NC) % a.n_kv_heads);
     const uint4 k = *reinterpret_cast<const uint4 *>(a.k + c * 8);
     const uint4 v = *reinterpret_cast<const uint4 *>(a.v + c * 8);
-    *reinterpret_cast<uint4 *>(a.k_out + c * 8) =
-        widen_fp8x8(encode8<HWKV_KV_FP8_E4M3>(k, a.k_scale[h]));
-    *reinterpret_cast<uint4 *>(a.v_out + c * 8) =
-        widen_fp8x8(encode8<HWKV_KV_FP8_E4M3>(v, a.v_scale[h]));
+    if constexpr (F == HWKV_KV_F16) {
+      *reinterpret_cast<uint4 *>(a.k_out + c * 8) = encode8<HWKV_KV_F16>(k, 1.0f);
+      *reinterpret_cast<uint4 *>(a.v_out + c * 8) = encode8<HWKV_KV_F16>(v, 1.0f);
+    } else {
+      *reinterpret_cast<uint4 *>(a.k_out + c * 8) =
+          widen_fp8x8(encode8<HWKV_KV_FP8_E4M3>(k, a.k_scale[h]));
+      *reinterpret_cast<uint4 *>(a.v_out + c * 8) =
+          widen_fp8x8(encode8<HWKV_KV_FP8_E4M3>(v, a.v_scale[h]));
+    }
   }
 }
 
@@ -257,12 +262,19 @@ hipError_t launch_stage_units(int D, const StageArgs &a, hipStream_t s) {
 
 hipError_t launch_stage_chunk(int D, const StageChunkArgs &a, hipStream_t s) {
   const dim3 grid((unsigned)std::max<int64_t>(1, std::min<int64_t>((a.n_chunks + 255) / 256, 4096)));
+  if (a.fmt != HWKV_KV_F16 && a.fmt != HWKV_KV_FP8_E4M3) return hipErrorInvalidValue;
+#define HWKV_SC(DD)                                                                   \
+  if (a.fmt == HWKV_KV_F16)                                                           \
+    hipLaunchKernelGGL((stage_chunk<DD, HWKV_KV_F16>), grid, dim3(256), 0, s, a);     \
+  else                                                                                \
+    hipLaunchKernelGGL((stage_chunk<DD, HWKV_KV_FP8_E4M3>), grid, dim3(256), 0, s, a)
   switch (D) {
-    case 64: hipLaunchKernelGGL(stage_chunk<64>, grid, dim3(256), 0, s, a); break;
-    case 128: hipLaunchKernelGGL(stage_chunk<128>, grid, dim3(256), 0, s, a); break;
-    case 256: hipLaunchKernelGGL(stage_chunk<256>, grid, dim3(256), 0, s, a); break;
+    case 64: HWKV_SC(64); break;
+    case 128: HWKV_SC(128); break;
+    case 256: HWKV_SC(256); break;
     default: return hipErrorInvalidValue;
   }
+#undef HWKV_SC
   return hipGetLastError();
 }
 

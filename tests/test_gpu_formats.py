@@ -184,27 +184,59 @@ def test_fp8_cache_rejects_prefill_attention():
 # ---------------------------------------------------------------------------
 @pytest.mark.timeout(1200)
 def test_fp8_ctx112k_workload_full_size():
+    """Residency of all 64 units (stored codes, bit-exact) after prefill and
+    after the last step; outputs of every layer and query head at steps 0, 1,
+    63, 126 and 127 against the oracle over the stored values."""
     import workloads as W
     from hwkv_harness import timed
     cfg = W.CONFIGS["ctx112k"]
-    track = [0, 15]
     sc = W.fp8_scales(cfg)
-    r = Run(cfg, track=track, device_gen=True, kv_format="fp8", k_scale=sc, v_scale=sc)
-    with timed("fp8 ctx112k prefill"):
+    r = Run(cfg, device_gen=True, kv_format="fp8", k_scale=sc, v_scale=sc)
+    _full_size_run(r, cfg, "fp8 ctx112k", {0, 1, 63, 126, 127}, timed)
+
+
+@pytest.mark.timeout(1200)
+def test_f16_ctx112k_workload_full_size():
+    """The same workload in binary16: every layer's residency after prefill
+    and at the end, every layer's outputs at steps 0, 1, 63, 126 and 127."""
+    import workloads as W
+    from hwkv_harness import timed
+    cfg = W.CONFIGS["ctx112k"]
+    r = Run(cfg, device_gen=True, kv_format="f16")
+    _full_size_run(r, cfg, "f16 ctx112k", {0, 1, 63, 126, 127}, timed)
+
+
+@pytest.mark.timeout(900)
+def test_f16_ctx32k_workload():
+    """The 32K workload (d = 256, GQA 6, outlier channels) in binary16: all
+    256 steps, outputs at 34 seeded steps, residency after prefill and at the
+    end."""
+    import workloads as W
+    from hwkv_harness import timed
+    cfg = W.CONFIGS["ctx32k"]
+    check = set(W.rng(cfg["seed"], 0, W.SAMPLE, 0).choice(cfg["steps"], size=32,
+                                                          replace=False).tolist())
+    check |= {0, cfg["steps"] - 1}
+    r = Run(cfg, kv_format="f16")
+    _full_size_run(r, cfg, "f16 ctx32k", check, timed)
+
+
+def _full_size_run(r, cfg, what, sample, timed):
+    with timed(f"{what} prefill + residency"):
         for l in range(cfg["n_layers"]):
             r.prefill(l, 0)
-            if l in track:
-                r.check_layer(l)
+            r.check_layer(l)
     worst = 0.0
-    with timed("fp8 ctx112k 128 steps x 16 layers"):
+    with timed(f"{what} {cfg['steps']} steps x {cfg['n_layers']} layers"):
         for st in range(cfg["steps"]):
             for l in range(cfg["n_layers"]):
                 qa, out = r.step(l)
-                if st in (0, cfg["steps"] - 1) and l in track:
-                    worst = max(worst, r.check_out(l, qa, out, f"fp8 ctx112k layer {l} step {st}"))
-    for l in track:
-        r.check_layer(l)
-    log(f"fp8 ctx112k: max rel err {worst:.3e}")
+                if st in sample:
+                    worst = max(worst, r.check_out(l, qa, out, f"{what} layer {l} step {st}"))
+    with timed(f"{what} final residency"):
+        for l in range(cfg["n_layers"]):
+            r.check_layer(l)
+    log(f"{what}: max rel err {worst:.3e}")
     r.free()
 
 
@@ -212,9 +244,15 @@ def test_fp8_ctx112k_workload_full_size():
 # prefill attention over an fp8 cache: keys below the chunk as stored, the
 # chunk's own as the cache will store them (hwkv_prefill_attn_ws)
 # ---------------------------------------------------------------------------
+# rounding of the softmax weights where they enter the value product: bf16
+# (fp8 caches, staged to bf16 code values) or binary16 (binary16 caches)
+WEIGHT_ROUND = {"fp8": 2.0 ** -8, "f16": 2.0 ** -11}
+
+
 def _check_stored_rows(r, layer, b, rows, q_rows, out, what):
-    """The 1e-2 row bar, and per channel the bound of the bf16 weights:
-    |o - ref| <= (2^-8 + 2e-5) max |v| over the row's retained stored values."""
+    """The 1e-2 row bar, and per channel the bound of the rounded weights:
+    |o - ref| <= (u + 2e-5) max |v| over the row's retained stored values,
+    u = 2^-8 for bf16 weights (fp8 caches), 2^-11 for binary16 ones."""
     from hwkv_harness import REL_TOL, rel_err
     torch.cuda.synchronize()
     rows = np.asarray(rows, dtype=np.int64)
@@ -230,25 +268,59 @@ def _check_stored_rows(r, layer, b, rows, q_rows, out, what):
             pos = KF.retained_positions(int(t), r.S, r.windows[layer][h])
             vb[i, h] = np.abs(vv[pos, h]).max(axis=0)
     vb = np.repeat(vb, r.G, axis=1)
-    ratio = float((np.abs(got - ref) / ((2.0 ** -8 + 2e-5) * vb)).max())
+    ratio = float((np.abs(got - ref) / ((WEIGHT_ROUND[r.kv_format] + 2e-5) * vb)).max())
     assert ratio <= 1.0, f"{what}: error {ratio:.3f} x the weight-rounding bound"
     return e, ratio
 
 
+@pytest.mark.parametrize("fmt", ["fp8", "f16"])
 @pytest.mark.parametrize("paged", [False, True])
-@pytest.mark.parametrize("D,G,S,w", [(64, 4, 4, 150), (256, 6, 3, 40), (128, 8, 0, 700)])
-def test_fp8_prefill_attention(paged, D, G, S, w):
+@pytest.mark.parametrize("D,G,S,w", [(64, 4, 4, 150), (256, 6, 3, 40), (128, 8, 0, 700),
+                                     (128, 1, 2, 33), (64, 2, 4, 31)])
+def test_stored_format_prefill_attention(fmt, paged, D, G, S, w):
+    """Prefill attention over an fp8 or binary16 cache, chunked (1, 100,
+    333 and 512 tokens from 0): every row against the oracle over the stored
+    values, the residency bit-exact, then decode from the materialised cache."""
     cfg = mini(head_dim=D, n_q_heads=2 * G, n_sinks=S, level_windows=[w, 0], prompt=[700],
                max_ctx=800, seed=35)
-    r = Run(cfg, n_pages=8 if paged else None, **fmt_args("fp8", 0.013, 0.009, 1, 2))
+    r = Run(cfg, n_pages=8 if paged else None, **fmt_args(fmt, 0.013, 0.009, 1, 2))
     q, qh, out = r.prefill_with_attn(0, 0, chunks=[1, 100, 333, 512])
     rows = np.arange(700)
-    e, ratio = _check_stored_rows(r, 0, 0, rows, qh[rows], out, f"paged={paged} D={D} G={G}")
+    e, ratio = _check_stored_rows(r, 0, 0, rows, qh[rows], out,
+                                  f"{fmt} paged={paged} D={D} G={G}")
     r.check_layer(0)
     for st in range(2):            # decode continues from the materialised cache
         qa, o = r.step(0, fused=bool(st))
         r.check_out(0, qa, o, f"step {st}")
-    log(f"fp8 prefill paged={paged} D={D} G={G}: max rel err {e:.3e}, {ratio:.3f} of the bound")
+    log(f"{fmt} prefill paged={paged} D={D} G={G}: max rel err {e:.3e}, "
+        f"{ratio:.3f} of the bound")
+    r.free()
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("paged", [False, True])
+def test_f16_prefill_attention_16k(paged):
+    """A 16K-token prompt over a binary16 cache in ragged chunks (head_dim
+    128, 6 q heads per kv head, windows 1024 and full, 4 sinks): 384 sampled
+    rows, the chunk edges among them, against the oracle over the stored
+    values; residency bit-exact; decode continues from the cache."""
+    import workloads as W
+    N = 16384 + 77
+    cuts = [1, 515, 4096, 8192 + 3, 12000]
+    cfg = mini(head_dim=128, n_q_heads=12, n_kv_heads=2, n_sinks=4, level_windows=[1024, 0],
+               prompt=[N], max_ctx=N + 64, seed=37)
+    r = Run(cfg, n_pages=(N + 64 + 255) // 256 + 1 if paged else None, kv_format="f16")
+    q, qh, out = r.prefill_with_attn(0, 0, chunks=cuts)
+    pick = W.rng(37, 0, W.SAMPLE, 0).choice(N, size=384 - 2 * len(cuts) - 2, replace=False)
+    edges = [c + d for c in cuts for d in (-1, 0)] + [0, N - 1]
+    rows = np.unique(np.concatenate([pick, np.asarray(edges)]))
+    e, ratio = _check_stored_rows(r, 0, 0, rows, qh[rows], out, f"f16 16k paged={paged}")
+    r.check_layer(0)
+    for st in range(2):
+        qa, o = r.step(0, fused=bool(st))
+        r.check_out(0, qa, o, f"step {st}")
+    log(f"f16 prefill 16k paged={paged}: {len(rows)} rows, max rel err {e:.3e}, "
+        f"{ratio:.3f} of the bound")
     r.free()
 
 
@@ -258,23 +330,23 @@ def test_prefill_attention_ws_errors_and_bf16_equivalence():
     kv = torch.zeros((4, 2, 64), dtype=torch.bfloat16, device=dev)
     out = torch.zeros((4, 8, 64), dtype=torch.float32, device=dev)
     pol = hwkv.policy_set(1, 2, 8, 64, 4, [256, 0], [[0, 1]])
-    # binary16: not bf16 values, rejected with or without a workspace
-    c16 = hwkv.cache_alloc(pol, 1, 400, kv_format="f16")
-    ws = torch.zeros(1 << 20, dtype=torch.uint8, device=dev)
-    with pytest.raises(hwkv.HwkvError) as e:
-        hwkv.prefill_attn(c16, 0, 0, 0, q, kv, kv, 0.125, out, ws=ws)
-    assert e.value.code == hwkv.EINVAL
-    c16.free()
-    # fp8: a short workspace is EINVAL and changes nothing
-    c8 = hwkv.cache_alloc(pol, 1, 400, kv_format="fp8")
-    need = hwkv.prefill_attn_workspace_bytes(c8, 4)
-    assert need > 0
-    short = torch.zeros(need - 1, dtype=torch.uint8, device=dev)
-    with pytest.raises(hwkv.HwkvError) as e:
-        hwkv.prefill_attn(c8, 0, 0, 0, q, kv, kv, 0.125, out, ws=short)
-    assert e.value.code == hwkv.EINVAL
-    assert hwkv.cache_seq_len(c8, 0, 0) == 0
-    c8.free()
+    # fp8 and binary16: no workspace (the plain entry) or a short one is
+    # EINVAL and changes nothing; binary16 needs the chunk's K and V only
+    for fmt in ("fp8", "f16"):
+        c = hwkv.cache_alloc(pol, 1, 400, kv_format=fmt)
+        need = hwkv.prefill_attn_workspace_bytes(c, 4)
+        if fmt == "f16":
+            assert need == 2 * 4 * 2 * 64 * 2
+        assert need > 0
+        with pytest.raises(hwkv.HwkvError) as e:
+            hwkv.prefill_attn(c, 0, 0, 0, q, kv, kv, 0.125, out)
+        assert e.value.code == hwkv.EINVAL
+        short = torch.zeros(need - 1, dtype=torch.uint8, device=dev)
+        with pytest.raises(hwkv.HwkvError) as e:
+            hwkv.prefill_attn(c, 0, 0, 0, q, kv, kv, 0.125, out, ws=short)
+        assert e.value.code == hwkv.EINVAL
+        assert hwkv.cache_seq_len(c, 0, 0) == 0
+        c.free()
     # bf16: the workspace path is the plain path, bit for bit
     cfg = mini(head_dim=128, n_q_heads=12, level_windows=[90, 0], prompt=[300], seed=36)
     a, b = Run(cfg), Run(cfg)

@@ -21,7 +21,7 @@ import pytest
 import torch
 
 import workloads as W
-from hwkv_harness import REL_TOL, Run, log, rel_err, timed
+from hwkv_harness import REL_TOL, Run, log, rel_err, retained_absmax, timed
 from paper_2609_02029_amd import hwkv
 
 pytestmark = pytest.mark.gpu
@@ -47,21 +47,12 @@ P_ROUND = 2.0 ** -8 + 2e-5   # bf16 rounding of the weights, plus fp32 slack
 
 def vmax_bound(r, layer, b, rows):
     """[rows, Hkv, D]: max |v| per channel over each row's retained keys
-    (over all keys up to the row when the history is long)."""
-    vh = W.bf16_bits_to_f32(r.vh[layer][b][: int(rows[-1]) + 1])   # [n, Hkv, D]
-    av = np.abs(vh)
+    (its head's window), at every size."""
+    av = np.abs(W.bf16_bits_to_f32(r.vh[layer][b][: int(rows[-1]) + 1]))   # [n, Hkv, D]
     out = np.empty((len(rows), r.Hkv, r.D), dtype=np.float64)
-    if rows[-1] >= 8192:
-        out[:] = av.max(axis=0)[None]
-        return out
-    pos = np.arange(av.shape[0])
     for i, t in enumerate(rows):
         for h in range(r.Hkv):
-            w = r.windows[layer][h]
-            keep = pos <= t
-            if w:
-                keep &= (pos < r.S) | (pos >= t + 1 - w)
-            out[i, h] = av[keep, h].max(axis=0)
+            out[i, h] = retained_absmax(av[:, h], int(t), r.windows[layer][h], r.S)
     return out
 
 

@@ -25,11 +25,11 @@ SCRATCH_ALLOWED = {
 
 
 def _demangle(name):
-    m = re.search(r"(\w+?)I((?:Li-?\d+E)+)E", name)
+    m = re.search(r"(\w+?)I((?:L[ib]-?\d+E)+)E", name)
     if not m:
         return re.sub(r"^_ZN4hwkv12_GLOBAL__N_1\d+", "", name)
     base = re.sub(r"^.*\d", "", re.sub(r"^_ZN4hwkv12_GLOBAL__N_1", "", m.group(1)))
-    args = re.findall(r"Li(-?\d+)E", m.group(2))
+    args = re.findall(r"L[ib](-?\d+)E", m.group(2))   # int and bool arguments
     return f"{base}<{', '.join(args)}>"
 
 
@@ -74,7 +74,9 @@ def kernel_table(tmp_path_factory):
 
 def test_every_hot_kernel_is_present(kernel_table):
     for name in ["decode_split<256, 6, 0>", "decode_split<256, 6, 2>", "decode_split<256, 6, 1>",
-                 "decode_split<256, 8, 0>", "decode_split<64, 1, 0>", "prefill_attn<256, 8>", "prefill_attn<128, 8>", "prefill_attn<64, 8>",
+                 "decode_split<256, 8, 0>", "decode_split<64, 1, 0>",
+                 "prefill_attn<256, 8, 0>", "prefill_attn<128, 8, 0>", "prefill_attn<64, 8, 0>",
+                 "prefill_attn<256, 8, 1>", "prefill_attn<128, 8, 1>", "prefill_attn<64, 8, 1>",
                  "replay_attn<256, 8>", "replay_merge<256>", "prefill_write<256, 0>",
                  "append_token<256, 2>"]:
         assert name in kernel_table, sorted(kernel_table)
