@@ -306,30 +306,48 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
 
   const DecodeItems &it = a.it;
   const int blk = blockIdx.x;
-  int lo = 0, hi = it.n_items - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (it.split_begin[mid] <= blk)
-      lo = mid;
-    else
-      hi = mid - 1;
-  }
-  const int item = lo;
-  const int j = blk - it.split_begin[item];               // workgroup of the item
-  const int nwg = it.split_begin[item + 1] - it.split_begin[item];
-  const int nv = it.n_valid[item];
-  const int new_slot = it.new_slot[item];
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
+  // The item and its fields in one round of independent loads, lane i
+  // reading item i's (entries of split_begin past the launch's items hold
+  // INT32_MAX): the item is the number of items that begin at or before
+  // this workgroup, less one, and its fields are read from its lane.  (A
+  // search over split_begin would be a chain of dependent loads before the
+  // first tile load of every workgroup.)
+  static_assert(kMaxItems == 64, "one lane per item");
+  const int sb_l = it.split_begin[lane];
+  const int sb1_l = it.split_begin[lane + 1];
+  const int nv_l = it.n_valid[lane];
+  const int ns_l = it.new_slot[lane];
+  const int pto_l = it.pto[lane];
+  const int qrow_l = it.q_row[lane];
+  const int64_t koff_l = it.k_off[lane];
+  const int64_t voff_l = it.v_off[lane];
+  const int item = __builtin_amdgcn_readfirstlane(__popcll(__ballot(sb_l <= blk)) - 1);
+  auto pick = [&](int v) { return __builtin_amdgcn_readlane(v, item); };
+  auto pick64 = [&](int64_t v) {
+    const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)v, item);
+    const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)v >> 32), item);
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+  };
+  const int j = blk - pick(sb_l);                          // workgroup of the item
+  const int nwg = pick(sb1_l) - pick(sb_l);
+  const int nv = pick(nv_l);
+  const int new_slot = pick(ns_l);
+  const int q_row = pick(qrow_l);
   const int c8 = lane % NC;
   const int rsub = lane / NC;
   const int n_tiles = (nv + 63) / 64;
-  const int pto = it.pto[item];
+  const int pto = pick(pto_l);
+  // read out of their lanes here, not under the paged test below (where the
+  // compiler would otherwise move their loads, a second round trip)
+  int64_t koff_i = pick64(koff_l), voff_i = pick64(voff_l);
+  asm volatile("" : "+s"(koff_i), "+s"(voff_i));
   // the item's K tiles and V rows, or the page pool of a paged unit (the
   // offsets are uniform; said so, or the compiler may keep them in vector
   // registers and then fail to feed them to the scalar operands below)
-  const int64_t koff = uniform64(pto >= 0 ? a.pool_off : it.k_off[item]);
-  const int64_t voff = uniform64(pto >= 0 ? a.pool_off + kPageTokens * D : it.v_off[item]);
+  const int64_t koff = uniform64(pto >= 0 ? a.pool_off : koff_i);
+  const int64_t voff = uniform64(pto >= 0 ? a.pool_off + kPageTokens * D : voff_i);
   uint8_t *const kbase = static_cast<uint8_t *>(a.cache) + koff * EB;
   uint8_t *const vbase = static_cast<uint8_t *>(a.cache) + voff * EB;
 
@@ -442,7 +460,7 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
   };
   // q chunk c of head h is qw[h NC + c - wave] (the wave's chunks are
   // c = 4i + wave)
-  const cu32x4_t *const qw = (const cu32x4_t *)(a.q + (size_t)it.q_row[item] * D) + wave;
+  const cu32x4_t *const qw = (const cu32x4_t *)(a.q + (size_t)q_row * D) + wave;
   float *const pl = sm.u.t.p;
 
   int t = j;                     // logical tile
@@ -745,7 +763,7 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
     const float L = sm.l[h];
     if (nwg == 1) {
       const float inv = 1.0f / L;
-      *reinterpret_cast<float4 *>(&a.out[((size_t)it.q_row[item] + h) * D + c]) =
+      *reinterpret_cast<float4 *>(&a.out[((size_t)q_row + h) * D + c]) =
           make_float4(A.x * inv, A.y * inv, A.z * inv, A.w * inv);
     } else {
       *reinterpret_cast<float4 *>(&a.part_acc[((size_t)pidx * G + h) * D + c]) = A;

@@ -623,6 +623,9 @@ int decode_impl(hwkv_cache *c, int32_t layer, const void *k_new,
       splits += nwg[i];
     }
     a.it.split_begin[cnt] = splits;
+    // entries past the items: no workgroup begins there (the split kernel
+    // counts the items that begin at or before a workgroup)
+    for (int j = cnt + 1; j <= hwkv::kMaxItems; ++j) a.it.split_begin[j] = INT32_MAX;
     a.it.n_items = cnt;
     a.it.ws_split0 = ws_split;
     a.cache = c->base;
