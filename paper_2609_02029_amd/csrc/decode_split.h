@@ -105,6 +105,7 @@ typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
 typedef const __attribute__((address_space(4))) u32x4_t cu32x4_t;
 
@@ -233,7 +234,9 @@ struct SplitSmem {
     float lg[2][G][kWaves][64];     // partial logits (head, wave, slot), by tile parity
     float p[64 * PST];              // the tile's weights (slot, head)
   };
-  union {
+  // separate areas (not a union): the epilogue's writes need no barrier
+  // behind the last tile's reads
+  struct {
     Tile t;                                               // the tile walk
     __attribute__((aligned(16))) float acc[kWaves][G][D];  // epilogue: wave sums
   } u;
@@ -732,7 +735,6 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
   for (int h = 0; h < G; ++h)
 #pragma unroll
     for (int e = 0; e < 4; ++e) red[h][e] = half_sum_pair(acc[h][e], acc[h][e + 4]);
-  __syncthreads();  // every wave is done with the tile buffers that acc reuses
   if ((lane & 31) < NC) {
 #pragma unroll
     for (int h = 0; h < G; ++h)
@@ -761,15 +763,19 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
       A.w *= vsc;
     }
     const float L = sm.l[h];
+    // streaming (non-temporal) stores: nothing here is read again by this
+    // kernel
     if (nwg == 1) {
       const float inv = 1.0f / L;
-      *reinterpret_cast<float4 *>(&a.out[((size_t)q_row + h) * D + c]) =
-          make_float4(A.x * inv, A.y * inv, A.z * inv, A.w * inv);
+      __builtin_nontemporal_store(f32x4_t{A.x * inv, A.y * inv, A.z * inv, A.w * inv},
+                                  reinterpret_cast<f32x4_t *>(&a.out[((size_t)q_row + h) * D + c]));
     } else {
-      *reinterpret_cast<float4 *>(&a.part_acc[((size_t)pidx * G + h) * D + c]) = A;
+      __builtin_nontemporal_store(
+          f32x4_t{A.x, A.y, A.z, A.w},
+          reinterpret_cast<f32x4_t *>(&a.part_acc[((size_t)pidx * G + h) * D + c]));
       if (c == 0)
-        *reinterpret_cast<float2 *>(&a.part_ml[((size_t)pidx * G + h) * 2]) =
-            make_float2(sm.m[h], L);
+        __builtin_nontemporal_store(
+            f32x2_t{sm.m[h], L}, reinterpret_cast<f32x2_t *>(&a.part_ml[((size_t)pidx * G + h) * 2]));
     }
   }
 }
