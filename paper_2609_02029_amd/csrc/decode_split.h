@@ -30,8 +30,10 @@
 //         SGPR operand) with fp32 accumulate; fp8 keys are first widened to
 //         bf16 pairs (exact: every E4M3 value is a bf16 value) and take the
 //         same path, with the K scale folded into the logit scale; binary16
-//         keys meet the fp32-widened q in fp32 FMAs.  Each wave covers a
-//         quarter of the channels; the quarters are summed through LDS.
+//         keys meet q staged in LDS as binary16 (each head under a power of
+//         two that keeps every component within 2^31 of its largest exact)
+//         in v_dot2_f32_f16.  Each wave covers a quarter of the channels;
+//         the quarters are summed through LDS.
 //   softmax  online, base 2 (log2(e) folded into the scale); the tile max is
 //         one DPP row reduction plus four lane reads per head.
 //   p.v   lanes own 8 channels of one row (V row-major, a wave reads whole
@@ -91,13 +93,10 @@ constexpr int kPrefetch = HWKV_DECODE_PREFETCH;  // 16-byte loads in flight
 constexpr int kPrefetch8 = HWKV_DECODE_PREFETCH8;  // 8-byte loads in flight
 // VGPR budget: four waves per SIMD (four workgroups per CU); eight q heads
 // per KV head (64 value accumulators per lane), and six with binary16 keys
-// at head_dim 128 and 256 (whose q.k widens the keys and q), need the
-// budget of three, and eight with binary16 keys at head_dim 128 and 256
-// the budget of two
+// at head_dim 256, need the budget of three
 constexpr int split_waves_per_eu(int D, int G, int F) {
   if (HWKV_DECODE_MINWAVES <= 2) return HWKV_DECODE_MINWAVES;
-  if (F == HWKV_KV_F16 && G == 8 && D >= 128) return HWKV_DECODE_MINWAVES - 2;
-  return (G == 8 || (F == HWKV_KV_F16 && G == 6 && D >= 128)) ? HWKV_DECODE_MINWAVES - 1
+  return (G == 8 || (F == HWKV_KV_F16 && G == 6 && D >= 256)) ? HWKV_DECODE_MINWAVES - 1
                                                               : HWKV_DECODE_MINWAVES;
 }
 
@@ -107,6 +106,7 @@ typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef const __attribute__((address_space(4))) u32x4_t cu32x4_t;
 
 __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
@@ -227,7 +227,7 @@ __device__ __forceinline__ float wave_sum(float v) {
          (lane_read(v, 32) + lane_read(v, 48));
 }
 
-template <int D, int G>
+template <int D, int G, int F>
 struct SplitSmem {
   static constexpr int PST = (G + 3) & ~3;  // weights per slot (fp32), 16-byte rows
   struct Tile {
@@ -242,6 +242,10 @@ struct SplitSmem {
   } u;
   float alpha[G];                   // the tile's rescale of each head's sums
   float m[G], l[G];                 // the workgroup's shift and normaliser
+  // binary16 keys: the item's q as binary16 pairs (head-major), and each
+  // head's logit scale
+  __attribute__((aligned(16))) uint32_t q16[F == HWKV_KV_F16 ? G * D / 2 : 4];
+  float qsc[G];
 };
 
 // x of lane l and x of lane l ^ 32 for two values at once (VALU lane swap):
@@ -296,7 +300,7 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
   // loads in flight per lane; the ring slot of a load is its piece number
   // mod PF, the same in every tile
   constexpr int PF = PFW < PIECES ? PFW : PIECES;
-  constexpr int PST = SplitSmem<D, G>::PST;
+  constexpr int PST = SplitSmem<D, G, F>::PST;
   // fp8 values: p.v over pairs of a wave's V steps with v_dot2_f32_f16 --
   // steps 4(2i) + w and 4(2i + 1) + w read rows r and r + 4 RPS of the same
   // channels, whose codes widen exactly to binary16 pairs; the weights enter
@@ -305,7 +309,7 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
   static_assert(NC % kWaves == 0, "the four waves share a tile's chunks");
   static_assert(PIECES % PF == 0, "ring slots repeat from tile to tile");
   static_assert(!PAIR || NCW % 2 == 0, "fp8 p.v takes a wave's V steps in pairs");
-  __shared__ SplitSmem<D, G> sm;
+  __shared__ SplitSmem<D, G, F> sm;
 
   const DecodeItems &it = a.it;
   const int blk = blockIdx.x;
@@ -432,6 +436,46 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
   for (int h = 0; h < G; ++h)
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
+  // binary16 keys: q goes to LDS as binary16, head h scaled by the power of
+  // two 2^sh that puts its largest |q| in [2^14, 2^15), so that every
+  // component within a factor 2^31 of it converts exactly; the head's logit
+  // scale takes 2^-sh back (sh is capped so that the scale stays normal).
+  // The keys' binary16 pairs then meet q in v_dot2_f32_f16 (exact products,
+  // fp32 sums), as bf16 keys meet q in v_dot2_f32_bf16.
+  // Every wave stages every head and writes the same values (dividing the
+  // heads between the waves makes the compiler fail with an illegal VGPR to
+  // SGPR copy).
+  if constexpr (F == HWKV_KV_F16) {
+    int ez;
+    (void)frexpf(a.scale_log2, &ez);
+    for (int h = 0; h < G; ++h) {
+      const uint16_t *qh = a.q + ((size_t)q_row + h) * D;
+      uint2 w[(D + 255) / 256];
+      float mx = 0.0f;
+#pragma unroll
+      for (int r = 0; r < (D + 255) / 256; ++r) {
+        const int c = 256 * r + 4 * lane;
+        w[r] = c < D ? *reinterpret_cast<const uint2 *>(qh + c) : make_uint2(0u, 0u);
+        mx = fmaxf(mx, fmaxf(fmaxf(fabsf(bf_lo(w[r].x)), fabsf(bf_hi(w[r].x))),
+                             fmaxf(fabsf(bf_lo(w[r].y)), fabsf(bf_hi(w[r].y)))));
+      }
+      mx = wave_max(mx);
+      int ex;
+      (void)frexpf(mx, &ex);               // mx in [2^(ex-1), 2^ex)
+      const int sh = __builtin_amdgcn_readfirstlane(min(mx > 0.0f ? 15 - ex : 0, ez + 120));
+#pragma unroll
+      for (int r = 0; r < (D + 255) / 256; ++r) {
+        const int c = 256 * r + 4 * lane;
+        if (c < D) {
+          const f16x2_t lo = {(_Float16)ldexpf(bf_lo(w[r].x), sh), (_Float16)ldexpf(bf_hi(w[r].x), sh)};
+          const f16x2_t hi = {(_Float16)ldexpf(bf_lo(w[r].y), sh), (_Float16)ldexpf(bf_hi(w[r].y), sh)};
+          *reinterpret_cast<uint2 *>(&sm.q16[(h * D + c) / 2]) =
+              make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
+        }
+      }
+      if (lane == 0) sm.qsc[h] = ldexpf(a.scale_log2, -sh);
+    }
+  }
   // Only this workgroup reads the new slot in this launch: a workgroup-scope
   // release/acquire around the barrier orders the store before its loads
   // (agent scope would write back and invalidate the whole L2).
@@ -439,9 +483,18 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
   __syncthreads();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 
-  // logit scale (base 2), with the fp8 K scale folded in
+  // logit scale (base 2), with the fp8 K scale folded in; binary16 keys: the
+  // scale of each head the wave owns, with its q shift taken back
   const float zscale =
       F == HWKV_KV_FP8_E4M3 ? a.scale_log2 * it.k_scale[item] : a.scale_log2;
+  float zsc[OWN];
+#pragma unroll
+  for (int o = 0; o < OWN; ++o) {
+    const int h = min(wave + kWaves * o, G - 1);
+    zsc[o] = F == HWKV_KV_F16 ? __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(
+                                                               __builtin_bit_cast(int, sm.qsc[h])))
+                              : zscale;
+  }
   // per-lane parts of the piece addresses (the step is in soffset)
   const int kl = lane * LB;                    // K: lane = slot
   const int vl = rsub * D * EB + c8 * LB;      // V: row rsub of the step, 8 channels
@@ -522,7 +575,7 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
       const Chunk x = buf[q % PF];
       issue(jc);
       const cu32x4_t *qj = (const cu32x4_t *)qaddr;
-      if constexpr (!QAHEAD) {
+      if constexpr (!QAHEAD && F != HWKV_KV_F16) {
 #pragma unroll
         for (int h = 0; h < G; ++h) qc[h] = qj[h * NC + kWaves * q];
       }
@@ -550,18 +603,24 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
           s[h] = dot2(qc[h].w, k3, s[h]);
         }
       } else {
-        float kf[8];
-        widen8<F>(x, kf);
+        // binary16 keys: q chunk (kWaves q + wave) of head h from LDS (one
+        // address for every lane: a broadcast read).  The 16-byte vectors are
+        // reinterpreted whole and split into pairs by shuffles: bit-casting
+        // single elements of the u32x4 vector instead made this toolchain
+        // feed the first element to all four products.
+        const u32x4_t *q16 = reinterpret_cast<const u32x4_t *>(sm.q16) + kWaves * q + wave;
+        const f16x8_t kv = __builtin_bit_cast(f16x8_t, u32x4_t{x.x, x.y, x.z, x.w});
 #pragma unroll
         for (int h = 0; h < G; ++h) {
-          s[h] = fmaf(bf_lo(qc[h].x), kf[0], s[h]);
-          s[h] = fmaf(bf_hi(qc[h].x), kf[1], s[h]);
-          s[h] = fmaf(bf_lo(qc[h].y), kf[2], s[h]);
-          s[h] = fmaf(bf_hi(qc[h].y), kf[3], s[h]);
-          s[h] = fmaf(bf_lo(qc[h].z), kf[4], s[h]);
-          s[h] = fmaf(bf_hi(qc[h].z), kf[5], s[h]);
-          s[h] = fmaf(bf_lo(qc[h].w), kf[6], s[h]);
-          s[h] = fmaf(bf_hi(qc[h].w), kf[7], s[h]);
+          const f16x8_t qv = __builtin_bit_cast(f16x8_t, q16[h * NC]);
+          s[h] = __builtin_amdgcn_fdot2(__builtin_shufflevector(qv, qv, 0, 1),
+                                        __builtin_shufflevector(kv, kv, 0, 1), s[h], false);
+          s[h] = __builtin_amdgcn_fdot2(__builtin_shufflevector(qv, qv, 2, 3),
+                                        __builtin_shufflevector(kv, kv, 2, 3), s[h], false);
+          s[h] = __builtin_amdgcn_fdot2(__builtin_shufflevector(qv, qv, 4, 5),
+                                        __builtin_shufflevector(kv, kv, 4, 5), s[h], false);
+          s[h] = __builtin_amdgcn_fdot2(__builtin_shufflevector(qv, qv, 6, 7),
+                                        __builtin_shufflevector(kv, kv, 6, 7), s[h], false);
         }
       }
       if constexpr (QAHEAD && q + 1 < NCW) {
@@ -593,7 +652,7 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
         float z = 0.f;
 #pragma unroll
         for (int w = 0; w < kWaves; ++w) z += sm.u.t.lg[k & 1][h][w][lane];  // fixed order
-        z = valid ? z * zscale : -INFINITY;
+        z = valid ? z * zsc[o] : -INFINITY;
         const float mnew = fmaxf(m[o], wave_max(z));
         float alpha = 1.0f;
         if (mnew > m[o]) {  // uniform

@@ -91,8 +91,7 @@ def test_no_scratch_spills(kernel_table):
 def test_register_budgets(kernel_table):
     # decode splits: four waves per SIMD (128 registers), three (168) for 8 q
     # heads per kv head, whose 64 value accumulators per lane do not fit 128,
-    # and for 6 with binary16 keys at head_dim 128 and 256 (two, 256, for 8
-    # with binary16 keys there);
+    # and for 6 with binary16 keys at head_dim 256;
     # prefill attention: two waves of eight per SIMD (256)
     for n, (vg, _) in kernel_table.items():
         if n.startswith("prefill_attn<"):
@@ -100,8 +99,6 @@ def test_register_budgets(kernel_table):
         if n.startswith("decode_split<"):
             d, g, _f = (int(x) for x in n[n.index("<") + 1:-1].split(","))
             budget = 128
-            if g == 8 or (_f == 1 and g == 6 and d >= 128):
+            if g == 8 or (_f == 1 and g == 6 and d >= 256):
                 budget = 168
-            if _f == 1 and g == 8 and d >= 128:
-                budget = 256
             assert vg <= budget, (n, vg)
