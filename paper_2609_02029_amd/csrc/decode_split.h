@@ -523,6 +523,15 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
   int tp = phys(t);              // its place in the unit
   int pg = page_of(tp);
   __amdgpu_buffer_rsrc_t krs = k_rsrc(tp, pg), vrs = v_rsrc(tp, pg);
+  // q is read through scalar loads during the walk, and a step's q is cold
+  // (in HBM).  One vector load per lane touching its own 64-byte piece of
+  // the item's q, issued with the first tile's loads, brings q's lines into
+  // L2 in the shadow of those loads; the value is only consumed at the end
+  // of the kernel, so nothing waits for it early.  (Binary16 keys stage q
+  // through LDS instead.)
+  uint32_t qtouch = 0;
+  if constexpr (F != HWKV_KV_F16)
+    qtouch = reinterpret_cast<const uint32_t *>(a.q + (size_t)q_row * D)[min(lane * 16, G * D / 2 - 1)];
   Chunk buf[PF];
   static_for<PF>([&](auto jc) { buf[jc.value] = ld(krs, vrs, jc); });
   for (int k = 0;; ++k) {
@@ -837,6 +846,7 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
             f32x2_t{sm.m[h], L}, reinterpret_cast<f32x2_t *>(&a.part_ml[((size_t)pidx * G + h) * 2]));
     }
   }
+  asm volatile("" ::"v"(qtouch));   // the q touch above, consumed
 }
 
 
