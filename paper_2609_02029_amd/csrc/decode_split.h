@@ -436,45 +436,28 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
   for (int h = 0; h < G; ++h)
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
-  // binary16 keys: q goes to LDS as binary16, head h scaled by the power of
-  // two 2^sh that puts its largest |q| in [2^14, 2^15), so that every
-  // component within a factor 2^31 of it converts exactly; the head's logit
-  // scale takes 2^-sh back (sh is capped so that the scale stays normal).
-  // The keys' binary16 pairs then meet q in v_dot2_f32_f16 (exact products,
-  // fp32 sums), as bf16 keys meet q in v_dot2_f32_bf16.
-  // Every wave stages every head and writes the same values (dividing the
-  // heads between the waves makes the compiler fail with an illegal VGPR to
-  // SGPR copy).
+  // the first tile (its page entry is read before q, so that waiting for it
+  // does not wait for q)
+  int t = j;                     // logical tile
+  int tp = phys(t);              // its place in the unit
+  int pg = page_of(tp);
+  // binary16 keys: every head's q in one round of loads, issued before the
+  // first tile's loads (a step's q is cold; its conversion below then waits
+  // for q alone, not for the tile).  Buffer loads: with plain loads here the
+  // compiler fails with an illegal VGPR to SGPR copy.  Lanes past D read the
+  // head's last four values again (D = 64, 128), which leaves its max as is.
+  constexpr int QR = (D + 255) / 256;
+  uint2 w[F == HWKV_KV_F16 ? G : 1][QR];
   if constexpr (F == HWKV_KV_F16) {
-    int ez;
-    (void)frexpf(a.scale_log2, &ez);
-    for (int h = 0; h < G; ++h) {
-      const uint16_t *qh = a.q + ((size_t)q_row + h) * D;
-      uint2 w[(D + 255) / 256];
-      float mx = 0.0f;
+    const __amdgpu_buffer_rsrc_t qr = make_rsrc(a.q + (size_t)q_row * D, (uint32_t)(G * D * 2));
 #pragma unroll
-      for (int r = 0; r < (D + 255) / 256; ++r) {
-        const int c = 256 * r + 4 * lane;
-        w[r] = c < D ? *reinterpret_cast<const uint2 *>(qh + c) : make_uint2(0u, 0u);
-        mx = fmaxf(mx, fmaxf(fmaxf(fabsf(bf_lo(w[r].x)), fabsf(bf_hi(w[r].x))),
-                             fmaxf(fabsf(bf_lo(w[r].y)), fabsf(bf_hi(w[r].y)))));
-      }
-      mx = wave_max(mx);
-      int ex;
-      (void)frexpf(mx, &ex);               // mx in [2^(ex-1), 2^ex)
-      const int sh = __builtin_amdgcn_readfirstlane(min(mx > 0.0f ? 15 - ex : 0, ez + 120));
+    for (int h = 0; h < G; ++h)
 #pragma unroll
-      for (int r = 0; r < (D + 255) / 256; ++r) {
-        const int c = 256 * r + 4 * lane;
-        if (c < D) {
-          const f16x2_t lo = {(_Float16)ldexpf(bf_lo(w[r].x), sh), (_Float16)ldexpf(bf_hi(w[r].x), sh)};
-          const f16x2_t hi = {(_Float16)ldexpf(bf_lo(w[r].y), sh), (_Float16)ldexpf(bf_hi(w[r].y), sh)};
-          *reinterpret_cast<uint2 *>(&sm.q16[(h * D + c) / 2]) =
-              make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
-        }
+      for (int r = 0; r < QR; ++r) {
+        const int c = min(256 * r + 4 * lane, D - 4);
+        const u32x2_t x = __builtin_amdgcn_raw_buffer_load_b64(qr, (h * D + c) * 2, 0, 0);
+        w[h][r] = make_uint2(x.x, x.y);
       }
-      if (lane == 0) sm.qsc[h] = ldexpf(a.scale_log2, -sh);
-    }
   }
   // Only this workgroup reads the new slot in this launch: a workgroup-scope
   // release/acquire around the barrier orders the store before its loads
@@ -483,18 +466,6 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
   __syncthreads();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 
-  // logit scale (base 2), with the fp8 K scale folded in; binary16 keys: the
-  // scale of each head the wave owns, with its q shift taken back
-  const float zscale =
-      F == HWKV_KV_FP8_E4M3 ? a.scale_log2 * it.k_scale[item] : a.scale_log2;
-  float zsc[OWN];
-#pragma unroll
-  for (int o = 0; o < OWN; ++o) {
-    const int h = min(wave + kWaves * o, G - 1);
-    zsc[o] = F == HWKV_KV_F16 ? __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(
-                                                               __builtin_bit_cast(int, sm.qsc[h])))
-                              : zscale;
-  }
   // per-lane parts of the piece addresses (the step is in soffset)
   const int kl = lane * LB;                    // K: lane = slot
   const int vl = rsub * D * EB + c8 * LB;      // V: row rsub of the step, 8 channels
@@ -519,9 +490,6 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
   const cu32x4_t *const qw = (const cu32x4_t *)(a.q + (size_t)q_row * D) + wave;
   float *const pl = sm.u.t.p;
 
-  int t = j;                     // logical tile
-  int tp = phys(t);              // its place in the unit
-  int pg = page_of(tp);
   __amdgpu_buffer_rsrc_t krs = k_rsrc(tp, pg), vrs = v_rsrc(tp, pg);
   // q is read through scalar loads during the walk, and a step's q is cold
   // (in HBM).  One vector load per lane touching its own 64-byte piece of
@@ -534,6 +502,57 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
     qtouch = reinterpret_cast<const uint32_t *>(a.q + (size_t)q_row * D)[min(lane * 16, G * D / 2 - 1)];
   Chunk buf[PF];
   static_for<PF>([&](auto jc) { buf[jc.value] = ld(krs, vrs, jc); });
+  // binary16 keys: q goes to LDS as binary16, head h scaled by the power of
+  // two 2^sh that puts its largest |q| in [2^14, 2^15), so that every
+  // component within a factor 2^31 of it converts exactly; the head's logit
+  // scale takes 2^-sh back (sh is capped so that the scale stays normal).
+  // The keys' binary16 pairs then meet q in v_dot2_f32_f16 (exact products,
+  // fp32 sums), as bf16 keys meet q in v_dot2_f32_bf16.
+  if constexpr (F == HWKV_KV_F16) {
+    int ez;
+    (void)frexpf(a.scale_log2, &ez);
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      if (h % kWaves != wave) continue;   // wave h % 4 stages head h
+      float mx = 0.0f;
+#pragma unroll
+      for (int r = 0; r < QR; ++r)
+        mx = fmaxf(mx, fmaxf(fmaxf(fabsf(bf_lo(w[h][r].x)), fabsf(bf_hi(w[h][r].x))),
+                             fmaxf(fabsf(bf_lo(w[h][r].y)), fabsf(bf_hi(w[h][r].y)))));
+      mx = wave_max(mx);
+      int ex;
+      (void)frexpf(mx, &ex);               // mx in [2^(ex-1), 2^ex)
+      const int sh = __builtin_amdgcn_readfirstlane(min(mx > 0.0f ? 15 - ex : 0, ez + 120));
+#pragma unroll
+      for (int r = 0; r < QR; ++r) {
+        const int c = 256 * r + 4 * lane;
+        if (c < D) {
+          const uint2 x = w[h][r];
+          const f16x2_t lo = {(_Float16)ldexpf(bf_lo(x.x), sh), (_Float16)ldexpf(bf_hi(x.x), sh)};
+          const f16x2_t hi = {(_Float16)ldexpf(bf_lo(x.y), sh), (_Float16)ldexpf(bf_hi(x.y), sh)};
+          *reinterpret_cast<uint2 *>(&sm.q16[(h * D + c) / 2]) =
+              make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
+        }
+      }
+      if (lane == 0) sm.qsc[h] = ldexpf(a.scale_log2, -sh);
+    }
+    // LDS only: the tile's loads stay in flight across this barrier
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+  }
+  // logit scale (base 2), with the fp8 K scale folded in; binary16 keys: the
+  // scale of each head the wave owns, with its q shift taken back
+  const float zscale =
+      F == HWKV_KV_FP8_E4M3 ? a.scale_log2 * it.k_scale[item] : a.scale_log2;
+  float zsc[OWN];
+#pragma unroll
+  for (int o = 0; o < OWN; ++o) {
+    const int h = min(wave + kWaves * o, G - 1);
+    zsc[o] = F == HWKV_KV_F16 ? __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(
+                                                               __builtin_bit_cast(int, sm.qsc[h])))
+                              : zscale;
+  }
   for (int k = 0;; ++k) {
     const bool has_next = t + nwg < n_tiles;
     // the next tile and its page: its first PF loads are issued during the
