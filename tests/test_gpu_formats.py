@@ -164,6 +164,38 @@ def test_format_batched_ragged(fmt, ks, vs):
     r.free()
 
 
+# Every workgroup walks several tiles: the launch holds far more 64-slot tiles
+# than its workgroups (8 sequences x 2 kv heads, 16K + 4K resident rows: 2,560
+# tiles against at most five workgroups per CU), so each workgroup's load
+# ring runs on from one tile into the next -- at every head dim, group size
+# and format, not only at the benchmark's shape.
+WALK_CASES = [("bf16", None, None, 64, 1), ("bf16", None, None, 64, 8),
+              ("bf16", None, None, 128, 2), ("bf16", None, None, 128, 6),
+              ("bf16", None, None, 256, 4), ("bf16", None, None, 256, 8),
+              ("f16", None, None, 64, 8), ("f16", None, None, 128, 4),
+              ("f16", None, None, 256, 6), ("fp8", 0.013, 0.009, 64, 2),
+              ("fp8", 0.013, 0.009, 128, 8), ("fp8", 0.013, 0.009, 256, 6)]
+
+
+@pytest.mark.parametrize("fmt,ks,vs,D,G", WALK_CASES)
+def test_workgroups_walk_several_tiles(fmt, ks, vs, D, G):
+    B, P = 8, 16384
+    cfg = mini(batch=B, head_dim=D, n_kv_heads=2, n_q_heads=2 * G,
+               level_windows=[4096, 0], prompt=[P] * B, max_ctx=P + 8, seed=34)
+    n_cus = torch.cuda.get_device_properties(0).multi_processor_count
+    tiles = B * ((4096 + 4 + 63) // 64 + (P + 1 + 63) // 64)
+    assert tiles >= 2 * 5 * n_cus, "the launch must give every workgroup several tiles"
+    log(f"walk {fmt} D={D} G={G}: {tiles} tiles")
+    r = Run(cfg, **fmt_args(fmt, ks, vs, 1, 2))
+    for b in range(B):
+        r.prefill(0, b)
+    for st in range(2):
+        qa, out = r.step(0, fused=bool(st))
+        r.check_out(0, qa, out, f"{fmt} D={D} G={G} step {st}")
+    r.check_layer(0)
+    r.free()
+
+
 def test_fp8_cache_rejects_prefill_attention():
     pol = hwkv.policy_set(1, 2, 8, 64, 4, [256, 0], [[0, 1]])
     cache = hwkv.cache_alloc(pol, 1, 400, kv_format="fp8")
