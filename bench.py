@@ -324,7 +324,9 @@ def decode_run(args, dev, one_core=True):
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "decode_split (split-K attention over one layer's resident K/V)",
+            "kernel": ("decode_mfma (split-K attention over one layer's resident fp8 K/V, "
+                       "products on the matrix cores)" if args.kv_format == "fp8" else
+                       "decode_split (split-K attention over one layer's resident K/V)"),
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
@@ -402,7 +404,8 @@ def suite(args, dev):
 
 
 def measured_traffic(args):
-    """HBM bytes per decode_split launch from the committed counter record
+    """HBM bytes per split launch (decode_split, or decode_mfma for fp8) from
+    the committed counter record
     (FETCH_SIZE + WRITE_SIZE, copy-calibrated), if it was taken on the current
     kernel source and on this workload; otherwise None."""
     if args.workload != "ctx112k" or args.unfused or args.paged:
@@ -420,7 +423,10 @@ def measured_traffic(args):
         return None, "counter record is stale: decode kernel source changed"
     from paper_2609_02029_amd import hwkv
     code = hwkv.KV_FORMATS[args.kv_format][0]
-    if not rec.get("kernel", "").endswith(f", {code}>"):
+    kern = rec.get("kernel", "")
+    ok = (kern.startswith("decode_mfma<") if args.kv_format == "fp8"
+          else kern.startswith("decode_split<") and kern.endswith(f", {code}>"))
+    if not ok:
         return None, "counter record is for another cache format"
     total = rec["fetch_bytes"] + rec["write_bytes"]
     return round(total), {"fetch_bytes": round(rec["fetch_bytes"]),

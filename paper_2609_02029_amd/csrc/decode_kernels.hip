@@ -179,9 +179,11 @@ struct CombineLaunch {
 }  // namespace
 
 int decode_workgroup_target(int fmt, int D, int G) {
-  // at most one workgroup per SIMD slot the register budget holds
-  const int want = fmt == HWKV_KV_FP8_E4M3 ? kDecodeWgPerCuX4Fp8 : kDecodeWgPerCuX4;
-  const int per_cu4 = std::min(want, 4 * split_waves_per_eu(D, G, fmt));
+  // at most one workgroup per SIMD slot the register budget holds (the fp8
+  // kernel, on the matrix cores, holds two waves per SIMD)
+  const int per_cu4 = fmt == HWKV_KV_FP8_E4M3
+                          ? std::min(kDecodeWgPerCuX4, 8)
+                          : std::min(kDecodeWgPerCuX4, 4 * split_waves_per_eu(D, G, fmt));
   return std::max(1, per_cu4 * device_cus() / 4);
 }
 int decode_combine_blocks_per_item(int D, int G) {

@@ -1,6 +1,8 @@
 // decode_split.h -- split phase of the decode attention over per-head grouped
-// caches (gfx950, wave64, VALU), templated on the cache format; instantiated
-// once per format by decode_split_<format>.hip.
+// caches (gfx950, wave64, VALU) for the 16-bit cache formats, bf16 and
+// binary16; instantiated once per format by decode_split_<format>.hip.  fp8
+// caches take the matrix-core kernel of decode_mfma.h (included below, it
+// shares this file's work decomposition, helpers and launcher).
 //
 // What is computed (paper: Eqs. conditional-attention-weight and
 // conditional-attention, exact scaled dot-product logit): for every sequence b
@@ -20,17 +22,14 @@
 // the same tile (split_body below).  The G query heads of an item share every
 // K/V byte read.
 //
-// Inside a wave, per tile (one stream of chunk-sized buffer loads per lane
-// -- 16 bytes, or 8 for fp8 -- with PF loads always in flight, running on
-// into the next tile):
+// Inside a wave, per tile (one stream of 16-byte buffer loads per lane with
+// PF loads always in flight, running on into the next tile):
 //   q.k   one lane per slot: the K tile is stored slot-minor in 8-element
 //         channel chunks, so chunk g of the tile is contiguous and lane t
 //         reads its own slot's chunk; q is uniform and comes through scalar
 //         loads.  bf16 keys: v_dot2_f32_bf16 multiplies bf16 pairs (q as an
-//         SGPR operand) with fp32 accumulate; fp8 keys are first widened to
-//         bf16 pairs (exact: every E4M3 value is a bf16 value) and take the
-//         same path, with the K scale folded into the logit scale; binary16
-//         keys meet q staged in LDS as binary16 (each head under a power of
+//         SGPR operand) with fp32 accumulate; binary16 keys meet q staged in
+//         LDS as binary16 (each head under a power of
 //         two that keeps every component within 2^31 of its largest exact)
 //         in v_dot2_f32_f16.  Each wave covers a quarter of the channels;
 //         the quarters are summed through LDS.
@@ -38,11 +37,8 @@
 //         one DPP row reduction plus four lane reads per head.
 //   p.v   lanes own 8 channels of one row (V row-major, a wave reads whole
 //         rows contiguously); p is broadcast through a per-wave LDS slice.
-//         bf16 and binary16 values are widened to fp32 (exactly) and take
-//         one fp32 FMA per (row, channel, head) with the fp32 weights; fp8
-//         values go over pairs of rows in binary16 (v_dot2_f32_f16, the
-//         weights rounded to binary16, the normaliser in fp32), and the fp8
-//         V scale multiplies the workgroup's result.
+//         The values are widened to fp32 (exactly) and take one fp32 FMA per
+//         (row, channel, head) with the fp32 weights.
 //         The V buffer descriptor of a tile ends at row n_valid, so rows
 //         past it read as zero (and their p is zero).
 // The fused append writes the new token, in the cache format, into its slot
@@ -79,9 +75,6 @@ __device__ __forceinline__ void static_for(F &&f) {
 #ifndef HWKV_DECODE_PREFETCH
 #define HWKV_DECODE_PREFETCH 4     // 16-byte chunk loads in flight
 #endif
-#ifndef HWKV_DECODE_PREFETCH8
-#define HWKV_DECODE_PREFETCH8 8    // 8-byte (fp8) chunk loads in flight
-#endif
 #ifndef HWKV_DECODE_AUX
 #define HWKV_DECODE_AUX 2  // cache-policy bits of the streaming loads (nt)
 #endif
@@ -90,7 +83,6 @@ __device__ __forceinline__ void static_for(F &&f) {
 #endif
 constexpr int kWaves = kDecodeWaves;             // waves per workgroup
 constexpr int kPrefetch = HWKV_DECODE_PREFETCH;  // 16-byte loads in flight
-constexpr int kPrefetch8 = HWKV_DECODE_PREFETCH8;  // 8-byte loads in flight
 // VGPR budget: four waves per SIMD (four workgroups per CU); eight q heads
 // per KV head (64 value accumulators per lane), and six with binary16 keys
 // at head_dim 256, need the budget of three
@@ -168,29 +160,16 @@ __device__ __forceinline__ uint32_t fp8x2_bf16x2(uint32_t w) {
                             __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, HI));
 }
 
-// fp8 codes 2i, 2i + 1 of a word as one binary16 pair (exact: every E4M3
-// value is a binary16 value), low code first.
-template <bool HI>
-__device__ __forceinline__ f16x2_t fp8x2_f16x2(uint32_t w) {
-  return __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w, 1.0f, HI);
-}
 
-// The 8 elements of a V chunk widened to fp32 (exact for every format).
+// The 8 elements of a V chunk widened to fp32 (exact).
 template <int F>
 __device__ __forceinline__ void widen8(typename KvFormat<F>::Chunk x, float (&vf)[8]) {
   if constexpr (F == HWKV_KV_BF16) {
     vf[0] = bf_lo(x.x); vf[1] = bf_hi(x.x); vf[2] = bf_lo(x.y); vf[3] = bf_hi(x.y);
     vf[4] = bf_lo(x.z); vf[5] = bf_hi(x.z); vf[6] = bf_lo(x.w); vf[7] = bf_hi(x.w);
-  } else if constexpr (F == HWKV_KV_F16) {
+  } else {
     vf[0] = h_lo(x.x); vf[1] = h_hi(x.x); vf[2] = h_lo(x.y); vf[3] = h_hi(x.y);
     vf[4] = h_lo(x.z); vf[5] = h_hi(x.z); vf[6] = h_lo(x.w); vf[7] = h_hi(x.w);
-  } else {
-    const f32x2_t a0 = __builtin_amdgcn_cvt_pk_f32_fp8(x.x, false);
-    const f32x2_t a1 = __builtin_amdgcn_cvt_pk_f32_fp8(x.x, true);
-    const f32x2_t a2 = __builtin_amdgcn_cvt_pk_f32_fp8(x.y, false);
-    const f32x2_t a3 = __builtin_amdgcn_cvt_pk_f32_fp8(x.y, true);
-    vf[0] = a0.x; vf[1] = a0.y; vf[2] = a1.x; vf[3] = a1.y;
-    vf[4] = a2.x; vf[5] = a2.y; vf[6] = a3.x; vf[7] = a3.y;
   }
 }
 
@@ -301,14 +280,9 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
   // mod PF, the same in every tile
   constexpr int PF = PFW < PIECES ? PFW : PIECES;
   constexpr int PST = SplitSmem<D, G, F>::PST;
-  // fp8 values: p.v over pairs of a wave's V steps with v_dot2_f32_f16 --
-  // steps 4(2i) + w and 4(2i + 1) + w read rows r and r + 4 RPS of the same
-  // channels, whose codes widen exactly to binary16 pairs; the weights enter
-  // the product rounded to binary16 (the normaliser keeps the fp32 weights)
-  constexpr bool PAIR = F == HWKV_KV_FP8_E4M3;
   static_assert(NC % kWaves == 0, "the four waves share a tile's chunks");
   static_assert(PIECES % PF == 0, "ring slots repeat from tile to tile");
-  static_assert(!PAIR || NCW % 2 == 0, "fp8 p.v takes a wave's V steps in pairs");
+  static_assert(F == HWKV_KV_BF16 || F == HWKV_KV_F16, "16-bit formats (fp8: decode_mfma)");
   __shared__ SplitSmem<D, G, F> sm;
 
   const DecodeItems &it = a.it;
@@ -541,10 +515,9 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
   }
-  // logit scale (base 2), with the fp8 K scale folded in; binary16 keys: the
-  // scale of each head the wave owns, with its q shift taken back
-  const float zscale =
-      F == HWKV_KV_FP8_E4M3 ? a.scale_log2 * it.k_scale[item] : a.scale_log2;
+  // logit scale (base 2); binary16 keys: the scale of each head the wave
+  // owns, with its q shift taken back
+  const float zscale = a.scale_log2;
   float zsc[OWN];
 #pragma unroll
   for (int o = 0; o < OWN; ++o) {
@@ -620,16 +593,6 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
           s[h] = dot2(qc[h].z, x.z, s[h]);
           s[h] = dot2(qc[h].w, x.w, s[h]);
         }
-      } else if constexpr (F == HWKV_KV_FP8_E4M3) {
-        const uint32_t k0 = fp8x2_bf16x2<false>(x.x), k1 = fp8x2_bf16x2<true>(x.x);
-        const uint32_t k2 = fp8x2_bf16x2<false>(x.y), k3 = fp8x2_bf16x2<true>(x.y);
-#pragma unroll
-        for (int h = 0; h < G; ++h) {
-          s[h] = dot2(qc[h].x, k0, s[h]);
-          s[h] = dot2(qc[h].y, k1, s[h]);
-          s[h] = dot2(qc[h].z, k2, s[h]);
-          s[h] = dot2(qc[h].w, k3, s[h]);
-        }
       } else {
         // binary16 keys: q chunk (kWaves q + wave) of head h from LDS (one
         // address for every lane: a broadcast read).  The 16-byte vectors are
@@ -667,12 +630,6 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
 
     // ---- online softmax, base 2, of the heads this wave owns
     const bool valid = 64 * tp + lane < nv;
-    // fp8: the binary16 weights go in pair order: slot t is row t % RPS of
-    // V step st = t / RPS, which is step i = st / 4 of wave st % 4 -- half
-    // i % 2 of that wave's pair i / 2
-    const int st = lane / RPS;
-    const int ppid = ((st % kWaves) * (NCW / 2) + st / (2 * kWaves)) * RPS + lane % RPS;
-    const int phalf = (st / kWaves) & 1;
 #pragma unroll
     for (int o = 0; o < OWN; ++o) {
       const int h = wave + kWaves * o;
@@ -690,10 +647,7 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
         }
         const float p = exp2f(z - mnew);
         l[o] += p;
-        if constexpr (PAIR)
-          reinterpret_cast<_Float16 *>(pl)[2 * (ppid * G + h) + phalf] = (_Float16)p;
-        else
-          pl[lane * PST + h] = p;
+        pl[lane * PST + h] = p;
         if (lane == 0) sm.alpha[h] = alpha;
       }
     }
@@ -710,77 +664,38 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
     }
 
     // ---- p.v over the wave's V steps (rows (4i + w) RPS + rsub)
-    if constexpr (PAIR) {
-      const uint32_t *pp = reinterpret_cast<const uint32_t *>(pl);
-      uint32_t pw[G];
-      Chunk xp;
-      static_for<NCW>([&](auto jc) {
-        constexpr int i = decltype(jc)::value;
-        constexpr int q = NCW + i;
+    // p of a step's row is read from LDS one step ahead (pc: this step,
+    // pn: the next), so the LDS latency overlaps a step of work
+    float pc[G];
+#pragma unroll
+    for (int h = 0; h < G; ++h) pc[h] = pl[(wave * RPS + rsub) * PST + h];
+    static_for<NCW>([&](auto jc) {
+      constexpr int i = decltype(jc)::value;
+      constexpr int q = NCW + i;
+#pragma unroll
+      for (int h = 0; h < G; ++h)
+#pragma unroll
+        for (int e = 0; e < 8; e += 2)
+          asm volatile("" : "+v"(acc[h][e]), "+v"(acc[h][e + 1]));
+      const Chunk x = buf[q % PF];
+      issue(std::integral_constant<int, q>{});
+      float pn[G];
+      if constexpr (i + 1 < NCW) {
 #pragma unroll
         for (int h = 0; h < G; ++h)
+          pn[h] = pl[((kWaves * (i + 1) + wave) * RPS + rsub) * PST + h];
+      }
+      float vf[8];
+      widen8<F>(x, vf);
 #pragma unroll
-          for (int e = 0; e < 8; e += 2)
-            asm volatile("" : "+v"(acc[h][e]), "+v"(acc[h][e + 1]));
-        const Chunk x = buf[q % PF];
-        issue(std::integral_constant<int, q>{});
-        if constexpr (i % 2 == 0) {
-          xp = x;
+      for (int h = 0; h < G; ++h)
 #pragma unroll
-          for (int h = 0; h < G; ++h)
-            pw[h] = pp[((wave * (NCW / 2) + i / 2) * RPS + rsub) * G + h];
-        } else {
-          const uint32_t w0 = __builtin_amdgcn_perm(x.x, xp.x, 0x05010400u);
-          const uint32_t w1 = __builtin_amdgcn_perm(x.x, xp.x, 0x07030602u);
-          const uint32_t w2 = __builtin_amdgcn_perm(x.y, xp.y, 0x05010400u);
-          const uint32_t w3 = __builtin_amdgcn_perm(x.y, xp.y, 0x07030602u);
-          const f16x2_t v[8] = {fp8x2_f16x2<false>(w0), fp8x2_f16x2<true>(w0),
-                                fp8x2_f16x2<false>(w1), fp8x2_f16x2<true>(w1),
-                                fp8x2_f16x2<false>(w2), fp8x2_f16x2<true>(w2),
-                                fp8x2_f16x2<false>(w3), fp8x2_f16x2<true>(w3)};
+        for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pc[h], vf[e], acc[h][e]);
+      if constexpr (i + 1 < NCW) {
 #pragma unroll
-          for (int h = 0; h < G; ++h) {
-            const f16x2_t ph = __builtin_bit_cast(f16x2_t, pw[h]);
-#pragma unroll
-            for (int e = 0; e < 8; ++e)
-              acc[h][e] = __builtin_amdgcn_fdot2(ph, v[e], acc[h][e], false);
-          }
-        }
-      });
-    } else {
-      // p of a step's row is read from LDS one step ahead (pc: this step,
-      // pn: the next), so the LDS latency overlaps a step of work
-      float pc[G];
-#pragma unroll
-      for (int h = 0; h < G; ++h) pc[h] = pl[(wave * RPS + rsub) * PST + h];
-      static_for<NCW>([&](auto jc) {
-        constexpr int i = decltype(jc)::value;
-        constexpr int q = NCW + i;
-#pragma unroll
-        for (int h = 0; h < G; ++h)
-#pragma unroll
-          for (int e = 0; e < 8; e += 2)
-            asm volatile("" : "+v"(acc[h][e]), "+v"(acc[h][e + 1]));
-        const Chunk x = buf[q % PF];
-        issue(std::integral_constant<int, q>{});
-        float pn[G];
-        if constexpr (i + 1 < NCW) {
-#pragma unroll
-          for (int h = 0; h < G; ++h)
-            pn[h] = pl[((kWaves * (i + 1) + wave) * RPS + rsub) * PST + h];
-        }
-        float vf[8];
-        widen8<F>(x, vf);
-#pragma unroll
-        for (int h = 0; h < G; ++h)
-#pragma unroll
-          for (int e = 0; e < 8; ++e) acc[h][e] = fmaf(pc[h], vf[e], acc[h][e]);
-        if constexpr (i + 1 < NCW) {
-#pragma unroll
-          for (int h = 0; h < G; ++h) pc[h] = pn[h];
-        }
-      });
-    }
+        for (int h = 0; h < G; ++h) pc[h] = pn[h];
+      }
+    });
     if (!has_next) break;
     t = tn;
     tp = tnp;
@@ -831,7 +746,6 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
   __syncthreads();
 
   const int pidx = it.ws_split0 + blk;   // this workgroup's partial
-  const float vsc = F == HWKV_KV_FP8_E4M3 ? it.v_scale[item] : 1.0f;
   for (int idx = threadIdx.x; idx < G * D / 4; idx += kWaves * 64) {
     const int h = idx / (D / 4), c = (idx % (D / 4)) * 4;
     float4 A = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -842,12 +756,6 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
       A.y += x.y;
       A.z += x.z;
       A.w += x.w;
-    }
-    if constexpr (F == HWKV_KV_FP8_E4M3) {  // the V scale of the codes
-      A.x *= vsc;
-      A.y *= vsc;
-      A.z *= vsc;
-      A.w *= vsc;
     }
     const float L = sm.l[h];
     // streaming (non-temporal) stores: nothing here is read again by this
@@ -870,7 +778,7 @@ __device__ __forceinline__ void split_body(const DecodeArgs &a) {
 
 
 template <int F>
-constexpr int kSplitDepth = KvFormat<F>::kBytes == 2 ? kPrefetch : kPrefetch8;
+constexpr int kSplitDepth = kPrefetch;
 
 template <int D, int G, int F>
 __global__ __launch_bounds__(kWaves * 64)
@@ -914,14 +822,27 @@ hipError_t dispatch_dg(int D, int G, Args &&...args) {
 #undef HWKV_G
 }
 
+}  // namespace
+}  // namespace hwkv
+
+#include "decode_mfma.h"
+
+namespace hwkv {
+namespace {
+
 template <int F>
 struct SplitLaunch {
   template <int D, int G>
   struct At {
     static hipError_t run(const DecodeArgs &a, int n, hipStream_t s, hipEvent_t e0,
                           hipEvent_t e1) {
-      hipExtLaunchKernelGGL((decode_split<D, G, F>), dim3(n), dim3(kWaves * 64), 0,
-                            s, e0, e1, 0, a);
+      // fp8 caches on the matrix cores (decode_mfma.h), 16-bit ones on VALU
+      if constexpr (F == HWKV_KV_FP8_E4M3)
+        hipExtLaunchKernelGGL((decode_mfma<D, G>), dim3(n), dim3(kWaves * 64), 0, s, e0,
+                              e1, 0, a);
+      else
+        hipExtLaunchKernelGGL((decode_split<D, G, F>), dim3(n), dim3(kWaves * 64), 0,
+                              s, e0, e1, 0, a);
       return hipGetLastError();
     }
   };

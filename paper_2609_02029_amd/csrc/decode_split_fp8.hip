@@ -1,5 +1,5 @@
-// decode_split_fp8.hip -- decode split kernels for fp8-e4m3 caches (all head
-// dims and group sizes).
+// decode_split_fp8.hip -- decode split kernels for fp8-E4M3 caches (the
+// matrix-core kernel of decode_mfma.h; all head dims and group sizes).
 #include "decode_split.h"
 
 namespace hwkv {

@@ -35,16 +35,11 @@ constexpr int kDecodeWaves = 4;  // waves of a decode split workgroup
 #ifndef HWKV_DECODE_WG_PER_CU_X4
 #define HWKV_DECODE_WG_PER_CU_X4 8
 #endif
-#ifndef HWKV_DECODE_WG_PER_CU_X4_FP8
-#define HWKV_DECODE_WG_PER_CU_X4_FP8 12
-#endif
 // Decode split workgroups a launch aims at, in quarters per CU: the host
 // picks the tiles per workgroup so that the launch has about this many
-// workgroups (at most as many as the kernel's register budget holds at once).
-// Two per CU for the 16-bit formats; three for fp8, whose split kernel spends
-// more VALU work per byte and hides it better with a third wave per SIMD.
+// workgroups (at most as many as the kernel's register budget holds at once):
+// two per CU.
 constexpr int kDecodeWgPerCuX4 = HWKV_DECODE_WG_PER_CU_X4;
-constexpr int kDecodeWgPerCuX4Fp8 = HWKV_DECODE_WG_PER_CU_X4_FP8;
 
 // Decode work of one launch: items are (sequence b, kv head h) pairs of one
 // layer; item i owns rows [0, n_valid[i]) of its unit and the launch's split

@@ -8,7 +8,7 @@
     (expected: MIB MiB read and MIB MiB written per copy).
 ``python -m paper_2609_02029_amd.profiling record DB_FETCH DB_WRITE MIB [KERNEL]``
     the head_dim-256 line of one kernel in the traffic table as JSON
-    (``decode_split`` by default, or ``prefill_attn``), with the hash of the
+    (``decode_split`` by default, ``decode_mfma`` or ``prefill_attn``), with the hash of the
     kernel source it was measured on
 ``python -m paper_2609_02029_amd.profiling mfma DB``
     MFMA busy fraction and bf16 MFMA FLOP per dispatch of every kernel that
@@ -33,8 +33,8 @@ import sqlite3
 import statistics
 import sys
 
-KERNELS = (r"(decode_split<[^>]*>|decode_split_deep<[^>]*>|decode_combine<[^>]*>|prefill_write<[^>]*>|append_token<[^>]*>"
-           r"|prefill_attn<[^>]*>)")
+KERNELS = (r"(decode_split<[^>]*>|decode_mfma<[^>]*>|decode_combine<[^>]*>|prefill_write<[^>]*>"
+           r"|append_token<[^>]*>|prefill_attn<[^>]*>)")
 N_SIMD = 1024   # 256 CUs x 4 SIMDs
 N_CU = 256
 # GRBM_GUI_ACTIVE comes back as one value per dispatch that sums the active
@@ -45,9 +45,7 @@ N_XCD = 8
 def short(name):
     m = re.search(KERNELS, name or "")
     if m:
-        # the split phase at either load depth is one row: decode_split_deep
-        # serves the launches with fewer split workgroups than CUs
-        return m.group(1).replace("decode_split_deep<", "decode_split<")
+        return m.group(1)
     if "copyBuffer" in (name or ""):  # the runtime's blit kernel (torch copy_)
         return "copy:" + (name or "")[:60]
     return (name or "")[:60]
@@ -131,6 +129,7 @@ def traffic(db_fetch, db_write, mib):
 # source files of each profiled kernel (the split kernel's template and the
 # format helpers it inlines)
 SOURCES = {"decode_split<": ["decode_split.h", "kv_format.h"],
+           "decode_mfma<": ["decode_mfma.h", "decode_split.h", "kv_format.h"],
            "prefill_attn<": ["prefill_attn_kernels.hip"]}
 
 

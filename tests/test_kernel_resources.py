@@ -73,8 +73,9 @@ def kernel_table(tmp_path_factory):
 
 
 def test_every_hot_kernel_is_present(kernel_table):
-    for name in ["decode_split<256, 6, 0>", "decode_split<256, 6, 2>", "decode_split<256, 6, 1>",
-                 "decode_split<256, 8, 0>", "decode_split<64, 1, 0>",
+    for name in ["decode_split<256, 6, 0>", "decode_mfma<256, 6>", "decode_split<256, 6, 1>",
+                 "decode_split<256, 8, 0>", "decode_split<64, 1, 0>", "decode_mfma<64, 1>",
+                 "decode_mfma<128, 8>",
                  "prefill_attn<256, 8, 0>", "prefill_attn<128, 8, 0>", "prefill_attn<64, 8, 0>",
                  "prefill_attn<256, 8, 1>", "prefill_attn<128, 8, 1>", "prefill_attn<64, 8, 1>",
                  "replay_attn<256, 8>", "replay_merge<256>", "prefill_write<256, 0>",
@@ -91,10 +92,10 @@ def test_no_scratch_spills(kernel_table):
 def test_register_budgets(kernel_table):
     # decode splits: four waves per SIMD (128 registers), three (168) for 8 q
     # heads per kv head, whose 64 value accumulators per lane do not fit 128,
-    # and for 6 with binary16 keys at head_dim 256;
-    # prefill attention: two waves of eight per SIMD (256)
+    # and for 6 with binary16 keys at head_dim 256; the fp8 matrix-core split
+    # and prefill attention: two waves per SIMD (256)
     for n, (vg, _) in kernel_table.items():
-        if n.startswith("prefill_attn<"):
+        if n.startswith("prefill_attn<") or n.startswith("decode_mfma<"):
             assert vg <= 256, (n, vg)
         if n.startswith("decode_split<"):
             d, g, _f = (int(x) for x in n[n.index("<") + 1:-1].split(","))
