@@ -336,7 +336,9 @@ int hwkv_decode_workspace_bytes(const hwkv_cache *cache, size_t *bytes);
  * state.  Fp32 accumulation; the result does not depend on the slot order.
  * Keys and values enter with their stored values: for fp8, q.k is taken over
  * the decoded codes and multiplied by the K scale, and the output by the V
- * scale; for binary16, q enters q.k as binary16 after a power-of-two scaling
+ * scale, and the softmax weights enter the value product as two bf16 terms
+ * (round(p) and round(p - round(p))), which carry each weight to 2^-18 of
+ * itself; for binary16, q enters q.k as binary16 after a power-of-two scaling
  * per query head, exact for every component within a factor 2^31 of the
  * head's largest |q| (the products are exact, the sums fp32). */
 int hwkv_decode_attn(hwkv_cache *cache, int32_t layer, const void *q,
