@@ -85,6 +85,12 @@ typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
 typedef __attribute__((address_space(3))) void lds_void_t;
 
 constexpr int kKeys = 32;                  // keys per tile
+// Operand reads from LDS issued ahead of the products (sched_group_barrier
+// masks: matrix-core instructions, LDS reads)
+constexpr int kPipeK = 4;                  // K operands (one 16-byte read each)
+constexpr int kPipeV = 3;                  // V operands (two 8-byte reads each)
+constexpr int kSchedMfma = 0x008;
+constexpr int kSchedDsRead = 0x100;
 
 __device__ __forceinline__ u32x4_t ld16(const uint16_t *p) {
   return *reinterpret_cast<const u32x4_t *>(p);
@@ -361,10 +367,23 @@ void prefill_attn(const PrefillAttnArgs a) {
     f32x16_t st;
 #pragma unroll
     for (int r = 0; r < 16; ++r) st[r] = 0.0f;
+    {
+      u32x4_t kx[KS];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const u32x4_t kx = *reinterpret_cast<const u32x4_t *>(kl + ks * 1024);
-      st = mfma16<F16>(kx, qv[ks], st);
+      for (int ks = 0; ks < KS; ++ks) kx[ks] = *reinterpret_cast<const u32x4_t *>(kl + ks * 1024);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) st = mfma16<F16>(kx[ks], qv[ks], st);
+      // K operand reads run kPipeK products ahead of their use (left to
+      // itself the scheduler reads each operand just before its product and
+      // waits out the LDS latency every time)
+      constexpr int PK = kPipeK < KS ? kPipeK : KS;
+      __builtin_amdgcn_sched_group_barrier(kSchedDsRead, PK, 0);
+#pragma unroll
+      for (int i = 0; i < KS - PK; ++i) {
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(kSchedMfma, PK, 0);
     }
     const bool full_vis = s0 + kKeys <= se && slast <= t_lo &&
                           (W == 0 || slast < S || s0 >= t_hi + 1 - W);
@@ -427,6 +446,17 @@ void prefill_attn(const PrefillAttnArgs a) {
             u32x4_t, __builtin_shufflevector(v2[0], v2[1], 0, 1, 2, 3, 4, 5, 6, 7));
         o[db] = mfma16<F16>(va, pb[s], o[db]);
       }
+    }
+    // V operand reads (two per product) run kPipeV products ahead
+    {
+      constexpr int PV = kPipeV < 2 * DB ? kPipeV : 2 * DB;
+      __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2 * PV, 1);
+#pragma unroll
+      for (int i = 0; i < 2 * DB - PV; ++i) {
+        __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 1);
+        __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 1);
+      }
+      __builtin_amdgcn_sched_group_barrier(kSchedMfma, PV, 1);
     }
   }
 
