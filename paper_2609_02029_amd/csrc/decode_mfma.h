@@ -20,8 +20,8 @@
 //               channels): lane (g, c) reads the codes of channel 16 vb + c in
 //               rows 4g .. 4g + 3 of the wave's rows from LDS and widens them.
 //               The weights go in as two bf16 terms, hi = round(p) and lo =
-//               round(p - hi), which carry p to ~2^-16 of itself, with fp32
-//               accumulation.
+//               round(p - hi), which carry p to within 2^-18 of itself, with
+//               fp32 accumulation.
 // A wave's 16 V rows go from global memory straight into its own LDS area
 // (buffer_load ... lds); K goes into registers.  The next tile's loads are
 // issued as soon as this tile's K and V have been read, and run during its
@@ -285,7 +285,7 @@ void decode_mfma(DecodeArgs a) {
       p[i] = exp2f(z[i] - m);
       lsum += p[i];
     }
-    // the weights as hi + lo 16-bit terms
+    // the weights as hi + lo bf16 terms
     u32x2_t ph, pl;
     ph.x = pack_bf16x2(p[0], p[1]);
     ph.y = pack_bf16x2(p[2], p[3]);
