@@ -393,10 +393,12 @@ def suite(args, dev):
                                            cpu_seconds=2.0), dev, one_core=False))
     add("batch16_paged", lambda: decode_run(opts(workload="batch16", steps=30, warmup=2,
                                                  paged=True, no_cpu_baseline=True), dev))
-    add("ctx112k_fp8", lambda: decode_run(opts(workload="ctx112k", kv_format="fp8", steps=30,
-                                               warmup=4, no_cpu_baseline=True), dev))
-    add("ctx112k_f16", lambda: decode_run(opts(workload="ctx112k", kv_format="f16", steps=30,
-                                               warmup=4, no_cpu_baseline=True), dev))
+    # the headline's steps and warmup: with fewer, the first of the three
+    # intervals has not reached the steady state and the median shows it
+    add("ctx112k_fp8", lambda: decode_run(opts(workload="ctx112k", kv_format="fp8", steps=60,
+                                               warmup=8, no_cpu_baseline=True), dev))
+    add("ctx112k_f16", lambda: decode_run(opts(workload="ctx112k", kv_format="f16", steps=60,
+                                               warmup=8, no_cpu_baseline=True), dev))
     add("prefill128k", lambda: prefill_run(opts(workload="prefill128k", steps=3, warmup=1,
                                                 cpu_seconds=8.0), dev))
     head["configs"] = configs
