@@ -1,6 +1,6 @@
 """Build the oracle's shared library (plain C, gcc, fp64, no fast-math).
 
-Test infrastructure: the oracle is the checker, never part of the product
+Test infrastructure: the oracle is what the tests compare against, never part of the product
 path.  ``build()`` compiles it every time it is called.
 """
 import os
