@@ -92,87 +92,126 @@ __global__ __launch_bounds__(256) void calib_means(const CalibArgs a) {
     a.means[(size_t)k * hkv + h] = ((part[0] + part[1]) + (part[2] + part[3])) / (float)n;
 }
 
-// Merge of the one-pass replay: one wavefront per (candidate k, column c),
-// lanes over channels.  Candidate k < K of column c (row position t) holds
-// the sinks and the keys s >= e = t + 1 - w_k; e <= S means every key, as the
-// full candidate (k = K) does.  Its parts: the sinks' partial; the partial of
-// split j (keys [j T, (j + 1) T), T = 32 tiles_per_split) when all of the
-// split's keys are >= e (e <= max(j T, S)); the window's edge partial when e
-// lies inside split j (max(j T, S) < e < (j + 1) T); nothing from splits at
-// or above e otherwise.  out = sum acc 2^((m - M) c) / sum l 2^((m - M) c),
-// M = max m over the parts with l > 0 (m in logit units, c = scale log2 e).
+// Merge of the one-pass replay: one wavefront per column c, lanes over
+// channels, every candidate in one walk over the column's split partials.
+// Candidate k < K of column c (row position t) holds the sinks and the keys
+// s >= e = t + 1 - w_k; e <= S means every key, as the full candidate (k = K)
+// does.  Its parts: the sinks' partial; the partial of split j (keys
+// [j T, (j + 1) T), T = 32 tiles_per_split) when all of the split's keys are
+// >= e, i.e. j >= j_k with j_k = e / T + (e > (e / T) T) (0 for e <= S); the
+// window's edge partial when e lies inside split e / T.  The windows ascend,
+// so j_k does not increase with k: walking the splits from the top down with
+// a running (M, L, acc) over splits [j, n_splits), candidate k is complete
+// when the walk has added split j_k, and takes the running state, its edge
+// partial and the sinks.  out = sum acc 2^((m - M) c) / sum l 2^((m - M) c),
+// M = max m over the parts with l > 0 (m in logit units, c = scale log2 e);
+// the running state carries its own shift and is rescaled as it rises.
 template <int D>
 __global__ __launch_bounds__(256) void replay_merge(const ReplayMergeArgs a) {
   constexpr int PER = D / 64;
-  const int wid = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int col = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int K = a.n_windows;
-  if (wid >= (K + 1) * a.n_cols) return;           // uniform per wave
-  const int k = wid / a.n_cols, col = wid - k * a.n_cols;
+  if (col >= a.n_cols) return;                     // uniform per wave
   const int h = (col % a.n_q_heads) / a.group;     // the column's kv head
   const int t = a.rows[col / a.n_q_heads];
   const int S = a.n_sinks;
   const int T = 32 * a.tiles_per_split;
-  const int e = k < K ? t + 1 - a.windows[k] : INT_MIN;
-  const bool all = e <= S;
-  const int je = all ? -1 : e / T;                 // the split holding the edge
-  const bool edge_part = !all && e > je * T;       // else split je lies inside
   const float c2 = a.scale_log2 * a.k_scale[h];
+  const float vs = a.v_scale[h];
   const size_t stride = (size_t)a.n_cols * (D + 4);
   const float *pc = a.part + (size_t)col * (D + 4);
-  float *orow = a.outs + ((size_t)k * a.n_cols + col) * D;
-  // the splits whose keys all lie in the candidate: every split for the full
-  // candidate, else those above the edge split (split je too when the edge
-  // is its first key)
-  const int j_begin = all ? 0 : (edge_part ? je + 1 : je);
-  float em = -1e30f, el = 0.0f;
-  if (edge_part) {
-    const float2 ml = *reinterpret_cast<const float2 *>(a.win_ml + ((size_t)k * a.n_cols + col) * 2);
-    em = ml.x;
-    el = ml.y;
-  }
-  const float *ps = pc + (size_t)a.n_splits * stride;   // the sinks' partial
+  // the sinks' partial
+  const float *ps = pc + (size_t)a.n_splits * stride;
   const bool sinks = S > 0 && ps[1] > 0.0f;
-  float M = -1e30f;
-  if (sinks) M = ps[0];
-  if (el > 0.0f) M = fmaxf(M, em);
-  for (int j = j_begin; j < a.n_splits; ++j) {
-    const float *pj = pc + (size_t)j * stride;
-    if (pj[1] > 0.0f) M = fmaxf(M, pj[0]);
-  }
-  float L = 0.f, acc[PER];
+  float sm = -1e30f, sl = 0.0f, sacc[PER];
 #pragma unroll
-  for (int i = 0; i < PER; ++i) acc[i] = 0.f;
-  if (el > 0.0f) {
-    const float f = __builtin_amdgcn_exp2f((em - M) * c2);
-    L += el * f;
-#pragma unroll
-    for (int i = 0; i < PER; ++i) acc[i] += orow[lane + 64 * i] * f;
-  }
+  for (int i = 0; i < PER; ++i) sacc[i] = 0.0f;
   if (sinks) {
-    const float f = __builtin_amdgcn_exp2f((ps[0] - M) * c2);
-    L += ps[1] * f;
+    sm = ps[0];
+    sl = ps[1];
 #pragma unroll
-    for (int i = 0; i < PER; ++i) acc[i] += ps[4 + lane + 64 * i] * f;
+    for (int i = 0; i < PER; ++i) sacc[i] = ps[4 + lane + 64 * i];
   }
-  for (int j = j_begin; j < a.n_splits; ++j) {
+  // the first split of candidate k's own keys
+  auto first_split = [&](int k) -> int {
+    const int e = t + 1 - a.windows[k];
+    if (e <= S) return 0;
+    const int je = e / T;
+    return e > je * T ? je + 1 : je;
+  };
+  // running state over the splits added so far
+  float M = -1e30f, L = 0.0f, acc[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) acc[i] = 0.0f;
+  // candidate k (K: the full one) from the running state, its edge partial
+  // (k < K and the edge inside a split) and the sinks
+  auto finish = [&](int k) {
+    float *orow = a.outs + ((size_t)k * a.n_cols + col) * D;
+    float em = -1e30f, el = 0.0f, eacc[PER];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) eacc[i] = 0.0f;
+    if (k < K) {
+      const int e = t + 1 - a.windows[k];
+      if (e > S && e > (e / T) * T) {
+        const float2 ml =
+            *reinterpret_cast<const float2 *>(a.win_ml + ((size_t)k * a.n_cols + col) * 2);
+        em = ml.x;
+        el = ml.y;
+        if (el > 0.0f) {
+#pragma unroll
+          for (int i = 0; i < PER; ++i) eacc[i] = orow[lane + 64 * i];
+        }
+      }
+    }
+    float Mx = -1e30f;
+    if (L > 0.0f) Mx = M;
+    if (el > 0.0f) Mx = fmaxf(Mx, em);
+    if (sinks) Mx = fmaxf(Mx, sm);
+    const float fr = L > 0.0f ? __builtin_amdgcn_exp2f((M - Mx) * c2) : 0.0f;
+    const float fe = el > 0.0f ? __builtin_amdgcn_exp2f((em - Mx) * c2) : 0.0f;
+    const float fs = sinks ? __builtin_amdgcn_exp2f((sm - Mx) * c2) : 0.0f;
+    const float inv = vs / (L * fr + el * fe + sl * fs);
+#pragma unroll
+    for (int i = 0; i < PER; ++i)
+      orow[lane + 64 * i] = (acc[i] * fr + eacc[i] * fe + sacc[i] * fs) * inv;
+  };
+  int k = 0;                                       // the next candidate to finish
+  // split j's partial, loaded one split ahead of its use
+  float nm = 0.0f, nl = 0.0f, nacc[PER];
+  auto load = [&](int j) {
     const float *pj = pc + (size_t)j * stride;
-    const float lj = pj[1];
-    if (!(lj > 0.0f)) continue;                    // uniform: empty split
-    const float f = __builtin_amdgcn_exp2f((pj[0] - M) * c2);
-    L += lj * f;
+    nm = pj[0];
+    nl = pj[1];
 #pragma unroll
-    for (int i = 0; i < PER; ++i) acc[i] += pj[4 + lane + 64 * i] * f;
+    for (int i = 0; i < PER; ++i) nacc[i] = pj[4 + lane + 64 * i];
+  };
+  if (a.n_splits > 0) load(a.n_splits - 1);
+  for (int j = a.n_splits - 1; j >= 0; --j) {
+    while (k < K && first_split(k) > j) finish(k++);   // complete before split j
+    const float m = nm, l = nl;
+    float x[PER];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) x[i] = nacc[i];
+    if (j > 0) load(j - 1);
+    if (l > 0.0f) {                                // uniform: empty splits add nothing
+      const float Mn = fmaxf(M, m);
+      const float f0 = L > 0.0f ? __builtin_amdgcn_exp2f((M - Mn) * c2) : 0.0f;
+      const float f1 = __builtin_amdgcn_exp2f((m - Mn) * c2);
+      L = L * f0 + l * f1;
+#pragma unroll
+      for (int i = 0; i < PER; ++i) acc[i] = acc[i] * f0 + x[i] * f1;
+      M = Mn;
+    }
   }
-  const float inv = a.v_scale[h] / L;
-#pragma unroll
-  for (int i = 0; i < PER; ++i) orow[lane + 64 * i] = acc[i] * inv;
+  while (k < K) finish(k++);                       // the candidates holding every split
+  finish(K);
 }
 
 }  // namespace
 
 hipError_t launch_replay_merge(int D, const ReplayMergeArgs &a, hipStream_t s) {
-  const dim3 grid((unsigned)(((size_t)(a.n_windows + 1) * a.n_cols + 3) / 4)), block(256);
+  const dim3 grid((unsigned)(((size_t)a.n_cols + 3) / 4)), block(256);
   switch (D) {
     case 64: hipLaunchKernelGGL(replay_merge<64>, grid, block, 0, s, a); break;
     case 128: hipLaunchKernelGGL(replay_merge<128>, grid, block, 0, s, a); break;
